@@ -1,0 +1,238 @@
+"""Seeded synthetic inputs for the BASE decode hot path.
+
+This module only draws random inputs. It holds none of the method's
+arithmetic: no routing, no expert evaluation, no prediction, no selection.
+Both the CPU oracle (``oracle/``) and the HIP path (``paper_2609_36222_amd``)
+take their inputs from here, and neither imports the other.
+
+The paper evaluates on real checkpoints (Qwen3-30B-A3B, DeepSeek-V2-Lite,
+Qwen1.5-MoE-A2.7B) with FineWeb-Edu calibration text (Sec. 4 setup;
+App. A "Calibration Details").  None of that is available here, so every
+input is synthetic with the shapes of those models' MoE layers:
+
+* hidden states: i.i.d. N(0,1) rows passed through RMSNorm (unit gain,
+  eps 1e-6), computed in fp32 and stored bf16 (fp32 for the tiny layer);
+* the batch-256 Qwen3-shaped layer mixes 128 rows drawn around 4 shared
+  Gaussian centres (centre + 0.1 N(0,I)) with 128 i.i.d. rows, interleaved
+  by a seeded shuffle, to vary the size of the batch union;
+* router weights N(0, 0.075) with a per-expert bias log(p_e), p_e
+  proportional to rank^-1.1 over a seeded permutation (a Zipf(1.1)
+  popularity law; with this scale a Qwen3-shaped router at batch 16 gives a
+  mean top-1 union near the 13.34 experts the paper reports in App. F);
+* SwiGLU expert weights with std 1/sqrt(fan_in), stored bf16;
+* a synthetic linear predictor (a_u, b_u) for the large layers (the tiny
+  layer's predictor is fitted by the oracle on its calibration tokens).
+
+bf16 tensors are returned as ``uint16`` bit patterns (round-to-nearest-even
+from the fp32 draw).  Generation is chunked over child seeds so the values
+do not depend on the number of threads used.
+"""
+from __future__ import annotations
+
+import concurrent.futures as _cf
+import dataclasses
+import os
+
+import numpy as np
+
+SEED_ROOT = 2609
+
+# stream ids inside a layer's seed sequence
+_S_ROUTER, _S_BIAS, _S_CALIB, _S_EXPERT, _S_TOKENS, _S_PRED = 0, 1, 2, 3, 4, 5
+
+
+@dataclasses.dataclass(frozen=True)
+class LayerShape:
+    name: str
+    index: int          # position in the workload table (enters the seed)
+    d: int              # hidden size
+    E: int              # routed experts
+    K: int              # experts per token (top-K)
+    I: int              # SwiGLU intermediate size
+    B: int              # decode batch (one token per sequence)
+    budgets: tuple      # expert budgets B_e evaluated on this layer
+    bf16: bool          # bf16 activations and expert weights (else fp32)
+    layers: int = 1     # stacked MoE layers (residual carried)
+    clustered: bool = False
+    router_std: float = 0.075
+    bias_kind: str = "zipf"   # "zipf" or "normal"
+    bias_std: float = 0.5
+    rmsnorm: bool = True
+    calib_tokens: int = 8192
+
+
+WORKLOADS = {
+    # d=256, E=16, top-2, I=512, batch 8, B_e=6, everything fp32,
+    # router N(0,0.02) plus bias N(0,0.5), experts N(0,1/sqrt(d)),
+    # predictor fitted on 2048 calibration tokens.
+    "tiny": LayerShape("tiny", 0, 256, 16, 2, 512, 8, (6,), False,
+                       router_std=0.02, bias_kind="normal", rmsnorm=False,
+                       calib_tokens=2048),
+    # OLMoE-shaped: d=2048, E=64, top-8, I=1024, batch 32.
+    "olmoe": LayerShape("olmoe", 1, 2048, 64, 8, 1024, 32, (16, 32), True),
+    # Qwen3-30B-A3B-shaped layer at batch 64.
+    "qwen3_b64": LayerShape("qwen3_b64", 2, 2048, 128, 8, 768, 64,
+                            (16, 32, 64), True),
+    # Same layer at batch 256, half the batch clustered.
+    "qwen3_b256": LayerShape("qwen3_b256", 3, 2048, 128, 8, 768, 256,
+                             (32, 64, 128), True, clustered=True),
+    # 48 stacked Qwen3-shaped MoE layers, batch 128, B_e=24 per layer.
+    "qwen3_stack48": LayerShape("qwen3_stack48", 4, 2048, 128, 8, 768, 128,
+                                (24,), True, layers=48),
+    # Mixtral-shaped: few large experts.
+    "mixtral": LayerShape("mixtral", 5, 4096, 8, 2, 14336, 128, (4,), True),
+}
+
+
+def seed_seq(shape: LayerShape, layer: int, stream: int, data_seed: int = 0):
+    return np.random.SeedSequence([SEED_ROOT, shape.index, layer, stream,
+                                   data_seed])
+
+
+def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Round fp32 values to bf16 (nearest, ties to even); return uint16 bits."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    u = a.view(np.uint32).astype(np.uint64)
+    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return rounded.astype(np.uint16)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    """Exact widening of bf16 bit patterns to fp32."""
+    return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32)
+            << 16).view(np.float32)
+
+
+def _normal_chunked(ss: np.random.SeedSequence, n: int, std: float,
+                    chunk: int = 1 << 22) -> np.ndarray:
+    """n draws of N(0, std^2) in fp32, chunk i from child seed i."""
+    out = np.empty(n, dtype=np.float32)
+    nchunks = max(1, (n + chunk - 1) // chunk)
+    children = ss.spawn(nchunks)
+
+    def fill(i):
+        lo, hi = i * chunk, min(n, (i + 1) * chunk)
+        g = np.random.Generator(np.random.PCG64(children[i]))
+        g.standard_normal(hi - lo, dtype=np.float32, out=out[lo:hi])
+        if std != 1.0:
+            out[lo:hi] *= np.float32(std)
+
+    workers = min(16, os.cpu_count() or 1, nchunks)
+    if workers <= 1:
+        for i in range(nchunks):
+            fill(i)
+    else:
+        with _cf.ThreadPoolExecutor(workers) as ex:
+            list(ex.map(fill, range(nchunks)))
+    return out
+
+
+def _rmsnorm_rows(z: np.ndarray, eps: float = 1e-6) -> np.ndarray:
+    """RMSNorm with unit gain, in fp32 (part of the input recipe)."""
+    z = z.astype(np.float32)
+    ms = np.mean(z.astype(np.float64) ** 2, axis=1, keepdims=True)
+    return (z / np.sqrt(ms + eps)).astype(np.float32)
+
+
+def hidden_states(shape: LayerShape, n: int, layer: int = 0,
+                  stream: int = _S_TOKENS, data_seed: int = 0,
+                  clustered=None) -> np.ndarray:
+    """n hidden-state rows [n, d] as fp32 values (bf16-representable when
+    the layer is bf16)."""
+    ss = seed_seq(shape, layer, stream, data_seed)
+    g = np.random.Generator(np.random.PCG64(ss))
+    d = shape.d
+    clustered = shape.clustered if clustered is None else clustered
+    z = g.standard_normal((n, d), dtype=np.float32)
+    if clustered and n >= 2:
+        nc = n // 2
+        centres = g.standard_normal((4, d), dtype=np.float32)
+        cid = g.integers(0, 4, size=nc)
+        zc = centres[cid] + np.float32(0.1) * g.standard_normal(
+            (nc, d), dtype=np.float32)
+        z[:nc] = zc
+        z = z[g.permutation(n)]
+    if shape.rmsnorm:
+        z = _rmsnorm_rows(z)
+    if shape.bf16:
+        z = bf16_bits_to_f32(f32_to_bf16_bits(z))
+    return np.ascontiguousarray(z, dtype=np.float32)
+
+
+def router(shape: LayerShape, layer: int = 0):
+    """Router weight [E, d] fp32 and bias [E] fp32."""
+    g = np.random.Generator(np.random.PCG64(seed_seq(shape, layer, _S_ROUTER)))
+    w = (g.standard_normal((shape.E, shape.d), dtype=np.float32)
+         * np.float32(shape.router_std))
+    gb = np.random.Generator(np.random.PCG64(seed_seq(shape, layer, _S_BIAS)))
+    if shape.bias_kind == "zipf":
+        perm = gb.permutation(shape.E)
+        rank = np.empty(shape.E, dtype=np.float64)
+        rank[perm] = np.arange(1, shape.E + 1, dtype=np.float64)
+        p = rank ** -1.1
+        p /= p.sum()
+        b = np.log(p).astype(np.float32)
+    else:
+        b = gb.standard_normal(shape.E, dtype=np.float32) * np.float32(
+            shape.bias_std)
+    return np.ascontiguousarray(w), np.ascontiguousarray(b)
+
+
+def experts(shape: LayerShape, layer: int = 0):
+    """SwiGLU expert weights.
+
+    Returns (w13, w2): w13 [E, 2I, d] (rows 0..I-1 gate, I..2I-1 up),
+    w2 [E, d, I].  uint16 bf16 bits for bf16 layers, fp32 otherwise.
+    Tiny layer: all three matrices std 1/sqrt(d).  Others: std 1/sqrt(fan_in).
+    """
+    E, d, I = shape.E, shape.d, shape.I
+    ss = seed_seq(shape, layer, _S_EXPERT)
+    s13, s2 = ss.spawn(2)
+    std13 = 1.0 / np.sqrt(d)
+    std2 = 1.0 / np.sqrt(d) if not shape.bf16 else 1.0 / np.sqrt(I)
+    w13 = _normal_chunked(s13, E * 2 * I * d, std13).reshape(E, 2 * I, d)
+    w2 = _normal_chunked(s2, E * d * I, std2).reshape(E, d, I)
+    if shape.bf16:
+        return f32_to_bf16_bits(w13), f32_to_bf16_bits(w2)
+    return w13, w2
+
+
+def synthetic_predictor(shape: LayerShape, layer: int = 0):
+    """A synthetic log-energy predictor (a [E,d] fp32, b [E] fp32).
+
+    Stands in for a calibrated one on the large layers: a_u has i.i.d.
+    N(0, (0.3)^2) entries, so a_u.z_bar varies with std 0.3 over unit
+    vectors; b_u = log(d * 0.18) + N(0, 0.25^2), roughly the log output
+    energy of a random SwiGLU expert with this module's weight scales.
+    """
+    g = np.random.Generator(np.random.PCG64(seed_seq(shape, layer, _S_PRED)))
+    a = g.standard_normal((shape.E, shape.d), dtype=np.float32) * np.float32(0.3)
+    b = (np.float32(np.log(shape.d * 0.18))
+         + g.standard_normal(shape.E, dtype=np.float32) * np.float32(0.25))
+    return np.ascontiguousarray(a), np.ascontiguousarray(b.astype(np.float32))
+
+
+def calibration_tokens(shape: LayerShape, layer: int = 0, n=None):
+    n = shape.calib_tokens if n is None else n
+    return hidden_states(shape, n, layer=layer, stream=_S_CALIB,
+                         clustered=False)
+
+
+def decode_tokens(shape: LayerShape, layer: int = 0, data_seed: int = 0,
+                  B=None):
+    return hidden_states(shape, shape.B if B is None else B, layer=layer,
+                         stream=_S_TOKENS, data_seed=data_seed)
+
+
+def layer_inputs(name: str, layer: int = 0, data_seed: int = 0,
+                 with_experts: bool = True, B=None):
+    """Everything one decode layer consumes, as numpy arrays."""
+    shape = WORKLOADS[name]
+    wr, br = router(shape, layer)
+    out = dict(shape=shape, x=decode_tokens(shape, layer, data_seed, B),
+               w_router=wr, b_router=br)
+    pa, pb = synthetic_predictor(shape, layer)
+    out["pred_a"], out["pred_b"] = pa, pb
+    if with_experts:
+        out["w13"], out["w2"] = experts(shape, layer)
+    return out
