@@ -1,0 +1,206 @@
+/*
+ * base.h -- C ABI of an MI355X (gfx950) implementation of the decode hot path
+ * of BASE (Batch-Aware Selection of Experts using predicted removal error).
+ *
+ * One MoE layer, one decode step, batch B (one token per active sequence):
+ *
+ *   route          l = x W_r^T + beta, top-K, router weights      (Sec. 3.1)
+ *   predict_cost   c(t,u) = w^2 exp(a_u . x/||x|| + b_u)   (Sec. 3.4, eq.
+ *                  log_energy_predictor; App. "Custom GPU Kernels")
+ *   select         D_hat_u = sum_t c(t,u); keep the budget experts with the
+ *                  largest D_hat among the batch union             (Sec. 3.4)
+ *   moe_forward    backfill each token onto the kept set, compact tokens by
+ *                  expert, grouped SwiGLU FFN over the kept experts only,
+ *                  gate-weighted combine                     (Sec. 3.5, 3.1)
+ *   decode_layer   all of the above in one call
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Pointers named in a base_layer and every array argument are DEVICE
+ *   pointers; `L`, `plan_out` and the return values are host memory.
+ * - `stream` is a hipStream_t (NULL = the null stream).  Every call only
+ *   enqueues work on it: no allocation, no host synchronisation, no
+ *   device-to-host copy.  Outputs are valid once the stream reaches them.
+ * - The caller owns every buffer.  Calls that need scratch memory take a
+ *   workspace `ws` of at least base_workspace_bytes(L, B, budget) bytes.
+ * - Validation happens on the host before anything is enqueued; on any
+ *   error the call returns a negative base_status and leaves every output
+ *   untouched.  A failed launch returns BASE_ERR_HIP.
+ * - Input values are not checked (NaN/Inf give unspecified results).
+ * - Integer outputs (ids, selected set, executed experts, compaction) and
+ *   every fp32 value of the scoring path are bit-deterministic and follow
+ *   one fixed fp32 operation order: dot products of length d use 64 partial
+ *   sums (partial j owns elements 256m + 4j + r, accumulated in ascending
+ *   order with single-rounding FMA) joined by a halving tree; batch scores
+ *   sum 64-token chunks by the same tree and chunks in ascending order;
+ *   exp is a fixed Cody-Waite + degree-7 polynomial sequence; division and
+ *   square root are correctly rounded.  The FFN output is deterministic
+ *   run to run.
+ * - Ties: wherever experts are ranked by a float key, equal keys are
+ *   ordered by the lower expert index.
+ *
+ * Limits (else BASE_ERR_SHAPE): 1 <= B <= 1024; d a multiple of 256 with
+ * d <= 16384; 1 <= K <= 16; K <= E <= 256; I a multiple of 64 with
+ * I <= 32768.  budget >= 1 (else BASE_ERR_BUDGET); a budget above E is
+ * clamped to E.
+ */
+#ifndef BASE_MI355X_BASE_H
+#define BASE_MI355X_BASE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BASE_OK = 0,
+    BASE_ERR_NULL = -1,       /* a required pointer is NULL */
+    BASE_ERR_SHAPE = -2,      /* B, d, E, K or I outside the limits above */
+    BASE_ERR_BUDGET = -3,     /* budget < 1 */
+    BASE_ERR_DTYPE = -4,      /* unknown dtype */
+    BASE_ERR_ALIGN = -5,      /* misaligned pointer (see base_layer) */
+    BASE_ERR_WORKSPACE = -6,  /* workspace smaller than base_workspace_bytes */
+    BASE_ERR_HIP = -7,        /* a HIP launch failed */
+    BASE_ERR_FLAGS = -8       /* unknown bits in flags */
+} base_status;
+
+/* Element type of x, y, residual and the expert weights w13, w2.  Router
+ * and predictor parameters are always fp32. */
+typedef enum { BASE_F32 = 0, BASE_BF16 = 1 } base_dtype;
+
+/* flags of base_moe_forward / base_decode_layer */
+enum {
+    /* Gate of an executed expert v of token t: its original router score
+     * exp(l_v - l_max) over the router's own denominator (the original
+     * top-K sum), also for backfilled experts (Sec. 3.5).  Default. */
+    BASE_GATE_PAPER = 0,
+    /* ... or renormalised over the experts the token executes. */
+    BASE_GATE_RENORM = 1,
+    /* A token executes its K highest-ranked experts inside the kept set,
+     * backfilling unavailable routes (Sec. 3.5).  Default. */
+    BASE_FILL_BACKFILL = 0,
+    /* ... or only its routed experts that were kept (fill-rule ablation,
+     * Sec. 4, Table fill_rule_ablation). */
+    BASE_FILL_DROP = 2
+};
+
+/* One MoE layer.  Host struct holding device pointers. */
+typedef struct base_layer {
+    int32_t d;          /* hidden size */
+    int32_t E;          /* routed experts */
+    int32_t K;          /* experts per token (router top-K) */
+    int32_t I;          /* SwiGLU intermediate size */
+    int32_t dtype;      /* base_dtype of x, y, residual, w13, w2 */
+    int32_t norm_topk;  /* 1: w = p / sum_{top-K} p ; 0: w = softmax p */
+    const float *w_router;  /* [E][d] fp32, 16-B aligned */
+    const float *b_router;  /* [E] fp32 router bias, or NULL */
+    const float *pred_a;    /* [E][d] fp32 predictor slopes a_u, 16-B aligned */
+    const float *pred_b;    /* [E] fp32 predictor intercepts b_u (bias
+                               correction folded in, App. A) */
+    const void *w13;        /* [E][2I][d]: rows 0..I-1 gate, I..2I-1 up;
+                               16-B aligned */
+    const void *w2;         /* [E][d][I] down projection; 16-B aligned */
+} base_layer;
+
+/* Device pointers into the caller's workspace, filled by base_moe_forward
+ * and base_decode_layer when plan_out != NULL.  Arrays not produced by the
+ * call are set to NULL.  Valid until the workspace is reused. */
+typedef struct base_plan {
+    /* produced by base_decode_layer only */
+    float   *logits;          /* [B][E] */
+    int32_t *topk_ids;        /* [B][K] */
+    float   *topk_w;          /* [B][K] */
+    float   *cost;            /* [B][K] */
+    float   *scores;          /* [E] */
+    int32_t *counts;          /* [E] */
+    int32_t *sel_ids;         /* [budget] */
+    int32_t *n_sel;           /* [1] */
+    int32_t *slot_of_expert;  /* [E] */
+    /* produced by both */
+    int32_t *exec_ids;        /* [B][K] expert executed at rank j, -1 padded */
+    float   *exec_gates;      /* [B][K] its gate, 0 padded */
+    int32_t *offsets;         /* [budget+1] first pair of each slot; the
+                                 entries from n_sel on equal the pair count */
+    int32_t *pair_tok;        /* [B*K] token of pair p (pairs sorted by
+                                 (slot, token)) */
+    float   *pair_gate;       /* [B*K] gate of pair p */
+    int32_t *pair_of;         /* [B][K] pair index of (t, j), -1 if none */
+} base_plan;
+
+/* Bytes of workspace base_moe_forward / base_decode_layer need for this
+ * layer, batch and budget (0 if the shape is invalid).  The workspace must
+ * be 256-byte aligned. */
+size_t base_workspace_bytes(const base_layer *L, int32_t B, int32_t budget);
+
+/* Router (Sec. 3.1; App. "Custom GPU Kernels": the routing stage provides
+ * z_t, R_t and w_{t,u}).
+ *   x         [B][d] (L->dtype), 16-B aligned
+ *   logits    [B][E] fp32 out: l = x . W_r[e] + beta_e
+ *   topk_ids  [B][K] int32 out: R_t, ordered by (logit desc, index asc)
+ *   topk_w    [B][K] fp32 out: exp(l_u - l_max) / S, S = sum over R_t
+ *             (norm_topk = 1) or over all E experts (norm_topk = 0) */
+base_status base_route(const base_layer *L, const void *x, int32_t B,
+                       float *logits, int32_t *topk_ids, float *topk_w,
+                       void *stream);
+
+/* Predicted removal cost of every routed pair (Sec. 3.4, eq.
+ * log_energy_predictor): z_bar = x / ||x|| (0 if x = 0),
+ * s_hat = a_u . z_bar + b_u, cost = w^2 exp(s_hat).
+ *   topk_ids, topk_w  [B][K] as produced by base_route
+ *   cost              [B][K] fp32 out */
+base_status base_predict_cost(const base_layer *L, const void *x, int32_t B,
+                              const int32_t *topk_ids, const float *topk_w,
+                              float *cost, void *stream);
+
+/* Batch aggregation and budgeted selection (Sec. 3.4; Sec. 3.5 "loads the M
+ * experts with the largest scores").
+ *   scores          [E] fp32 out: D_hat_u = sum of cost over tokens routing u
+ *   counts          [E] int32 out: number of tokens routing u
+ *   sel_ids         [budget] int32 out: the kept experts in rank order
+ *                   (D_hat desc, index asc) among experts with count > 0;
+ *                   -1 beyond n_sel
+ *   n_sel           [1] int32 out: min(budget, |batch union|)
+ *   slot_of_expert  [E] int32 out: rank of u in sel_ids, or -1 */
+base_status base_select(const base_layer *L, int32_t B,
+                        const int32_t *topk_ids, const float *cost,
+                        int32_t budget, float *scores, int32_t *counts,
+                        int32_t *sel_ids, int32_t *n_sel,
+                        int32_t *slot_of_expert, void *stream);
+
+/* Re-routing onto the kept set and the restricted MoE (Sec. 3.5; Sec. 3.1):
+ * backfill (or drop) per token, gates per `flags`, compaction of the
+ * executed (token, expert) pairs by kept slot, grouped SwiGLU FFN over the
+ * kept experts only -- each kept expert's weights are read once -- and
+ *   y_t = residual_t + sum_j gate_{t,j} E_{X_t[j]}(x_t)   (j ascending).
+ *   logits, topk_ids          from base_route
+ *   sel_ids, n_sel, slot_of_expert   from base_select (same budget)
+ *   residual  [B][d] (L->dtype) or NULL
+ *   y         [B][d] (L->dtype) out, 16-B aligned; may not alias x
+ *   plan_out  host struct, may be NULL
+ *   ws        workspace, ws_bytes >= base_workspace_bytes(L, B, budget) */
+base_status base_moe_forward(const base_layer *L, const void *x, int32_t B,
+                             const float *logits, const int32_t *topk_ids,
+                             const int32_t *sel_ids, const int32_t *n_sel,
+                             const int32_t *slot_of_expert, int32_t budget,
+                             int32_t flags, const void *residual, void *y,
+                             base_plan *plan_out, void *ws, size_t ws_bytes,
+                             void *stream);
+
+/* The whole layer in one call: route, predict, select and moe_forward.
+ * Every intermediate lives in the workspace (reported through plan_out)
+ * and equals, bit for bit, what the staged calls produce. */
+base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
+                              int32_t budget, int32_t flags,
+                              const void *residual, void *y,
+                              base_plan *plan_out, void *ws, size_t ws_bytes,
+                              void *stream);
+
+/* Static description of a status code. */
+const char *base_status_string(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BASE_MI355X_BASE_H */

@@ -1,0 +1,190 @@
+"""ctypes binding of libbase.so (the C ABI in include/base.h).
+
+Argument marshalling only: torch tensors in, raw device pointers and sizes
+out, the caller's current HIP stream, and a Python exception for a negative
+status.  Every step of the computation runs in the library's HIP kernels.
+The library must be built (``paper_2609_36222_amd.build``); loading fails
+loudly otherwise -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "_lib", "libbase.so")
+
+BASE_F32, BASE_BF16 = 0, 1
+GATE_PAPER, GATE_RENORM = 0, 1
+FILL_BACKFILL, FILL_DROP = 0, 2
+
+EXPORTS = ("base_workspace_bytes", "base_route", "base_predict_cost",
+           "base_select", "base_moe_forward", "base_decode_layer",
+           "base_status_string")
+
+_vp = ctypes.c_void_p
+_i32 = ctypes.c_int32
+
+
+class base_layer(ctypes.Structure):
+    _fields_ = [("d", _i32), ("E", _i32), ("K", _i32), ("I", _i32),
+                ("dtype", _i32), ("norm_topk", _i32),
+                ("w_router", _vp), ("b_router", _vp), ("pred_a", _vp),
+                ("pred_b", _vp), ("w13", _vp), ("w2", _vp)]
+
+
+_PLAN_FIELDS = ["logits", "topk_ids", "topk_w", "cost", "scores", "counts",
+                "sel_ids", "n_sel", "slot_of_expert", "exec_ids", "exec_gates",
+                "offsets", "pair_tok", "pair_gate", "pair_of"]
+
+
+class base_plan(ctypes.Structure):
+    _fields_ = [(f, _vp) for f in _PLAN_FIELDS]
+
+
+class BaseError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{msg} (status {status})")
+        self.status = status
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libbase.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(
+            f"{path} is missing: build it with "
+            "`python -m paper_2609_36222_amd.build` (no CPU fallback exists)")
+    L = ctypes.CDLL(path)
+    L.base_workspace_bytes.restype = ctypes.c_size_t
+    L.base_workspace_bytes.argtypes = [ctypes.POINTER(base_layer), _i32, _i32]
+    L.base_route.restype = _i32
+    L.base_route.argtypes = [ctypes.POINTER(base_layer), _vp, _i32, _vp, _vp,
+                             _vp, _vp]
+    L.base_predict_cost.restype = _i32
+    L.base_predict_cost.argtypes = [ctypes.POINTER(base_layer), _vp, _i32,
+                                    _vp, _vp, _vp, _vp]
+    L.base_select.restype = _i32
+    L.base_select.argtypes = [ctypes.POINTER(base_layer), _i32, _vp, _vp,
+                              _i32, _vp, _vp, _vp, _vp, _vp, _vp]
+    L.base_moe_forward.restype = _i32
+    L.base_moe_forward.argtypes = [ctypes.POINTER(base_layer), _vp, _i32, _vp,
+                                   _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
+                                   ctypes.POINTER(base_plan), _vp,
+                                   ctypes.c_size_t, _vp]
+    L.base_decode_layer.restype = _i32
+    L.base_decode_layer.argtypes = [ctypes.POINTER(base_layer), _vp, _i32,
+                                    _i32, _i32, _vp, _vp,
+                                    ctypes.POINTER(base_plan), _vp,
+                                    ctypes.c_size_t, _vp]
+    L.base_status_string.restype = ctypes.c_char_p
+    L.base_status_string.argtypes = [_i32]
+    _lib = L
+    return L
+
+
+def status_string(status: int) -> str:
+    return load().base_status_string(int(status)).decode()
+
+
+def _check(status):
+    if status != 0:
+        raise BaseError(status, status_string(status))
+
+
+def _ptr(t):
+    """Device pointer of a tensor (None -> NULL)."""
+    if t is None:
+        return None
+    return t.data_ptr()
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+class Layer:
+    """One MoE layer: torch tensors plus the C descriptor pointing at them.
+
+    w_router, b_router, pred_a, pred_b: fp32; w13 [E,2I,d], w2 [E,d,I]:
+    fp32 or bf16 (the layer dtype, also the dtype of x and y)."""
+
+    def __init__(self, w_router, b_router, pred_a, pred_b, w13, w2,
+                 norm_topk: int = 1):
+        import torch
+        E, d = w_router.shape
+        I = w2.shape[2]
+        K = None
+        self.tensors = (w_router, b_router, pred_a, pred_b, w13, w2)
+        self.dtype = BASE_BF16 if w13.dtype == torch.bfloat16 else BASE_F32
+        self.torch_dtype = w13.dtype
+        self.d, self.E, self.I, self.K = d, E, I, K
+        self.norm_topk = norm_topk
+        self._desc = None
+
+    def desc(self, K: int) -> base_layer:
+        w_router, b_router, pred_a, pred_b, w13, w2 = self.tensors
+        return base_layer(self.d, self.E, K, self.I, self.dtype,
+                          self.norm_topk, _ptr(w_router), _ptr(b_router),
+                          _ptr(pred_a), _ptr(pred_b), _ptr(w13), _ptr(w2))
+
+
+def base_workspace_bytes(desc: base_layer, B: int, budget: int) -> int:
+    return int(load().base_workspace_bytes(ctypes.byref(desc), B, budget))
+
+
+def base_route(desc, x, B, logits, topk_ids, topk_w, stream=None):
+    _check(load().base_route(ctypes.byref(desc), _ptr(x), B, _ptr(logits),
+                             _ptr(topk_ids), _ptr(topk_w), _stream(stream)))
+
+
+def base_predict_cost(desc, x, B, topk_ids, topk_w, cost, stream=None):
+    _check(load().base_predict_cost(ctypes.byref(desc), _ptr(x), B,
+                                    _ptr(topk_ids), _ptr(topk_w), _ptr(cost),
+                                    _stream(stream)))
+
+
+def base_select(desc, B, topk_ids, cost, budget, scores, counts, sel_ids,
+                n_sel, slot_of_expert, stream=None):
+    _check(load().base_select(ctypes.byref(desc), B, _ptr(topk_ids),
+                              _ptr(cost), budget, _ptr(scores), _ptr(counts),
+                              _ptr(sel_ids), _ptr(n_sel),
+                              _ptr(slot_of_expert), _stream(stream)))
+
+
+def base_moe_forward(desc, x, B, logits, topk_ids, sel_ids, n_sel,
+                     slot_of_expert, budget, flags, residual, y, ws,
+                     plan=None, stream=None):
+    """Returns the filled base_plan (device pointers into ws)."""
+    plan = base_plan() if plan is None else plan
+    _check(load().base_moe_forward(
+        ctypes.byref(desc), _ptr(x), B, _ptr(logits), _ptr(topk_ids),
+        _ptr(sel_ids), _ptr(n_sel), _ptr(slot_of_expert), budget, flags,
+        _ptr(residual), _ptr(y), ctypes.byref(plan), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
+    return plan
+
+
+def base_decode_layer(desc, x, B, budget, flags, residual, y, ws, plan=None,
+                      stream=None):
+    """Returns the filled base_plan (device pointers into ws)."""
+    plan = base_plan() if plan is None else plan
+    _check(load().base_decode_layer(
+        ctypes.byref(desc), _ptr(x), B, budget, flags, _ptr(residual), _ptr(y),
+        ctypes.byref(plan), _ptr(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
+    return plan
+
+
+def plan_offset(plan: base_plan, field: str, ws) -> int:
+    """Byte offset of a plan array inside the workspace tensor."""
+    p = getattr(plan, field)
+    return None if p is None else p - ws.data_ptr()

@@ -1,0 +1,295 @@
+// C ABI of the BASE decode hot path: host-side validation, workspace
+// layout and the launch sequence of every call.  Nothing here touches device
+// memory; all work is enqueued on the caller's stream.
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/base.h"
+#include "internal.hpp"
+
+namespace {
+
+using namespace basek;
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+size_t elem_bytes(int32_t dtype) { return dtype == BASE_BF16 ? 2 : 4; }
+
+base_status check_layer(const base_layer *L, int32_t B, bool need_router,
+                        bool need_pred, bool need_experts) {
+  if (!L) return BASE_ERR_NULL;
+  if (L->dtype != BASE_F32 && L->dtype != BASE_BF16) return BASE_ERR_DTYPE;
+  if (B < 1 || B > MAX_B) return BASE_ERR_SHAPE;
+  if (L->d < 256 || L->d > 16384 || L->d % 256) return BASE_ERR_SHAPE;
+  if (L->K < 1 || L->K > MAX_K || L->E < L->K || L->E > MAX_E) return BASE_ERR_SHAPE;
+  if (L->I < 64 || L->I > 32768 || L->I % 64) return BASE_ERR_SHAPE;
+  if (L->norm_topk != 0 && L->norm_topk != 1) return BASE_ERR_SHAPE;
+  if (need_router) {
+    if (!L->w_router) return BASE_ERR_NULL;
+    if (!aligned(L->w_router, 16)) return BASE_ERR_ALIGN;
+    if (L->b_router && !aligned(L->b_router, 4)) return BASE_ERR_ALIGN;
+  }
+  if (need_pred) {
+    if (!L->pred_a || !L->pred_b) return BASE_ERR_NULL;
+    if (!aligned(L->pred_a, 16) || !aligned(L->pred_b, 4)) return BASE_ERR_ALIGN;
+  }
+  if (need_experts) {
+    if (!L->w13 || !L->w2) return BASE_ERR_NULL;
+    if (!aligned(L->w13, 16) || !aligned(L->w2, 16)) return BASE_ERR_ALIGN;
+  }
+  return BASE_OK;
+}
+
+base_status check_ptr(const void *p, size_t a) {
+  if (!p) return BASE_ERR_NULL;
+  return aligned(p, a) ? BASE_OK : BASE_ERR_ALIGN;
+}
+
+#define BASE_TRY(expr)                          \
+  do {                                          \
+    base_status _s = (expr);                    \
+    if (_s != BASE_OK) return _s;               \
+  } while (0)
+
+#define HIP_TRY(expr)                           \
+  do {                                          \
+    if ((expr) != hipSuccess) return BASE_ERR_HIP; \
+  } while (0)
+
+// Workspace layout: every array starts on a 256-byte boundary.
+struct Layout {
+  size_t logits, topk_ids, topk_w, cost, scores, counts, sel_ids, n_sel,
+      slot_of, exec_ids, exec_gates, offsets, pair_tok, pair_gate, pair_of,
+      H, pairbuf, total;
+};
+
+size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+Layout layout(const base_layer *L, int32_t B, int32_t bc) {
+  Layout o;
+  size_t at = 0;
+  auto take = [&](size_t bytes) {
+    size_t here = at;
+    at = up256(at + bytes);
+    return here;
+  };
+  const size_t BK = (size_t)B * L->K;
+  o.logits = take((size_t)B * L->E * 4);
+  o.topk_ids = take(BK * 4);
+  o.topk_w = take(BK * 4);
+  o.cost = take(BK * 4);
+  o.scores = take((size_t)L->E * 4);
+  o.counts = take((size_t)L->E * 4);
+  o.sel_ids = take((size_t)bc * 4);
+  o.n_sel = take(4);
+  o.slot_of = take((size_t)L->E * 4);
+  o.exec_ids = take(BK * 4);
+  o.exec_gates = take(BK * 4);
+  o.offsets = take(((size_t)bc + 1) * 4);
+  o.pair_tok = take(BK * 4);
+  o.pair_gate = take(BK * 4);
+  o.pair_of = take(BK * 4);
+  o.H = take(BK * L->I * elem_bytes(L->dtype));
+  o.pairbuf = take(BK * L->d * 4);
+  o.total = at;
+  return o;
+}
+
+template <typename T>
+T *at(void *ws, size_t off) {
+  return reinterpret_cast<T *>(static_cast<char *>(ws) + off);
+}
+
+// backfill + compaction + FFN + combine, on plan arrays already in place
+base_status run_forward(const base_layer *L, const void *x, int32_t B,
+                        const float *logits, const int32_t *ids,
+                        const int32_t *sel_ids, const int32_t *n_sel,
+                        const int32_t *slot_of, int32_t bc, int32_t flags,
+                        const void *residual, void *y, void *ws,
+                        const Layout &o, hipStream_t st) {
+  const bool bf16 = L->dtype == BASE_BF16;
+  int32_t *exec_ids = at<int32_t>(ws, o.exec_ids);
+  float *exec_gates = at<float>(ws, o.exec_gates);
+  int32_t *offsets = at<int32_t>(ws, o.offsets);
+  int32_t *pair_tok = at<int32_t>(ws, o.pair_tok);
+  float *pair_gate = at<float>(ws, o.pair_gate);
+  int32_t *pair_of = at<int32_t>(ws, o.pair_of);
+  HIP_TRY(launch_backfill(B, L->E, L->K, L->norm_topk, flags, logits, ids,
+                          slot_of, n_sel, exec_ids, exec_gates, st));
+  HIP_TRY(launch_compact(B, L->K, bc, exec_ids, exec_gates, slot_of, n_sel,
+                         offsets, pair_tok, pair_gate, pair_of, st));
+  HIP_TRY(launch_ffn(bf16, x, B, L->d, L->I, L->K, L->E, bc, L->w13, L->w2, sel_ids,
+                     n_sel, offsets, pair_tok, pair_gate, at<void>(ws, o.H),
+                     at<float>(ws, o.pairbuf), st));
+  HIP_TRY(launch_combine(bf16, B, L->d, L->K, pair_of, at<float>(ws, o.pairbuf),
+                         residual, y, st));
+  return BASE_OK;
+}
+
+void fill_plan(base_plan *P, void *ws, const Layout &o, bool full) {
+  if (!P) return;
+  P->logits = full ? at<float>(ws, o.logits) : nullptr;
+  P->topk_ids = full ? at<int32_t>(ws, o.topk_ids) : nullptr;
+  P->topk_w = full ? at<float>(ws, o.topk_w) : nullptr;
+  P->cost = full ? at<float>(ws, o.cost) : nullptr;
+  P->scores = full ? at<float>(ws, o.scores) : nullptr;
+  P->counts = full ? at<int32_t>(ws, o.counts) : nullptr;
+  P->sel_ids = full ? at<int32_t>(ws, o.sel_ids) : nullptr;
+  P->n_sel = full ? at<int32_t>(ws, o.n_sel) : nullptr;
+  P->slot_of_expert = full ? at<int32_t>(ws, o.slot_of) : nullptr;
+  P->exec_ids = at<int32_t>(ws, o.exec_ids);
+  P->exec_gates = at<float>(ws, o.exec_gates);
+  P->offsets = at<int32_t>(ws, o.offsets);
+  P->pair_tok = at<int32_t>(ws, o.pair_tok);
+  P->pair_gate = at<float>(ws, o.pair_gate);
+  P->pair_of = at<int32_t>(ws, o.pair_of);
+}
+
+base_status check_ws(const base_layer *L, int32_t B, int32_t bc, void *ws,
+                     size_t ws_bytes) {
+  if (!ws) return BASE_ERR_NULL;
+  if (!aligned(ws, 256)) return BASE_ERR_ALIGN;
+  if (ws_bytes < layout(L, B, bc).total) return BASE_ERR_WORKSPACE;
+  return BASE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t base_workspace_bytes(const base_layer *L, int32_t B, int32_t budget) {
+  if (check_layer(L, B, false, false, false) != BASE_OK || budget < 1) return 0;
+  return layout(L, B, budget < L->E ? budget : L->E).total;
+}
+
+base_status base_route(const base_layer *L, const void *x, int32_t B,
+                       float *logits, int32_t *topk_ids, float *topk_w,
+                       void *stream) {
+  BASE_TRY(check_layer(L, B, true, false, false));
+  BASE_TRY(check_ptr(x, 16));
+  BASE_TRY(check_ptr(logits, 4));
+  BASE_TRY(check_ptr(topk_ids, 4));
+  BASE_TRY(check_ptr(topk_w, 4));
+  hipStream_t st = (hipStream_t)stream;
+  const bool bf16 = L->dtype == BASE_BF16;
+  HIP_TRY(launch_route_logits(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
+                              logits, st));
+  HIP_TRY(launch_token(bf16, x, B, L->d, L->E, L->K, L->norm_topk, logits,
+                       topk_ids, topk_w, nullptr, nullptr, nullptr, 1, st));
+  return BASE_OK;
+}
+
+base_status base_predict_cost(const base_layer *L, const void *x, int32_t B,
+                              const int32_t *topk_ids, const float *topk_w,
+                              float *cost, void *stream) {
+  BASE_TRY(check_layer(L, B, false, true, false));
+  BASE_TRY(check_ptr(x, 16));
+  BASE_TRY(check_ptr(topk_ids, 4));
+  BASE_TRY(check_ptr(topk_w, 4));
+  BASE_TRY(check_ptr(cost, 4));
+  HIP_TRY(launch_token(L->dtype == BASE_BF16, x, B, L->d, L->E, L->K,
+                       L->norm_topk, nullptr, const_cast<int32_t *>(topk_ids),
+                       const_cast<float *>(topk_w), L->pred_a, L->pred_b, cost,
+                       2, (hipStream_t)stream));
+  return BASE_OK;
+}
+
+base_status base_select(const base_layer *L, int32_t B, const int32_t *topk_ids,
+                        const float *cost, int32_t budget, float *scores,
+                        int32_t *counts, int32_t *sel_ids, int32_t *n_sel,
+                        int32_t *slot_of_expert, void *stream) {
+  BASE_TRY(check_layer(L, B, false, false, false));
+  if (budget < 1) return BASE_ERR_BUDGET;
+  BASE_TRY(check_ptr(topk_ids, 4));
+  BASE_TRY(check_ptr(cost, 4));
+  BASE_TRY(check_ptr(scores, 4));
+  BASE_TRY(check_ptr(counts, 4));
+  BASE_TRY(check_ptr(sel_ids, 4));
+  BASE_TRY(check_ptr(n_sel, 4));
+  BASE_TRY(check_ptr(slot_of_expert, 4));
+  const int32_t bc = budget < L->E ? budget : L->E;
+  HIP_TRY(launch_select(B, L->K, L->E, topk_ids, cost, bc, scores, counts,
+                        sel_ids, n_sel, slot_of_expert, (hipStream_t)stream));
+  return BASE_OK;
+}
+
+base_status base_moe_forward(const base_layer *L, const void *x, int32_t B,
+                             const float *logits, const int32_t *topk_ids,
+                             const int32_t *sel_ids, const int32_t *n_sel,
+                             const int32_t *slot_of_expert, int32_t budget,
+                             int32_t flags, const void *residual, void *y,
+                             base_plan *plan_out, void *ws, size_t ws_bytes,
+                             void *stream) {
+  BASE_TRY(check_layer(L, B, false, false, true));
+  if (budget < 1) return BASE_ERR_BUDGET;
+  if (flags & ~3) return BASE_ERR_FLAGS;
+  BASE_TRY(check_ptr(x, 16));
+  BASE_TRY(check_ptr(logits, 4));
+  BASE_TRY(check_ptr(topk_ids, 4));
+  BASE_TRY(check_ptr(sel_ids, 4));
+  BASE_TRY(check_ptr(n_sel, 4));
+  BASE_TRY(check_ptr(slot_of_expert, 4));
+  BASE_TRY(check_ptr(y, 16));
+  if (residual && !aligned(residual, 16)) return BASE_ERR_ALIGN;
+  const int32_t bc = budget < L->E ? budget : L->E;
+  BASE_TRY(check_ws(L, B, bc, ws, ws_bytes));
+  const Layout o = layout(L, B, bc);
+  BASE_TRY(run_forward(L, x, B, logits, topk_ids, sel_ids, n_sel,
+                       slot_of_expert, bc, flags, residual, y, ws, o,
+                       (hipStream_t)stream));
+  fill_plan(plan_out, ws, o, false);
+  return BASE_OK;
+}
+
+base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
+                              int32_t budget, int32_t flags,
+                              const void *residual, void *y,
+                              base_plan *plan_out, void *ws, size_t ws_bytes,
+                              void *stream) {
+  BASE_TRY(check_layer(L, B, true, true, true));
+  if (budget < 1) return BASE_ERR_BUDGET;
+  if (flags & ~3) return BASE_ERR_FLAGS;
+  BASE_TRY(check_ptr(x, 16));
+  BASE_TRY(check_ptr(y, 16));
+  if (residual && !aligned(residual, 16)) return BASE_ERR_ALIGN;
+  const int32_t bc = budget < L->E ? budget : L->E;
+  BASE_TRY(check_ws(L, B, bc, ws, ws_bytes));
+  const Layout o = layout(L, B, bc);
+  hipStream_t st = (hipStream_t)stream;
+  const bool bf16 = L->dtype == BASE_BF16;
+  float *logits = at<float>(ws, o.logits);
+  int32_t *ids = at<int32_t>(ws, o.topk_ids);
+  float *w = at<float>(ws, o.topk_w);
+  float *cost = at<float>(ws, o.cost);
+  int32_t *sel = at<int32_t>(ws, o.sel_ids);
+  int32_t *nsel = at<int32_t>(ws, o.n_sel);
+  int32_t *slot = at<int32_t>(ws, o.slot_of);
+  HIP_TRY(launch_route_logits(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
+                              logits, st));
+  HIP_TRY(launch_token(bf16, x, B, L->d, L->E, L->K, L->norm_topk, logits, ids,
+                       w, L->pred_a, L->pred_b, cost, 3, st));
+  HIP_TRY(launch_select(B, L->K, L->E, ids, cost, bc, at<float>(ws, o.scores),
+                        at<int32_t>(ws, o.counts), sel, nsel, slot, st));
+  BASE_TRY(run_forward(L, x, B, logits, ids, sel, nsel, slot, bc, flags,
+                       residual, y, ws, o, st));
+  fill_plan(plan_out, ws, o, true);
+  return BASE_OK;
+}
+
+const char *base_status_string(int32_t status) {
+  switch (status) {
+    case BASE_OK: return "ok";
+    case BASE_ERR_NULL: return "a required pointer is NULL";
+    case BASE_ERR_SHAPE: return "shape outside the supported limits";
+    case BASE_ERR_BUDGET: return "budget must be at least 1";
+    case BASE_ERR_DTYPE: return "unknown dtype";
+    case BASE_ERR_ALIGN: return "misaligned pointer";
+    case BASE_ERR_WORKSPACE: return "workspace too small";
+    case BASE_ERR_HIP: return "HIP launch failed";
+    case BASE_ERR_FLAGS: return "unknown flag bits";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

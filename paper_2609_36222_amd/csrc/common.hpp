@@ -1,0 +1,105 @@
+// Device-side building blocks shared by the BASE kernels (gfx950, wave64).
+//
+// Every translation unit is compiled with -ffp-contract=off: a multiply and
+// an add are fused only where the code says fmaf().  The scoring path relies
+// on that to follow one fixed fp32 operation order (see dot partials and
+// base_exp below).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace basek {
+
+constexpr int WAVE = 64;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
+__device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
+
+// ---------------------------------------------------------------- bf16 ---
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  return __uint_as_float(((uint32_t)h) << 16);
+}
+// round to nearest, ties to even (finite inputs)
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Four consecutive activations as fp32 (exact widening for bf16).
+__device__ __forceinline__ void load4(const float *p, float v[4]) {
+  float4 q = *reinterpret_cast<const float4 *>(p);
+  v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+}
+__device__ __forceinline__ void load4(const uint16_t *p, float v[4]) {
+  u32x2 q = *reinterpret_cast<const u32x2 *>(p);
+  v[0] = __uint_as_float(q.x << 16);
+  v[1] = __uint_as_float(q.x & 0xFFFF0000u);
+  v[2] = __uint_as_float(q.y << 16);
+  v[3] = __uint_as_float(q.y & 0xFFFF0000u);
+}
+
+// ---------------------------------------------------------- wave sums ---
+// Butterfly over the 64 lanes.  At step h lane j adds the value of lane
+// j^h; since fp32 addition is commutative this is, value for value, the
+// halving tree "s[j] = s[j] + s[j+h] for j < h" (h = 32 .. 1), and every
+// lane ends with the tree's s[0].
+__device__ __forceinline__ float wave_tree_sum(float v) {
+#pragma unroll
+  for (int h = 32; h >= 1; h >>= 1) v = v + __shfl_xor(v, h, WAVE);
+  return v;
+}
+
+// (value desc, index asc): does (a, ia) rank before (b, ib)?
+__device__ __forceinline__ bool ranks_before(float a, int ia, float b, int ib) {
+  return (a > b) || (a == b && ia < ib);
+}
+
+// Wave-wide first-ranked (value, index) pair; every lane gets the winner.
+__device__ __forceinline__ void wave_argbest(float &v, int &i) {
+#pragma unroll
+  for (int h = 32; h >= 1; h >>= 1) {
+    float ov = __shfl_xor(v, h, WAVE);
+    int oi = __shfl_xor(i, h, WAVE);
+    if (ranks_before(ov, oi, v, i)) { v = ov; i = oi; }
+  }
+}
+
+// ------------------------------------------------------------ base_exp ---
+// exp(x) by Cody-Waite reduction and a degree-7 Taylor polynomial:
+//   x <- clamp(x, -86, 88); n = rint(x * log2 e);
+//   r = fma(-n, C1, x); r = fma(-n, C2, r)   (C1 + C2 = ln 2, C1 short);
+//   p = 1/7!; p = fma(p, r, 1/k!) for k = 6 .. 0;  result p * 2^n.
+// Constants are the binary32 values nearest the stated reals; C1 is ln 2
+// with its 9 low significand bits cleared so that n * C1 is exact.
+__device__ __forceinline__ float base_exp(float x) {
+  const float C1 = __uint_as_float(0x3F317200u);
+  const float C2 = __uint_as_float(0x35BFBE8Eu);
+  x = fminf(fmaxf(x, -86.0f), 88.0f);
+  float t = x * 1.44269504088896341f;
+  float n = __builtin_rintf(t);
+  float r = __builtin_fmaf(-n, C1, x);
+  r = __builtin_fmaf(-n, C2, r);
+  float p = 1.0f / 5040.0f;
+  p = __builtin_fmaf(p, r, 1.0f / 720.0f);
+  p = __builtin_fmaf(p, r, 1.0f / 120.0f);
+  p = __builtin_fmaf(p, r, 1.0f / 24.0f);
+  p = __builtin_fmaf(p, r, 1.0f / 6.0f);
+  p = __builtin_fmaf(p, r, 0.5f);
+  p = __builtin_fmaf(p, r, 1.0f);
+  p = __builtin_fmaf(p, r, 1.0f);
+  return __builtin_ldexpf(p, (int)n);
+}
+
+// SwiGLU activation of the expert FFN (not part of the bit-exact path).
+__device__ __forceinline__ float silu(float a) {
+  return a / (1.0f + __expf(-a));
+}
+
+}  // namespace basek

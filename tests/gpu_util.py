@@ -1,0 +1,120 @@
+"""Helpers of the GPU tests: move seeded inputs to the device, call the C
+ABI through the binding, and read results back."""
+import ctypes
+
+import numpy as np
+import torch
+
+from paper_2609_36222_amd import binding as bd
+
+
+def dev_f32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+
+
+def dev_bf16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits, np.uint16).view(np.int16)).cuda().view(torch.bfloat16)
+
+
+def act_to_dev(x, bf16):
+    """Activations given as fp32 values (bf16-representable for bf16)."""
+    if bf16:
+        u = (np.ascontiguousarray(x, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+        return dev_bf16(u)
+    return dev_f32(x)
+
+
+def to_np_f32(t):
+    if t.dtype == torch.bfloat16:
+        u = t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        return (u.astype(np.uint32) << 16).view(np.float32)
+    return t.float().cpu().numpy()
+
+
+class GpuLayer:
+    def __init__(self, inp, pred_a=None, pred_b=None, norm_topk=1):
+        sh = inp["shape"]
+        self.shape = sh
+        self.bf16 = sh.bf16
+        self.K = sh.K
+        self.wr = dev_f32(inp["w_router"])
+        self.br = None if inp.get("b_router") is None else dev_f32(inp["b_router"])
+        self.pa = dev_f32(inp["pred_a"] if pred_a is None else pred_a)
+        self.pb = dev_f32(inp["pred_b"] if pred_b is None else pred_b)
+        if self.bf16:
+            self.w13, self.w2 = dev_bf16(inp["w13"]), dev_bf16(inp["w2"])
+        else:
+            self.w13, self.w2 = dev_f32(inp["w13"]), dev_f32(inp["w2"])
+        self.layer = bd.Layer(self.wr, self.br, self.pa, self.pb, self.w13,
+                              self.w2, norm_topk)
+        self.desc = self.layer.desc(sh.K)
+        self.E, self.d, self.I = sh.E, sh.d, sh.I
+
+    def x(self, xnp):
+        return act_to_dev(xnp, self.bf16)
+
+    def workspace(self, B, budget):
+        n = bd.base_workspace_bytes(self.desc, B, budget)
+        assert n > 0
+        return torch.empty(n, dtype=torch.uint8, device="cuda")
+
+    def route(self, x, B):
+        logits = torch.empty(B, self.E, dtype=torch.float32, device="cuda")
+        ids = torch.empty(B, self.K, dtype=torch.int32, device="cuda")
+        w = torch.empty(B, self.K, dtype=torch.float32, device="cuda")
+        bd.base_route(self.desc, x, B, logits, ids, w)
+        return logits, ids, w
+
+    def predict(self, x, B, ids, w):
+        cost = torch.empty(B, self.K, dtype=torch.float32, device="cuda")
+        bd.base_predict_cost(self.desc, x, B, ids, w, cost)
+        return cost
+
+    def select(self, B, ids, cost, budget):
+        bc = min(budget, self.E)
+        scores = torch.empty(self.E, dtype=torch.float32, device="cuda")
+        counts = torch.empty(self.E, dtype=torch.int32, device="cuda")
+        sel = torch.empty(bc, dtype=torch.int32, device="cuda")
+        nsel = torch.empty(1, dtype=torch.int32, device="cuda")
+        slot = torch.empty(self.E, dtype=torch.int32, device="cuda")
+        bd.base_select(self.desc, B, ids, cost, budget, scores, counts, sel,
+                       nsel, slot)
+        return scores, counts, sel, nsel, slot
+
+    def y_like(self, B):
+        return torch.empty(B, self.d, dtype=self.w13.dtype, device="cuda")
+
+
+def plan_arrays(plan, ws, B, K, E, budget, full):
+    """Copy the plan arrays out of the workspace (numpy)."""
+    bc = min(budget, E)
+    base = ws.data_ptr()
+    wsb = ws.cpu().numpy()
+
+    def arr(field, count, dtype):
+        p = getattr(plan, field)
+        if p is None:
+            return None
+        off = p - base
+        return wsb[off:off + count * 4].view(dtype).copy()
+
+    out = dict(
+        exec_ids=arr("exec_ids", B * K, np.int32).reshape(B, K),
+        exec_gates=arr("exec_gates", B * K, np.float32).reshape(B, K),
+        offsets=arr("offsets", bc + 1, np.int32),
+        pair_of=arr("pair_of", B * K, np.int32).reshape(B, K))
+    P = int(out["offsets"][-1])
+    out["pair_tok"] = arr("pair_tok", P, np.int32)
+    out["pair_gate"] = arr("pair_gate", P, np.float32)
+    if full:
+        out.update(
+            logits=arr("logits", B * E, np.float32).reshape(B, E),
+            topk_ids=arr("topk_ids", B * K, np.int32).reshape(B, K),
+            topk_w=arr("topk_w", B * K, np.float32).reshape(B, K),
+            cost=arr("cost", B * K, np.float32).reshape(B, K),
+            scores=arr("scores", E, np.float32),
+            counts=arr("counts", E, np.int32),
+            sel_ids=arr("sel_ids", bc, np.int32),
+            n_sel=int(arr("n_sel", 1, np.int32)[0]),
+            slot_of_expert=arr("slot_of_expert", E, np.int32))
+    return out

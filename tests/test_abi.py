@@ -1,0 +1,160 @@
+"""The C-ABI library loads and exports every symbol include/base.h declares;
+host-side validation returns its status codes before anything is enqueued
+(so these run without a GPU: no call here reaches a launch)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_36222_amd import binding as bd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+OK, NULL, SHAPE, BUDGET, DTYPE, ALIGN, WS, HIP, FLAGS = 0, -1, -2, -3, -4, -5, -6, -7, -8
+FAKE = 1 << 32          # a 256-byte aligned stand-in address, never touched
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(bd.LIB_PATH):
+        from paper_2609_36222_amd import build
+        build.build()
+    return bd.load()
+
+
+def header_functions():
+    with open(os.path.join(ROOT, "include", "base.h")) as f:
+        src = f.read()
+    return sorted(set(re.findall(r"^\s*(?:size_t|base_status|const char)\s*\*?\s*(base_\w+)\(",
+                                 src, re.M)))
+
+
+def test_header_and_binding_agree(lib):
+    fns = header_functions()
+    assert fns == sorted(bd.EXPORTS)
+    for f in fns:
+        assert hasattr(lib, f), f
+
+
+def test_exported_symbols_in_dynamic_table(lib):
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", bd.LIB_PATH],
+                         capture_output=True, text=True).stdout
+    syms = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    for f in header_functions():
+        assert f in syms, f
+
+
+def layer(**kw):
+    v = dict(d=2048, E=128, K=8, I=768, dtype=1, norm_topk=1, w_router=FAKE,
+             b_router=FAKE, pred_a=FAKE, pred_b=FAKE, w13=FAKE, w2=FAKE)
+    v.update(kw)
+    return bd.base_layer(v["d"], v["E"], v["K"], v["I"], v["dtype"],
+                         v["norm_topk"], v["w_router"], v["b_router"],
+                         v["pred_a"], v["pred_b"], v["w13"], v["w2"])
+
+
+def route(lib, L, x=FAKE, B=16, lg=FAKE, ids=FAKE, w=FAKE):
+    return lib.base_route(ctypes.byref(L), x, B, lg, ids, w, None)
+
+
+def decode(lib, L, B=16, budget=4, flags=0, x=FAKE, y=FAKE, ws=FAKE,
+           nbytes=None, residual=None):
+    if nbytes is None:
+        nbytes = lib.base_workspace_bytes(ctypes.byref(L), B, budget)
+    return lib.base_decode_layer(ctypes.byref(L), x, B, budget, flags,
+                                 residual, y, None, ws, nbytes, None)
+
+
+def test_status_strings(lib):
+    for s in (OK, NULL, SHAPE, BUDGET, DTYPE, ALIGN, WS, HIP, FLAGS):
+        assert bd.status_string(s)
+    assert bd.status_string(-99) == "unknown status"
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(d=2000), SHAPE), (dict(d=0), SHAPE), (dict(d=16640), SHAPE),
+    (dict(K=0), SHAPE), (dict(K=17, E=32), SHAPE), (dict(E=4, K=8), SHAPE),
+    (dict(E=257), SHAPE), (dict(I=100), SHAPE), (dict(I=0), SHAPE),
+    (dict(dtype=7), DTYPE), (dict(norm_topk=2), SHAPE),
+    (dict(w_router=0), NULL), (dict(w_router=FAKE + 4), ALIGN),
+    (dict(b_router=FAKE + 2), ALIGN)])
+def test_route_layer_validation(lib, kw, expect):
+    assert route(lib, layer(**kw)) == expect
+
+
+@pytest.mark.parametrize("B", [0, -1, 1025])
+def test_batch_limits(lib, B):
+    assert route(lib, layer(), B=B) == SHAPE
+    assert lib.base_workspace_bytes(ctypes.byref(layer()), B, 4) == 0
+
+
+def test_route_pointer_validation(lib):
+    L = layer()
+    assert route(lib, L, x=0) == NULL
+    assert route(lib, L, x=FAKE + 8) == ALIGN
+    assert route(lib, L, lg=0) == NULL
+    assert route(lib, L, ids=FAKE + 2) == ALIGN
+    assert route(lib, L, w=0) == NULL
+
+
+def test_predict_validation(lib):
+    L = layer(pred_a=0)
+    assert lib.base_predict_cost(ctypes.byref(L), FAKE, 4, FAKE, FAKE, FAKE, None) == NULL
+    L = layer(pred_a=FAKE + 4)
+    assert lib.base_predict_cost(ctypes.byref(L), FAKE, 4, FAKE, FAKE, FAKE, None) == ALIGN
+    L = layer()
+    assert lib.base_predict_cost(ctypes.byref(L), FAKE, 4, FAKE, FAKE, 0, None) == NULL
+
+
+def test_select_validation(lib):
+    L = layer()
+    f = lambda budget, **p: lib.base_select(
+        ctypes.byref(L), 16, p.get("ids", FAKE), FAKE, budget, FAKE, FAKE,
+        p.get("sel", FAKE), FAKE, FAKE, None)
+    assert f(0) == BUDGET
+    assert f(-5) == BUDGET
+    assert f(4, ids=0) == NULL
+    assert f(4, sel=FAKE + 1) == ALIGN
+
+
+def test_moe_forward_validation(lib):
+    L = layer()
+    nb = lib.base_workspace_bytes(ctypes.byref(L), 16, 4)
+
+    def f(budget=4, flags=0, ws=FAKE, n=nb, w13=FAKE, residual=None):
+        LL = layer(w13=w13)
+        return lib.base_moe_forward(ctypes.byref(LL), FAKE, 16, FAKE, FAKE,
+                                    FAKE, FAKE, FAKE, budget, flags, residual,
+                                    FAKE, None, ws, n, None)
+    assert f(budget=0) == BUDGET
+    assert f(flags=4) == FLAGS
+    assert f(w13=0) == NULL
+    assert f(w13=FAKE + 8) == ALIGN
+    assert f(ws=0) == NULL
+    assert f(ws=FAKE + 128) == ALIGN
+    assert f(n=nb - 1) == WS
+    assert f(residual=FAKE + 4) == ALIGN
+
+
+def test_decode_layer_validation(lib):
+    L = layer()
+    assert decode(lib, L, budget=0) == BUDGET
+    assert decode(lib, L, flags=8) == FLAGS
+    assert decode(lib, L, x=0) == NULL
+    assert decode(lib, L, y=FAKE + 4) == ALIGN
+    assert decode(lib, L, nbytes=100) == WS
+    assert decode(lib, layer(pred_b=0)) == NULL
+    assert decode(lib, layer(w2=0)) == NULL
+
+
+def test_workspace_grows_with_shape_and_clamps_budget(lib):
+    L = layer()
+    a = lib.base_workspace_bytes(ctypes.byref(L), 64, 16)
+    b = lib.base_workspace_bytes(ctypes.byref(L), 256, 16)
+    assert 0 < a < b
+    assert lib.base_workspace_bytes(ctypes.byref(L), 64, 128) == \
+        lib.base_workspace_bytes(ctypes.byref(L), 64, 1000)
+    assert lib.base_workspace_bytes(ctypes.byref(L), 64, 0) == 0
+    assert lib.base_workspace_bytes(None, 64, 4) == 0

@@ -90,11 +90,14 @@ def seed_seq(shape: LayerShape, layer: int, stream: int, data_seed: int = 0):
 
 
 def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
-    """Round fp32 values to bf16 (nearest, ties to even); return uint16 bits."""
-    a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    return rounded.astype(np.uint16)
+    """Round finite fp32 values to bf16 (nearest, ties to even); return
+    uint16 bits.  (No finite value overflows the 32-bit sum.)"""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    r = (u >> 16) & np.uint32(1)
+    r += u
+    r += np.uint32(0x7FFF)
+    r >>= 16
+    return r.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
@@ -104,18 +107,20 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
 
 
 def _normal_chunked(ss: np.random.SeedSequence, n: int, std: float,
-                    chunk: int = 1 << 22) -> np.ndarray:
-    """n draws of N(0, std^2) in fp32, chunk i from child seed i."""
-    out = np.empty(n, dtype=np.float32)
+                    chunk: int = 1 << 22, bf16: bool = False) -> np.ndarray:
+    """n draws of N(0, std^2) in fp32, chunk i from child seed i; returned
+    as bf16 bits (uint16) when bf16 is set."""
+    out = np.empty(n, dtype=np.uint16 if bf16 else np.float32)
     nchunks = max(1, (n + chunk - 1) // chunk)
     children = ss.spawn(nchunks)
 
     def fill(i):
         lo, hi = i * chunk, min(n, (i + 1) * chunk)
         g = np.random.Generator(np.random.PCG64(children[i]))
-        g.standard_normal(hi - lo, dtype=np.float32, out=out[lo:hi])
+        v = g.standard_normal(hi - lo, dtype=np.float32)
         if std != 1.0:
-            out[lo:hi] *= np.float32(std)
+            v *= np.float32(std)
+        out[lo:hi] = f32_to_bf16_bits(v) if bf16 else v
 
     workers = min(16, os.cpu_count() or 1, nchunks)
     if workers <= 1:
@@ -190,11 +195,9 @@ def experts(shape: LayerShape, layer: int = 0):
     s13, s2 = ss.spawn(2)
     std13 = 1.0 / np.sqrt(d)
     std2 = 1.0 / np.sqrt(d) if not shape.bf16 else 1.0 / np.sqrt(I)
-    w13 = _normal_chunked(s13, E * 2 * I * d, std13).reshape(E, 2 * I, d)
-    w2 = _normal_chunked(s2, E * d * I, std2).reshape(E, d, I)
-    if shape.bf16:
-        return f32_to_bf16_bits(w13), f32_to_bf16_bits(w2)
-    return w13, w2
+    w13 = _normal_chunked(s13, E * 2 * I * d, std13, bf16=shape.bf16)
+    w2 = _normal_chunked(s2, E * d * I, std2, bf16=shape.bf16)
+    return w13.reshape(E, 2 * I, d), w2.reshape(E, d, I)
 
 
 def synthetic_predictor(shape: LayerShape, layer: int = 0):
@@ -236,3 +239,24 @@ def layer_inputs(name: str, layer: int = 0, data_seed: int = 0,
     if with_experts:
         out["w13"], out["w2"] = experts(shape, layer)
     return out
+
+
+def custom_layer(d, E, K, I, B, bf16=True, seed=0, router_std=0.075,
+                 zipf_bias=True, rmsnorm=True, identical_tokens=False,
+                 zero_token=False):
+    """A seeded layer of arbitrary shape for edge cases (same recipe as the
+    named workloads; index 99 keeps its seeds apart from theirs)."""
+    shape = LayerShape(f"custom_d{d}_E{E}_K{K}_I{I}_B{B}", 99, d, E, K, I, B,
+                       (1,), bf16, router_std=router_std,
+                       bias_kind="zipf" if zipf_bias else "normal",
+                       rmsnorm=rmsnorm)
+    wr, br = router(shape, seed)
+    pa, pb = synthetic_predictor(shape, seed)
+    x = decode_tokens(shape, seed)
+    if identical_tokens:
+        x[:] = x[0]
+    if zero_token:
+        x[0] = 0.0
+    w13, w2 = experts(shape, seed)
+    return dict(shape=shape, x=x, w_router=wr, b_router=br, pred_a=pa,
+                pred_b=pb, w13=w13, w2=w2)
