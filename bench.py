@@ -1,0 +1,334 @@
+#!/usr/bin/env python3
+"""Benchmark of the BASE decode hot path on one MI355X.
+
+One step = one call of base_decode_layer (route, predict, aggregate,
+select, backfill, compact, grouped SwiGLU FFN over the kept experts,
+combine) on one synthetic batch.  Default workload: the Qwen3-30B-A3B-shaped
+MoE layer (d=2048, E=128, top-8, SwiGLU I=768, bf16 experts, fp32 router and
+predictor) at batch 256 with expert budget B_e=32, half the batch drawn
+around 4 shared centres.
+
+Weights are resident in HBM before timing starts.  Steps rotate over
+``--layers`` distinct layers (own router, predictor and experts each), as a
+decode step walks a model's layer stack, so the kept experts of a step are
+not still in the 256 MiB Infinity Cache from the previous steps.
+
+Prints ONE JSON line: the step latency in microseconds (``value``), the
+roofline of the dominant kernel (FFN gate/up: kept experts' gate and up rows
+against 8 TB/s of HBM3E), per-stage times from HIP events recorded by the
+library between its kernels, and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import math
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = ("MoE decode-step latency (µs) + HBM GB/s vs peak at batch "
+          "64/256, budget B_e")
+DOMINANT = "ffn_gateup"
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+
+
+def parse_args():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--workload", default="qwen3_b256")
+    p.add_argument("--budget", type=int, default=32)
+    p.add_argument("--layers", type=int, default=4,
+                   help="distinct layers the steps rotate over")
+    p.add_argument("--cpu-seconds", type=float, default=15.0,
+                   help="wall time budget of the CPU oracle sample")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--copy-probe", action="store_true",
+                   help="only run a plain 1 GiB device-to-device copy three "
+                        "times (calibrates the HBM byte counters)")
+    return p.parse_args()
+
+
+def copy_probe():
+    import torch
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_per_copy": n, "copies": 3}))
+
+
+def hip_runtime():
+    """The HIP runtime torch already loaded (events must share it)."""
+    maps = open("/proc/self/maps").read()
+    paths = sorted(set(re.findall(r"(/\S*libamdhip64\.so[.\d]*)", maps)))
+    if not paths:
+        raise RuntimeError("libamdhip64 not loaded")
+    hip = ctypes.CDLL(paths[0])
+    hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float),
+                                        ctypes.c_void_p, ctypes.c_void_p]
+    hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+    return hip
+
+
+def new_event(hip):
+    e = ctypes.c_void_p()
+    if hip.hipEventCreate(ctypes.byref(e)) != 0:
+        raise RuntimeError("hipEventCreate failed")
+    return e.value
+
+
+def elapsed_ms(hip, a, b):
+    ms = ctypes.c_float()
+    if hip.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
+        raise RuntimeError("hipEventElapsedTime failed")
+    return float(ms.value)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("ffn.hip", "common.hpp", "internal.hpp"):
+        with open(os.path.join(ROOT, "paper_2609_36222_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload, budget):
+    """HBM bytes per launch of the dominant kernel from the committed
+    rocprofv3 counter summary, or None when absent or taken on a different
+    kernel source."""
+    path = os.path.join(PROFILE_DIR, f"counters_{DOMINANT}_{workload}_be{budget}.md")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    m_src = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", txt)
+    m_b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    if not m_src or not m_b or m_src.group(1) != kernel_source_hash():
+        return None
+    return float(m_b.group(1))
+
+
+def cpu_baseline(inp, budget, seconds):
+    """The CPU oracle, as it stands, on whole decode layers of the same
+    workload until the time budget is spent."""
+    import numpy as np  # noqa: F401
+    from oracle import method, carith
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        blas = os.cpu_count() or 1
+    carith.build()
+    sh = inp["shape"]
+    ex = method.Experts(inp["w13"], inp["w2"], sh.bf16)
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        method.decode_layer_c(inp["x"], inp["w_router"], inp["b_router"],
+                              inp["pred_a"], inp["pred_b"], sh.K, budget, ex)
+        n += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    return dict(value=round(dt / n * 1e6, 1), unit="us per decode step",
+                cores=int(blas), kind="oracle",
+                sample=f"{n} full decode layers of the timed workload "
+                       f"({sh.name}, B={sh.B}, B_e={budget}): canonical fp32 "
+                       "scoring in C (1 thread) + fp64 NumPy/BLAS expert FFN")
+
+
+def main():
+    args = parse_args()
+    if args.copy_probe:
+        copy_probe()
+        return
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU "
+              "path (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2609_36222_amd import binding as bd
+    if not os.path.exists(bd.LIB_PATH):
+        from paper_2609_36222_amd import build as hb
+        hb.build()
+    bd.load()
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    shape = W.WORKLOADS[args.workload]
+    assert shape.layers == 1, "stacked workloads are not a bench step"
+    budget = args.budget
+
+    def f32(a):
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+
+    def bf16(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    layers, keep_inp = [], None
+    for r in range(args.layers):
+        inp = W.layer_inputs(args.workload, layer=r)
+        wdev = (bf16(inp["w13"]), bf16(inp["w2"])) if shape.bf16 else (f32(inp["w13"]), f32(inp["w2"]))
+        lay = bd.Layer(f32(inp["w_router"]), f32(inp["b_router"]),
+                       f32(inp["pred_a"]), f32(inp["pred_b"]), *wdev)
+        layers.append((lay, lay.desc(shape.K)))
+        if r == 0:
+            keep_inp = inp
+            xnp = inp["x"]
+        del inp
+    B = xnp.shape[0]
+    if shape.bf16:
+        x = bf16((xnp.view(np.uint32) >> 16).astype(np.uint16))
+    else:
+        x = f32(xnp)
+    ws = torch.empty(bd.base_workspace_bytes(layers[0][1], B, budget),
+                     dtype=torch.uint8, device=dev)
+    y = torch.empty(B, shape.d, dtype=torch.bfloat16 if shape.bf16 else torch.float32,
+                    device=dev)
+    stream = torch.cuda.current_stream()
+    sptr = ctypes.c_void_p(stream.cuda_stream)
+    lib = bd.load()
+    plan = bd.base_plan()
+
+    def step(i):
+        _, desc = layers[i % len(layers)]
+        st = lib.base_decode_layer(ctypes.byref(desc), x.data_ptr(), B, budget,
+                                   0, None, y.data_ptr(), ctypes.byref(plan),
+                                   ws.data_ptr(), ws.numel(), sptr)
+        if st != 0:
+            raise RuntimeError(bd.status_string(st))
+
+    hip = hip_runtime()
+    n_ev = bd.N_STAGES + 1
+    stage_ev = [[new_event(hip) for _ in range(n_ev)] for _ in range(args.steps)]
+    ev_keep = [(ctypes.c_void_p * n_ev)(*row) for row in stage_ev]
+    t_start, t_end = new_event(hip), new_event(hip)
+
+    print(f"[bench] {args.workload} B={B} B_e={budget} layers={len(layers)} "
+          f"warmup={args.warmup} steps={args.steps}", file=sys.stderr, flush=True)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # timed region: K steps, stage events recorded by the library
+    torch.cuda.synchronize()
+    hip.hipEventRecord(t_start, sptr)
+    for i in range(args.steps):
+        lib.base_set_stage_events(ev_keep[i], n_ev)
+        step(i)
+    lib.base_set_stage_events(None, 0)
+    hip.hipEventRecord(t_end, sptr)
+    torch.cuda.synchronize()
+    total_ms = elapsed_ms(hip, t_start, t_end)
+    us_step = total_ms * 1e3 / args.steps
+
+    stage_us = np.zeros((args.steps, bd.N_STAGES))
+    for i in range(args.steps):
+        for s in range(bd.N_STAGES):
+            stage_us[i, s] = elapsed_ms(hip, stage_ev[i][s], stage_ev[i][s + 1]) * 1e3
+    stage_mean = {bd.STAGES[s]: round(float(stage_us[:, s].mean()), 2)
+                  for s in range(bd.N_STAGES)}
+
+    # same steps without stage events, for the event overhead
+    torch.cuda.synchronize()
+    hip.hipEventRecord(t_start, sptr)
+    for i in range(args.steps):
+        step(i)
+    hip.hipEventRecord(t_end, sptr)
+    torch.cuda.synchronize()
+    us_step_plain = elapsed_ms(hip, t_start, t_end) * 1e3 / args.steps
+
+    # plan of the last step (for the algorithmic byte count)
+    def read_i32(ptr, n):
+        off = ptr - ws.data_ptr()
+        return ws[off:off + 4 * n].view(torch.int32).cpu().numpy()
+    n_sel = int(read_i32(plan.n_sel, 1)[0])
+    pairs = int(read_i32(plan.offsets, min(budget, shape.E) + 1)[-1])
+    esz = 2 if shape.bf16 else 4
+    gu_bytes = n_sel * 2 * shape.I * shape.d * esz          # gate + up rows
+    ffn_bytes = n_sel * 3 * shape.I * shape.d * esz         # + down
+    gu_us = stage_mean["ffn_gateup"]
+    ffn_us = stage_mean["ffn_gateup"] + stage_mean["ffn_down"]
+    achieved = gu_bytes / (gu_us * 1e-6) / 1e9
+    traffic = stored_traffic(args.workload, budget)
+    scoring_us = (stage_mean["topk_predict"] + stage_mean["aggregate_select"])
+    kernel_sum = float(sum(stage_mean.values()))
+
+    out = {
+        "metric": METRIC,
+        "value": round(us_step, 2),
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(us_step / 1e3, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if shape.bf16 else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.workload}: Qwen3-30B-A3B-shaped MoE layer d={shape.d} "
+                        f"E={shape.E} top-{shape.K} I={shape.I}, batch {B}, "
+                        f"B_e={budget}, bf16 experts, fp32 router+predictor",
+            "batch": B, "budget": budget, "n_sel": n_sel, "pairs": pairs,
+            "layers_rotated": len(layers),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k_gateup_bf16 (FFN gate/up)",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": gu_bytes,
+            "avg_launch_us": gu_us,
+        },
+        "ffn": {
+            "retained_weight_bytes": ffn_bytes,
+            "us": round(ffn_us, 2),
+            "GBps": round(ffn_bytes / (ffn_us * 1e-6) / 1e9, 1),
+            "GBps_over_step": round(ffn_bytes / (us_step * 1e-6) / 1e9, 1),
+        },
+        "stages_us": stage_mean,
+        "overhead": {
+            "predict_aggregate_select_us": round(scoring_us, 2),
+            "predict_aggregate_select_frac": round(scoring_us / us_step, 4),
+            "route_to_compact_us": round(kernel_sum - ffn_us - stage_mean["combine"], 2),
+            "route_to_compact_frac": round(
+                (kernel_sum - ffn_us - stage_mean["combine"]) / us_step, 4),
+        },
+        "us_per_step_without_stage_events": round(us_step_plain, 2),
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(keep_inp, budget, args.cpu_seconds)
+    for row in stage_ev:
+        for e in row:
+            hip.hipEventDestroy(e)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -197,6 +197,19 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
                               base_plan *plan_out, void *ws, size_t ws_bytes,
                               void *stream);
 
+/* Stage timing for profiling.  `events` holds BASE_N_STAGES + 1 hipEvent_t
+ * handles created by the caller (hipEventCreate), or is NULL to switch
+ * timing off (n_events is then ignored).  While set, base_decode_layer
+ * records events[i] on its stream right before stage i and
+ * events[BASE_N_STAGES] after the last one, so hipEventElapsedTime of
+ * consecutive events gives each kernel's duration.  Stages: 0 router
+ * logits, 1 top-K + predicted costs, 2 aggregation + selection, 3 backfill,
+ * 4 compaction, 5 FFN gate/up, 6 FFN down, 7 combine.  The setting belongs
+ * to the calling host thread; the caller keeps the events alive while it
+ * is set.  Returns BASE_ERR_SHAPE if n_events != BASE_N_STAGES + 1. */
+#define BASE_N_STAGES 8
+base_status base_set_stage_events(void *const *events, int32_t n_events);
+
 /* Static description of a status code. */
 const char *base_status_string(int32_t status);
 

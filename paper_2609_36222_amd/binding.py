@@ -20,7 +20,10 @@ FILL_BACKFILL, FILL_DROP = 0, 2
 
 EXPORTS = ("base_workspace_bytes", "base_route", "base_predict_cost",
            "base_select", "base_moe_forward", "base_decode_layer",
-           "base_status_string")
+           "base_set_stage_events", "base_status_string")
+N_STAGES = 8
+STAGES = ("route_logits", "topk_predict", "aggregate_select", "backfill",
+          "compact", "ffn_gateup", "ffn_down", "combine")
 
 _vp = ctypes.c_void_p
 _i32 = ctypes.c_int32
@@ -56,6 +59,9 @@ def load(path: str = LIB_PATH):
     global _lib
     if _lib is not None:
         return _lib
+    # torch first: libbase.so then binds to the HIP runtime torch loaded
+    # (same SONAME), so streams and events are shared with torch
+    import torch  # noqa: F401
     if not os.path.exists(path):
         raise ImportError(
             f"{path} is missing: build it with "
@@ -82,6 +88,8 @@ def load(path: str = LIB_PATH):
                                     _i32, _i32, _vp, _vp,
                                     ctypes.POINTER(base_plan), _vp,
                                     ctypes.c_size_t, _vp]
+    L.base_set_stage_events.restype = _i32
+    L.base_set_stage_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), _i32]
     L.base_status_string.restype = ctypes.c_char_p
     L.base_status_string.argtypes = [_i32]
     _lib = L
@@ -182,6 +190,16 @@ def base_decode_layer(desc, x, B, budget, flags, residual, y, ws, plan=None,
         ctypes.byref(plan), _ptr(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
     return plan
+
+
+def base_set_stage_events(events):
+    """events: a sequence of N_STAGES + 1 raw hipEvent_t handles, or None."""
+    if events is None:
+        _check(load().base_set_stage_events(None, 0))
+        return None
+    arr = (ctypes.c_void_p * len(events))(*events)
+    _check(load().base_set_stage_events(arr, len(events)))
+    return arr   # keep alive while timing is on
 
 
 def plan_offset(plan: base_plan, field: str, ws) -> int:

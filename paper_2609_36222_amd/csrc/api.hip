@@ -96,6 +96,13 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
   return o;
 }
 
+// stage timing (base_set_stage_events), per host thread
+thread_local void *const *g_stage_events = nullptr;
+
+void mark(int stage, hipStream_t st) {
+  if (g_stage_events) (void)hipEventRecord((hipEvent_t)g_stage_events[stage], st);
+}
+
 template <typename T>
 T *at(void *ws, size_t off) {
   return reinterpret_cast<T *>(static_cast<char *>(ws) + off);
@@ -107,7 +114,7 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
                         const int32_t *sel_ids, const int32_t *n_sel,
                         const int32_t *slot_of, int32_t bc, int32_t flags,
                         const void *residual, void *y, void *ws,
-                        const Layout &o, hipStream_t st) {
+                        const Layout &o, hipStream_t st, bool timed) {
   const bool bf16 = L->dtype == BASE_BF16;
   int32_t *exec_ids = at<int32_t>(ws, o.exec_ids);
   float *exec_gates = at<float>(ws, o.exec_gates);
@@ -115,15 +122,23 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
   int32_t *pair_tok = at<int32_t>(ws, o.pair_tok);
   float *pair_gate = at<float>(ws, o.pair_gate);
   int32_t *pair_of = at<int32_t>(ws, o.pair_of);
+  if (timed) mark(3, st);
   HIP_TRY(launch_backfill(B, L->E, L->K, L->norm_topk, flags, logits, ids,
                           slot_of, n_sel, exec_ids, exec_gates, st));
+  if (timed) mark(4, st);
   HIP_TRY(launch_compact(B, L->K, bc, exec_ids, exec_gates, slot_of, n_sel,
                          offsets, pair_tok, pair_gate, pair_of, st));
-  HIP_TRY(launch_ffn(bf16, x, B, L->d, L->I, L->K, L->E, bc, L->w13, L->w2, sel_ids,
-                     n_sel, offsets, pair_tok, pair_gate, at<void>(ws, o.H),
-                     at<float>(ws, o.pairbuf), st));
+  if (timed) mark(5, st);
+  HIP_TRY(launch_gateup(bf16, x, L->d, L->I, L->E, bc, L->w13, sel_ids, n_sel,
+                        offsets, pair_tok, at<void>(ws, o.H), st));
+  if (timed) mark(6, st);
+  HIP_TRY(launch_down(bf16, L->d, L->I, L->E, bc, L->w2, sel_ids, n_sel,
+                      offsets, pair_gate, at<void>(ws, o.H),
+                      at<float>(ws, o.pairbuf), st));
+  if (timed) mark(7, st);
   HIP_TRY(launch_combine(bf16, B, L->d, L->K, pair_of, at<float>(ws, o.pairbuf),
                          residual, y, st));
+  if (timed) mark(8, st);
   return BASE_OK;
 }
 
@@ -237,7 +252,7 @@ base_status base_moe_forward(const base_layer *L, const void *x, int32_t B,
   const Layout o = layout(L, B, bc);
   BASE_TRY(run_forward(L, x, B, logits, topk_ids, sel_ids, n_sel,
                        slot_of_expert, bc, flags, residual, y, ws, o,
-                       (hipStream_t)stream));
+                       (hipStream_t)stream, false));
   fill_plan(plan_out, ws, o, false);
   return BASE_OK;
 }
@@ -265,15 +280,30 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
   int32_t *sel = at<int32_t>(ws, o.sel_ids);
   int32_t *nsel = at<int32_t>(ws, o.n_sel);
   int32_t *slot = at<int32_t>(ws, o.slot_of);
+  mark(0, st);
   HIP_TRY(launch_route_logits(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
                               logits, st));
+  mark(1, st);
   HIP_TRY(launch_token(bf16, x, B, L->d, L->E, L->K, L->norm_topk, logits, ids,
                        w, L->pred_a, L->pred_b, cost, 3, st));
+  mark(2, st);
   HIP_TRY(launch_select(B, L->K, L->E, ids, cost, bc, at<float>(ws, o.scores),
                         at<int32_t>(ws, o.counts), sel, nsel, slot, st));
   BASE_TRY(run_forward(L, x, B, logits, ids, sel, nsel, slot, bc, flags,
-                       residual, y, ws, o, st));
+                       residual, y, ws, o, st, true));
   fill_plan(plan_out, ws, o, true);
+  return BASE_OK;
+}
+
+base_status base_set_stage_events(void *const *events, int32_t n_events) {
+  if (!events) {
+    g_stage_events = nullptr;
+    return BASE_OK;
+  }
+  if (n_events != BASE_N_STAGES + 1) return BASE_ERR_SHAPE;
+  for (int i = 0; i < n_events; ++i)
+    if (!events[i]) return BASE_ERR_NULL;
+  g_stage_events = events;
   return BASE_OK;
 }
 

@@ -32,12 +32,15 @@ hipError_t launch_compact(int B, int K, int budget, const int32_t *exec_ids,
                           const int32_t *n_sel, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
                           int32_t *pair_of, hipStream_t st);
-hipError_t launch_ffn(bool bf16, const void *x, int B, int d, int I, int K,
-                      int E, int budget, const void *w13, const void *w2,
-                      const int32_t *sel_ids, const int32_t *n_sel,
-                      const int32_t *offsets, const int32_t *pair_tok,
-                      const float *pair_gate, void *H, float *pairbuf,
-                      hipStream_t st);
+hipError_t launch_gateup(bool bf16, const void *x, int d, int I, int E,
+                         int budget, const void *w13, const int32_t *sel_ids,
+                         const int32_t *n_sel, const int32_t *offsets,
+                         const int32_t *pair_tok, void *H, hipStream_t st);
+hipError_t launch_down(bool bf16, int d, int I, int E, int budget,
+                       const void *w2, const int32_t *sel_ids,
+                       const int32_t *n_sel, const int32_t *offsets,
+                       const float *pair_gate, const void *H, float *pairbuf,
+                       hipStream_t st);
 hipError_t launch_combine(bool bf16, int B, int d, int K,
                           const int32_t *pair_of, const float *pairbuf,
                           const void *residual, void *y, hipStream_t st);
