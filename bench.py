@@ -53,6 +53,8 @@ def parse_args():
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="wall time budget of the CPU oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--rowmajor", action="store_true",
+                   help="keep the experts row-major instead of packing them")
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain 1 GiB device-to-device copy three "
                         "times (calibrates the HBM byte counters)")
@@ -104,7 +106,7 @@ def elapsed_ms(hip, a, b):
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for f in ("ffn.hip", "common.hpp", "internal.hpp"):
+    for f in ("ffn.hip", "common.hpp", "internal.hpp", "pack.hip"):
         with open(os.path.join(ROOT, "paper_2609_36222_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -191,6 +193,9 @@ def main():
         wdev = (bf16(inp["w13"]), bf16(inp["w2"])) if shape.bf16 else (f32(inp["w13"]), f32(inp["w2"]))
         lay = bd.Layer(f32(inp["w_router"]), f32(inp["b_router"]),
                        f32(inp["pred_a"]), f32(inp["pred_b"]), *wdev)
+        if shape.bf16 and not args.rowmajor:   # one-time, outside timing
+            lay = bd.packed_layer(lay, shape.K)
+            del wdev
         layers.append((lay, lay.desc(shape.K)))
         if r == 0:
             keep_inp = inp
@@ -292,6 +297,7 @@ def main():
                         f"E={shape.E} top-{shape.K} I={shape.I}, batch {B}, "
                         f"B_e={budget}, bf16 experts, fp32 router+predictor",
             "batch": B, "budget": budget, "n_sel": n_sel, "pairs": pairs,
+            "expert_layout": "row-major" if (args.rowmajor or not shape.bf16) else "packed",
             "layers_rotated": len(layers),
         },
         "roofline": {

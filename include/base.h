@@ -86,6 +86,16 @@ enum {
     BASE_FILL_DROP = 2
 };
 
+/* Layout of the expert weights w13 and w2 (see base_pack_experts). */
+enum {
+    /* w13 [E][2I][d], w2 [E][d][I], row-major */
+    BASE_W_ROWMAJOR = 0,
+    /* the same values permuted by base_pack_experts so that every MFMA
+     * operand fragment of the FFN is one contiguous 1 KiB block and each
+     * wavefront of the FFN reads one contiguous stream (bf16 only) */
+    BASE_W_PACKED = 1
+};
+
 /* One MoE layer.  Host struct holding device pointers. */
 typedef struct base_layer {
     int32_t d;          /* hidden size */
@@ -94,6 +104,7 @@ typedef struct base_layer {
     int32_t I;          /* SwiGLU intermediate size */
     int32_t dtype;      /* base_dtype of x, y, residual, w13, w2 */
     int32_t norm_topk;  /* 1: w = p / sum_{top-K} p ; 0: w = softmax p */
+    int32_t w_layout;   /* BASE_W_ROWMAJOR or BASE_W_PACKED */
     const float *w_router;  /* [E][d] fp32, 16-B aligned */
     const float *b_router;  /* [E] fp32 router bias, or NULL */
     const float *pred_a;    /* [E][d] fp32 predictor slopes a_u, 16-B aligned */
@@ -196,6 +207,24 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
                               const void *residual, void *y,
                               base_plan *plan_out, void *ws, size_t ws_bytes,
                               void *stream);
+
+/* Packed expert weights (BASE_W_PACKED).  A one-time permutation, done when
+ * a model is loaded; the values are unchanged.  With 16-row tiles and
+ * 32-element k-steps, a "fragment" is 16 rows x 32 elements of one matrix,
+ * stored as 64 lanes x 8 consecutive elements (lane l: row l % 16,
+ * elements 8 (l / 16) .. +7 of the k-step).  Rows are grouped four tiles at
+ * a time: for w13 group g (g < I/32) holds gate rows 32g..32g+31 (tiles 0,
+ * 1) and up rows I+32g..I+32g+31 (tiles 2, 3); for w2 group g (g < d/64)
+ * holds rows 64g..64g+63 (tiles 0..3).  Storage order:
+ * [E][group][k-step][tile 0..3][fragment], so each group is one contiguous
+ * stream read by one wavefront of the FFN.  Sizes equal the row-major
+ * sizes.
+ *   L          layer with dtype BASE_BF16 and row-major w13, w2 (inputs)
+ *   w13_packed [E * 2I * d] bf16 out, 16-B aligned, may not alias L->w13
+ *   w2_packed  [E * d * I] bf16 out, 16-B aligned, may not alias L->w2
+ * Returns BASE_ERR_DTYPE for fp32 layers. */
+base_status base_pack_experts(const base_layer *L, void *w13_packed,
+                              void *w2_packed, void *stream);
 
 /* Stage timing for profiling.  `events` holds BASE_N_STAGES + 1 hipEvent_t
  * handles created by the caller (hipEventCreate), or is NULL to switch

@@ -15,12 +15,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "_lib", "libbase.so")
 
 BASE_F32, BASE_BF16 = 0, 1
+W_ROWMAJOR, W_PACKED = 0, 1
 GATE_PAPER, GATE_RENORM = 0, 1
 FILL_BACKFILL, FILL_DROP = 0, 2
 
 EXPORTS = ("base_workspace_bytes", "base_route", "base_predict_cost",
            "base_select", "base_moe_forward", "base_decode_layer",
-           "base_set_stage_events", "base_status_string")
+           "base_pack_experts", "base_set_stage_events", "base_status_string")
 N_STAGES = 8
 STAGES = ("route_logits", "topk_predict", "aggregate_select", "backfill",
           "compact", "ffn_gateup", "ffn_down", "combine")
@@ -31,7 +32,7 @@ _i32 = ctypes.c_int32
 
 class base_layer(ctypes.Structure):
     _fields_ = [("d", _i32), ("E", _i32), ("K", _i32), ("I", _i32),
-                ("dtype", _i32), ("norm_topk", _i32),
+                ("dtype", _i32), ("norm_topk", _i32), ("w_layout", _i32),
                 ("w_router", _vp), ("b_router", _vp), ("pred_a", _vp),
                 ("pred_b", _vp), ("w13", _vp), ("w2", _vp)]
 
@@ -88,6 +89,8 @@ def load(path: str = LIB_PATH):
                                     _i32, _i32, _vp, _vp,
                                     ctypes.POINTER(base_plan), _vp,
                                     ctypes.c_size_t, _vp]
+    L.base_pack_experts.restype = _i32
+    L.base_pack_experts.argtypes = [ctypes.POINTER(base_layer), _vp, _vp, _vp]
     L.base_set_stage_events.restype = _i32
     L.base_set_stage_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), _i32]
     L.base_status_string.restype = ctypes.c_char_p
@@ -126,7 +129,7 @@ class Layer:
     fp32 or bf16 (the layer dtype, also the dtype of x and y)."""
 
     def __init__(self, w_router, b_router, pred_a, pred_b, w13, w2,
-                 norm_topk: int = 1):
+                 norm_topk: int = 1, w_layout: int = 0):
         import torch
         E, d = w_router.shape
         I = w2.shape[2]
@@ -136,12 +139,13 @@ class Layer:
         self.torch_dtype = w13.dtype
         self.d, self.E, self.I, self.K = d, E, I, K
         self.norm_topk = norm_topk
+        self.w_layout = w_layout
         self._desc = None
 
     def desc(self, K: int) -> base_layer:
         w_router, b_router, pred_a, pred_b, w13, w2 = self.tensors
         return base_layer(self.d, self.E, K, self.I, self.dtype,
-                          self.norm_topk, _ptr(w_router), _ptr(b_router),
+                          self.norm_topk, self.w_layout, _ptr(w_router), _ptr(b_router),
                           _ptr(pred_a), _ptr(pred_b), _ptr(w13), _ptr(w2))
 
 
@@ -190,6 +194,22 @@ def base_decode_layer(desc, x, B, budget, flags, residual, y, ws, plan=None,
         ctypes.byref(plan), _ptr(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
     return plan
+
+
+def base_pack_experts(desc, w13_packed, w2_packed, stream=None):
+    _check(load().base_pack_experts(ctypes.byref(desc), _ptr(w13_packed),
+                                    _ptr(w2_packed), _stream(stream)))
+
+
+def packed_layer(layer: "Layer", K: int, stream=None) -> "Layer":
+    """A Layer sharing router/predictor tensors, with expert weights packed
+    into new tensors by base_pack_experts (one-time, on the device)."""
+    import torch
+    w_router, b_router, pred_a, pred_b, w13, w2 = layer.tensors
+    w13p, w2p = torch.empty_like(w13), torch.empty_like(w2)
+    base_pack_experts(layer.desc(K), w13p, w2p, stream)
+    return Layer(w_router, b_router, pred_a, pred_b, w13p, w2p,
+                 layer.norm_topk, W_PACKED)
 
 
 def base_set_stage_events(events):

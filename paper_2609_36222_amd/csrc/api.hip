@@ -25,6 +25,8 @@ base_status check_layer(const base_layer *L, int32_t B, bool need_router,
   if (L->K < 1 || L->K > MAX_K || L->E < L->K || L->E > MAX_E) return BASE_ERR_SHAPE;
   if (L->I < 64 || L->I > 32768 || L->I % 64) return BASE_ERR_SHAPE;
   if (L->norm_topk != 0 && L->norm_topk != 1) return BASE_ERR_SHAPE;
+  if (L->w_layout != BASE_W_ROWMAJOR && L->w_layout != BASE_W_PACKED) return BASE_ERR_SHAPE;
+  if (L->w_layout == BASE_W_PACKED && L->dtype != BASE_BF16) return BASE_ERR_DTYPE;
   if (need_router) {
     if (!L->w_router) return BASE_ERR_NULL;
     if (!aligned(L->w_router, 16)) return BASE_ERR_ALIGN;
@@ -61,7 +63,7 @@ base_status check_ptr(const void *p, size_t a) {
 struct Layout {
   size_t logits, topk_ids, topk_w, cost, scores, counts, sel_ids, n_sel,
       slot_of, exec_ids, exec_gates, offsets, pair_tok, pair_gate, pair_of,
-      H, pairbuf, total;
+      tile_base, part_base, xp, H, pairbuf, total;
 };
 
 size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -90,7 +92,17 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
   o.pair_tok = take(BK * 4);
   o.pair_gate = take(BK * 4);
   o.pair_of = take(BK * 4);
-  o.H = take(BK * L->I * elem_bytes(L->dtype));
+  o.tile_base = take(((size_t)bc + 1) * 4);
+  o.part_base = take(((size_t)bc + 1) * 4);
+  if (L->dtype == BASE_BF16) {
+    // fragment-ordered tokens and SwiGLU activations (16-pair tiles)
+    const size_t tiles = (size_t)ffn_max_tiles(B, L->K, bc);
+    o.xp = take(tiles * 16 * (size_t)L->d * 2);
+    o.H = take(tiles * 16 * (size_t)L->I * 2);
+  } else {
+    o.xp = 0;
+    o.H = take(BK * L->I * 4);
+  }
   o.pairbuf = take(BK * L->d * 4);
   o.total = at;
   return o;
@@ -126,15 +138,23 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
   HIP_TRY(launch_backfill(B, L->E, L->K, L->norm_topk, flags, logits, ids,
                           slot_of, n_sel, exec_ids, exec_gates, st));
   if (timed) mark(4, st);
+  int32_t *tile_base = at<int32_t>(ws, o.tile_base);
+  int32_t *part_base = at<int32_t>(ws, o.part_base);
   HIP_TRY(launch_compact(B, L->K, bc, exec_ids, exec_gates, slot_of, n_sel,
-                         offsets, pair_tok, pair_gate, pair_of, st));
+                         offsets, pair_tok, pair_gate, pair_of, tile_base,
+                         part_base, st));
   if (timed) mark(5, st);
-  HIP_TRY(launch_gateup(bf16, x, L->d, L->I, L->E, bc, L->w13, sel_ids, n_sel,
-                        offsets, pair_tok, at<void>(ws, o.H), st));
+  if (bf16)
+    HIP_TRY(launch_gather(x, B, L->d, L->K, bc, n_sel, offsets, pair_tok,
+                          tile_base, at<void>(ws, o.xp), st));
+  const bool packed = L->w_layout == BASE_W_PACKED;
+  HIP_TRY(launch_gateup(bf16, packed, x, B, L->d, L->I, L->E, L->K, bc, L->w13,
+                        sel_ids, n_sel, offsets, pair_tok, tile_base, part_base,
+                        at<void>(ws, o.xp), at<void>(ws, o.H), st));
   if (timed) mark(6, st);
-  HIP_TRY(launch_down(bf16, L->d, L->I, L->E, bc, L->w2, sel_ids, n_sel,
-                      offsets, pair_gate, at<void>(ws, o.H),
-                      at<float>(ws, o.pairbuf), st));
+  HIP_TRY(launch_down(bf16, packed, B, L->d, L->I, L->E, L->K, bc, L->w2,
+                      sel_ids, n_sel, offsets, tile_base, part_base, pair_gate,
+                      at<void>(ws, o.H), at<float>(ws, o.pairbuf), st));
   if (timed) mark(7, st);
   HIP_TRY(launch_combine(bf16, B, L->d, L->K, pair_of, at<float>(ws, o.pairbuf),
                          residual, y, st));
@@ -292,6 +312,19 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
   BASE_TRY(run_forward(L, x, B, logits, ids, sel, nsel, slot, bc, flags,
                        residual, y, ws, o, st, true));
   fill_plan(plan_out, ws, o, true);
+  return BASE_OK;
+}
+
+base_status base_pack_experts(const base_layer *L, void *w13_packed,
+                              void *w2_packed, void *stream) {
+  if (!L) return BASE_ERR_NULL;
+  if (L->dtype != BASE_BF16) return BASE_ERR_DTYPE;
+  if (L->w_layout != BASE_W_ROWMAJOR) return BASE_ERR_SHAPE;
+  BASE_TRY(check_layer(L, 1, false, false, true));
+  BASE_TRY(check_ptr(w13_packed, 16));
+  BASE_TRY(check_ptr(w2_packed, 16));
+  HIP_TRY(launch_pack(L->w13, L->w2, w13_packed, w2_packed, L->E, L->d, L->I,
+                      (hipStream_t)stream));
   return BASE_OK;
 }
 

@@ -184,6 +184,34 @@ void k_backfill(int B, int E, int K, int norm_topk, int flags,
   }
 }
 
+// Exclusive prefix over slots s < n of ceil(cnt[s] / unit) by one
+// wavefront (4 slots per lane); out[MAX_E] receives the total.
+__device__ __forceinline__ void wave_scan_slots(const int *cnt, int n, int unit,
+                                                int *out) {
+  const int lane = lane_id();
+  int local[MAX_E / WAVE];
+  int sum = 0;
+#pragma unroll
+  for (int q = 0; q < MAX_E / WAVE; ++q) {
+    const int s = lane * (MAX_E / WAVE) + q;
+    local[q] = (s < n) ? (cnt[s] + unit - 1) / unit : 0;
+    sum += local[q];
+  }
+  int incl = sum;
+#pragma unroll
+  for (int h = 1; h < WAVE; h <<= 1) {
+    const int o = __shfl_up(incl, h, WAVE);
+    if (lane >= h) incl += o;
+  }
+  int run = incl - sum;
+#pragma unroll
+  for (int q = 0; q < MAX_E / WAVE; ++q) {
+    out[lane * (MAX_E / WAVE) + q] = run;
+    run += local[q];
+  }
+  if (lane == WAVE - 1) out[MAX_E] = incl;
+}
+
 constexpr int CP_THREADS = 1024;
 constexpr int CP_WORDS = MAX_B / 32;
 
@@ -193,12 +221,15 @@ void k_compact(int B, int K, int budget, const int32_t *__restrict__ exec_ids,
                const int32_t *__restrict__ slot_of,
                const int32_t *__restrict__ n_sel_p,
                int32_t *__restrict__ offsets, int32_t *__restrict__ pair_tok,
-               float *__restrict__ pair_gate, int32_t *__restrict__ pair_of) {
+               float *__restrict__ pair_gate, int32_t *__restrict__ pair_of,
+               int32_t *__restrict__ tile_base, int32_t *__restrict__ part_base) {
   // bits[s][w]: bit (t & 31) of word w = t >> 5 is set when token t runs slot s
   __shared__ uint32_t bits[MAX_E * CP_WORDS];
   __shared__ int pre[MAX_E * CP_WORDS];
   __shared__ int cnt[MAX_E];
   __shared__ int off[MAX_E + 1];
+  __shared__ int tb[MAX_E + 1];
+  __shared__ int pb[MAX_E + 1];
   const int tid = threadIdx.x, lane = lane_id();
   const int n_sel = min(max(*n_sel_p, 0), budget);
   const int nwords = (B + 31) / 32;
@@ -227,31 +258,16 @@ void k_compact(int B, int K, int budget, const int32_t *__restrict__ exec_ids,
     cnt[s] = run;
   }
   __syncthreads();
-  if (tid < WAVE) {   // exclusive scan of the slot counts by one wavefront
-    int local[MAX_E / WAVE];
-    int sum = 0;
-#pragma unroll
-    for (int q = 0; q < MAX_E / WAVE; ++q) {
-      const int s = lane * (MAX_E / WAVE) + q;
-      local[q] = (s < n_sel) ? cnt[s] : 0;
-      sum += local[q];
-    }
-    int incl = sum;
-#pragma unroll
-    for (int h = 1; h < WAVE; h <<= 1) {
-      const int o = __shfl_up(incl, h, WAVE);
-      if (lane >= h) incl += o;
-    }
-    int run = incl - sum;
-#pragma unroll
-    for (int q = 0; q < MAX_E / WAVE; ++q) {
-      const int s = lane * (MAX_E / WAVE) + q;
-      if (s <= MAX_E) off[s] = run;
-      run += local[q];
-    }
-    if (lane == WAVE - 1) off[MAX_E] = incl;
+  if (tid < WAVE) {   // exclusive scans over slots by one wavefront:
+    wave_scan_slots(cnt, n_sel, 1, off);          // pairs
+    wave_scan_slots(cnt, n_sel, 16, tb);          // 16-pair tiles
+    wave_scan_slots(cnt, n_sel, FFN_PART, pb);    // FFN token parts
   }
   __syncthreads();
+  for (int s = tid; s <= budget; s += CP_THREADS) {
+    tile_base[s] = (s < n_sel) ? tb[s] : tb[MAX_E];
+    part_base[s] = (s < n_sel) ? pb[s] : pb[MAX_E];
+  }
   const int total = off[MAX_E];
   for (int s = tid; s <= budget; s += CP_THREADS)
     offsets[s] = (s < n_sel) ? off[s] : total;
@@ -297,10 +313,11 @@ hipError_t launch_compact(int B, int K, int budget, const int32_t *exec_ids,
                           const float *exec_gates, const int32_t *slot_of,
                           const int32_t *n_sel, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
-                          int32_t *pair_of, hipStream_t st) {
+                          int32_t *pair_of, int32_t *tile_base,
+                          int32_t *part_base, hipStream_t st) {
   hipLaunchKernelGGL(k_compact, dim3(1), dim3(CP_THREADS), 0, st, B, K, budget,
                      exec_ids, exec_gates, slot_of, n_sel, offsets, pair_tok,
-                     pair_gate, pair_of);
+                     pair_gate, pair_of, tile_base, part_base);
   return hipGetLastError();
 }
 

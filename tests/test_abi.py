@@ -47,12 +47,14 @@ def test_exported_symbols_in_dynamic_table(lib):
 
 
 def layer(**kw):
-    v = dict(d=2048, E=128, K=8, I=768, dtype=1, norm_topk=1, w_router=FAKE,
-             b_router=FAKE, pred_a=FAKE, pred_b=FAKE, w13=FAKE, w2=FAKE)
+    v = dict(d=2048, E=128, K=8, I=768, dtype=1, norm_topk=1, w_layout=0,
+             w_router=FAKE, b_router=FAKE, pred_a=FAKE, pred_b=FAKE, w13=FAKE,
+             w2=FAKE)
     v.update(kw)
     return bd.base_layer(v["d"], v["E"], v["K"], v["I"], v["dtype"],
-                         v["norm_topk"], v["w_router"], v["b_router"],
-                         v["pred_a"], v["pred_b"], v["w13"], v["w2"])
+                         v["norm_topk"], v["w_layout"], v["w_router"],
+                         v["b_router"], v["pred_a"], v["pred_b"], v["w13"],
+                         v["w2"])
 
 
 def route(lib, L, x=FAKE, B=16, lg=FAKE, ids=FAKE, w=FAKE):
@@ -78,6 +80,7 @@ def test_status_strings(lib):
     (dict(K=0), SHAPE), (dict(K=17, E=32), SHAPE), (dict(E=4, K=8), SHAPE),
     (dict(E=257), SHAPE), (dict(I=100), SHAPE), (dict(I=0), SHAPE),
     (dict(dtype=7), DTYPE), (dict(norm_topk=2), SHAPE),
+    (dict(w_layout=2), SHAPE), (dict(w_layout=1, dtype=0), DTYPE),
     (dict(w_router=0), NULL), (dict(w_router=FAKE + 4), ALIGN),
     (dict(b_router=FAKE + 2), ALIGN)])
 def test_route_layer_validation(lib, kw, expect):
@@ -158,3 +161,14 @@ def test_workspace_grows_with_shape_and_clamps_budget(lib):
         lib.base_workspace_bytes(ctypes.byref(L), 64, 1000)
     assert lib.base_workspace_bytes(ctypes.byref(L), 64, 0) == 0
     assert lib.base_workspace_bytes(None, 64, 4) == 0
+
+
+def test_pack_validation(lib):
+    f = lambda L, a=FAKE, b=FAKE: lib.base_pack_experts(ctypes.byref(L), a, b, None)
+    assert lib.base_pack_experts(None, FAKE, FAKE, None) == NULL
+    assert f(layer(dtype=0)) == DTYPE
+    assert f(layer(w_layout=1)) == SHAPE
+    assert f(layer(), a=0) == NULL
+    assert f(layer(), b=FAKE + 8) == ALIGN
+    assert f(layer(w13=0)) == NULL
+    assert f(layer(I=100)) == SHAPE

@@ -132,6 +132,14 @@ def run_case(gu, inp, budget, flags=0, norm_topk=1, with_residual=False,
         assert np.array_equal(got2[f], ref[f]), f
     assert got2["n_sel"] == ref["n_sel"]
     assert np.array_equal(gu.to_np_f32(y2), y_staged)
+    if sh.bf16:
+        # packed expert layout: same values, same arithmetic, same bits
+        glp = gu.GpuLayer(inp, norm_topk=norm_topk, packed=True)
+        ws3 = glp.workspace(B, budget)
+        y3 = glp.y_like(B)
+        bd.base_decode_layer(glp.desc, x, B, budget, flags, res_d, y3, ws3)
+        torch.cuda.synchronize()
+        assert np.array_equal(gu.to_np_f32(y3), y_staged)
     return ref, y_staged
 
 
@@ -215,3 +223,32 @@ def test_repeat_runs_are_bit_identical(gu, qwen3_b256):
         outs.append(y.view(torch.int16).cpu().numpy())
     for o in outs[1:]:
         assert np.array_equal(o, outs[0])
+
+
+def test_packed_layout_matches_its_definition(gu):
+    """base_pack_experts against the layout stated in base.h, rebuilt here
+    with numpy from the row-major arrays."""
+    from paper_2609_36222_amd import binding as bd
+    inp = W.custom_layer(512, 6, 2, 192, 4, seed=21)
+    gl = gu.GpuLayer(inp, packed=True)
+    E, d, I = 6, 512, 192
+    got13 = gl.layer.tensors[4].view(torch.int16).cpu().numpy().view(np.uint16)
+    got2 = gl.layer.tensors[5].view(torch.int16).cpu().numpy().view(np.uint16)
+
+    def pack(w, rows_of_tile, groups, kdim):
+        E_ = w.shape[0]
+        out = np.empty((E_, groups, kdim // 32, 4, 64, 8), np.uint16)
+        lanes = np.arange(64)
+        for g in range(groups):
+            for t in range(4):
+                rows = rows_of_tile(g, t) + (lanes % 16)
+                for ks in range(kdim // 32):
+                    cols = 32 * ks + 8 * (lanes // 16)
+                    idx = cols[:, None] + np.arange(8)[None, :]
+                    out[:, g, ks, t] = w[:, rows[:, None], idx]
+        return out.reshape(-1)
+    exp13 = pack(inp["w13"], lambda g, t: (0 if t < 2 else I) + 32 * g + 16 * (t % 2),
+                 I // 32, d)
+    exp2 = pack(inp["w2"], lambda g, t: 64 * g + 16 * t, d // 64, I)
+    assert np.array_equal(got13.reshape(-1), exp13)
+    assert np.array_equal(got2.reshape(-1), exp2)
