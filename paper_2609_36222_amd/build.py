@@ -20,7 +20,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_lib")
 LIB = os.path.join(OUT_DIR, "libbase.so")
-SOURCES = ["api.hip", "route_predict.hip", "plan.hip", "ffn.hip", "pack.hip"]
+SOURCES = ["api.hip", "scores.hip", "route_predict.hip", "plan.hip", "ffn.hip",
+           "pack.hip"]
 ARCH = os.environ.get("BASE_OFFLOAD_ARCH", "gfx950")
 
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

@@ -61,9 +61,9 @@ base_status check_ptr(const void *p, size_t a) {
 
 // Workspace layout: every array starts on a 256-byte boundary.
 struct Layout {
-  size_t logits, topk_ids, topk_w, cost, scores, counts, sel_ids, n_sel,
+  size_t logits, q, ss, topk_ids, topk_w, cost, scores, counts, sel_ids, n_sel,
       slot_of, exec_ids, exec_gates, offsets, pair_tok, pair_gate, pair_of,
-      tile_base, part_base, xp, H, pairbuf, total;
+      parts, n_parts, xp, H, pairbuf, total;
 };
 
 size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -78,6 +78,8 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
   };
   const size_t BK = (size_t)B * L->K;
   o.logits = take((size_t)B * L->E * 4);
+  o.q = take((size_t)B * L->E * 4);
+  o.ss = take((size_t)B * 4);
   o.topk_ids = take(BK * 4);
   o.topk_w = take(BK * 4);
   o.cost = take(BK * 4);
@@ -92,8 +94,8 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
   o.pair_tok = take(BK * 4);
   o.pair_gate = take(BK * 4);
   o.pair_of = take(BK * 4);
-  o.tile_base = take(((size_t)bc + 1) * 4);
-  o.part_base = take(((size_t)bc + 1) * 4);
+  o.parts = take((size_t)ffn_max_parts(B, L->K, bc) * sizeof(PartRec));
+  o.n_parts = take(4);
   if (L->dtype == BASE_BF16) {
     // fragment-ordered tokens and SwiGLU activations (16-pair tiles)
     const size_t tiles = (size_t)ffn_max_tiles(B, L->K, bc);
@@ -138,22 +140,22 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
   HIP_TRY(launch_backfill(B, L->E, L->K, L->norm_topk, flags, logits, ids,
                           slot_of, n_sel, exec_ids, exec_gates, st));
   if (timed) mark(4, st);
-  int32_t *tile_base = at<int32_t>(ws, o.tile_base);
-  int32_t *part_base = at<int32_t>(ws, o.part_base);
+  PartRec *parts = at<PartRec>(ws, o.parts);
+  int32_t *n_parts = at<int32_t>(ws, o.n_parts);
   HIP_TRY(launch_compact(B, L->K, bc, exec_ids, exec_gates, slot_of, n_sel,
-                         offsets, pair_tok, pair_gate, pair_of, tile_base,
-                         part_base, st));
+                         offsets, pair_tok, pair_gate, pair_of, sel_ids, parts,
+                         n_parts, st));
   if (timed) mark(5, st);
   if (bf16)
-    HIP_TRY(launch_gather(x, B, L->d, L->K, bc, n_sel, offsets, pair_tok,
-                          tile_base, at<void>(ws, o.xp), st));
+    HIP_TRY(launch_gather(x, B, L->d, L->K, bc, parts, n_parts, pair_tok,
+                          at<void>(ws, o.xp), st));
   const bool packed = L->w_layout == BASE_W_PACKED;
   HIP_TRY(launch_gateup(bf16, packed, x, B, L->d, L->I, L->E, L->K, bc, L->w13,
-                        sel_ids, n_sel, offsets, pair_tok, tile_base, part_base,
+                        sel_ids, n_sel, offsets, pair_tok, parts, n_parts,
                         at<void>(ws, o.xp), at<void>(ws, o.H), st));
   if (timed) mark(6, st);
   HIP_TRY(launch_down(bf16, packed, B, L->d, L->I, L->E, L->K, bc, L->w2,
-                      sel_ids, n_sel, offsets, tile_base, part_base, pair_gate,
+                      sel_ids, n_sel, offsets, parts, n_parts, pair_gate,
                       at<void>(ws, o.H), at<float>(ws, o.pairbuf), st));
   if (timed) mark(7, st);
   HIP_TRY(launch_combine(bf16, B, L->d, L->K, pair_of, at<float>(ws, o.pairbuf),
@@ -208,10 +210,10 @@ base_status base_route(const base_layer *L, const void *x, int32_t B,
   BASE_TRY(check_ptr(topk_w, 4));
   hipStream_t st = (hipStream_t)stream;
   const bool bf16 = L->dtype == BASE_BF16;
-  HIP_TRY(launch_route_logits(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
-                              logits, st));
-  HIP_TRY(launch_token(bf16, x, B, L->d, L->E, L->K, L->norm_topk, logits,
-                       topk_ids, topk_w, nullptr, nullptr, nullptr, 1, st));
+  HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
+                        nullptr, 0, logits, nullptr, nullptr, st));
+  HIP_TRY(launch_tail(B, L->E, L->K, L->norm_topk, logits, nullptr, nullptr,
+                      nullptr, topk_ids, topk_w, nullptr, 1, st));
   return BASE_OK;
 }
 
@@ -223,10 +225,9 @@ base_status base_predict_cost(const base_layer *L, const void *x, int32_t B,
   BASE_TRY(check_ptr(topk_ids, 4));
   BASE_TRY(check_ptr(topk_w, 4));
   BASE_TRY(check_ptr(cost, 4));
-  HIP_TRY(launch_token(L->dtype == BASE_BF16, x, B, L->d, L->E, L->K,
-                       L->norm_topk, nullptr, const_cast<int32_t *>(topk_ids),
-                       const_cast<float *>(topk_w), L->pred_a, L->pred_b, cost,
-                       2, (hipStream_t)stream));
+  HIP_TRY(launch_predict(L->dtype == BASE_BF16, x, B, L->d, L->E, L->K,
+                         topk_ids, topk_w, L->pred_a, L->pred_b, cost,
+                         (hipStream_t)stream));
   return BASE_OK;
 }
 
@@ -300,12 +301,14 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
   int32_t *sel = at<int32_t>(ws, o.sel_ids);
   int32_t *nsel = at<int32_t>(ws, o.n_sel);
   int32_t *slot = at<int32_t>(ws, o.slot_of);
+  float *q = at<float>(ws, o.q);
+  float *ss = at<float>(ws, o.ss);
   mark(0, st);
-  HIP_TRY(launch_route_logits(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
-                              logits, st));
+  HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
+                        L->pred_a, L->E, logits, q, ss, st));
   mark(1, st);
-  HIP_TRY(launch_token(bf16, x, B, L->d, L->E, L->K, L->norm_topk, logits, ids,
-                       w, L->pred_a, L->pred_b, cost, 3, st));
+  HIP_TRY(launch_tail(B, L->E, L->K, L->norm_topk, logits, q, ss, L->pred_b,
+                      ids, w, cost, 3, st));
   mark(2, st);
   HIP_TRY(launch_select(B, L->K, L->E, ids, cost, bc, at<float>(ws, o.scores),
                         at<int32_t>(ws, o.counts), sel, nsel, slot, st));

@@ -61,6 +61,17 @@ __device__ __forceinline__ bool ranks_before(float a, int ia, float b, int ib) {
   return (a > b) || (a == b && ia < ib);
 }
 
+// A 64-bit key whose unsigned order is the order (value desc, index asc) of
+// ranks_before, for finite values: the high word maps the float's order onto
+// the unsigned integers (with -0 taken as +0, equal as floats), the low word
+// is larger for smaller indices.
+__device__ __forceinline__ uint64_t rank_key(float v, int e) {
+  uint32_t u = __float_as_uint(v);
+  if (u == 0x80000000u) u = 0u;
+  const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)o << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)e);
+}
+
 // Wave-wide first-ranked (value, index) pair; every lane gets the winner.
 __device__ __forceinline__ void wave_argbest(float &v, int &i) {
 #pragma unroll

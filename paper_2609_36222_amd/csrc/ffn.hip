@@ -20,7 +20,8 @@
 
 namespace basek {
 
-constexpr int FF_WAVES = 1;      // wavefronts per workgroup
+constexpr int GU_SPLIT = 4;      // gate/up: wavefronts per workgroup = contraction shares
+constexpr int DN_SPLIT = 1;      // down: one wavefront per unit
 constexpr int N_XCD = 8;         // accelerator dies, one L2 each
 constexpr int FF_RT = 4;         // 16-row weight tiles per wavefront
 constexpr int FF_NT = 4;         // 16-token tiles per wavefront (64 tokens)
@@ -66,9 +67,9 @@ __device__ __forceinline__ bf16x8 wload(const WeightSrc &w, int t, int ks) {
   return bload(w.r[t], w.voff, (uint32_t)ks * 64u);
 }
 
-// Token operands in fragment order.  The tokens of kept slot s occupy the
-// 16-pair tiles tile_base[s] .. tile_base[s+1]-1 (tile i holds the slot's
-// pairs 16 i' .. 16 i' + 15, i' = i - tile_base[s]; the last tile padded).
+// Token operands in fragment order.  The pairs of kept slot s occupy
+// consecutive 16-pair tiles (its i-th tile holds its pairs 16 i .. 16 i +
+// 15, the last one padded); a part's tiles start at its tile0.
 // For a contraction of `ks` k-steps a tile is ks fragments of 1 KiB:
 // fragment (tile, k-step) = 64 lanes x 8 elements, lane l holding pair
 // 16 i' + l % 16, elements 32 k-step + 8 (l / 16) .. +7.  So every operand
@@ -77,103 +78,114 @@ __device__ __forceinline__ bf16x8 wload(const WeightSrc &w, int t, int ks) {
 //   hp: the SwiGLU activations (contraction I), written by k_gateup
 // Padding rows are never written; they only meet discarded output columns.
 
-// One wavefront per (tile, k-step): gather 1 KiB of hidden states.
+// One wavefront per (part, k-step): the part's tiles' fragments of that
+// k-step, 1 KiB each; padding rows of a part's last tile are zeroed.
 __global__ __launch_bounds__(256)
-void k_gather(const uint16_t *__restrict__ x, int d, int budget,
-              const int32_t *__restrict__ n_sel_p,
-              const int32_t *__restrict__ offsets,
+void k_gather(const uint16_t *__restrict__ x, int d,
+              const PartRec *__restrict__ parts,
+              const int32_t *__restrict__ n_parts,
               const int32_t *__restrict__ pair_tok,
-              const int32_t *__restrict__ tile_base,
               uint16_t *__restrict__ xp) {
   const int ksteps = d / 32;
   const int v = blockIdx.x * (blockDim.x / WAVE) + wave_id();
-  const int n_sel = min(max(*n_sel_p, 0), budget);
-  const int tile = v / ksteps, ks = v % ksteps;
-  if (tile >= tile_base[n_sel]) return;
-  int lo = 0, hi = n_sel - 1;      // last slot with tile_base[s] <= tile
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) / 2;
-    if (tile_base[mid] <= tile) lo = mid; else hi = mid - 1;
+  const int q = v / ksteps, ks = v % ksteps;
+  if (q >= *n_parts) return;
+  const PartRec r = parts[q];
+  const int ts = q - r.part0;
+  const int p0 = r.off + FFN_PART * ts, n = min(FFN_PART, r.n - FFN_PART * ts);
+  const int tile0 = r.tile0 + (FFN_PART / 16) * ts;
+  const int lane = lane_id();
+  for (int j = 0; 16 * j < n; ++j) {
+    const int k = 16 * j + (lane & 15);
+    u32x4 v4 = {0u, 0u, 0u, 0u};
+    if (k < n)
+      v4 = *reinterpret_cast<const u32x4 *>(x + (size_t)pair_tok[p0 + k] * d + 32 * ks +
+                                            8 * (lane >> 4));
+    *reinterpret_cast<u32x4 *>(xp + (((size_t)(tile0 + j) * ksteps + ks) * WAVE + lane) * 8) =
+        v4;
   }
-  const int s = lo, lane = lane_id();
-  const int p = offsets[s] + 16 * (tile - tile_base[s]) + (lane & 15);
-  u32x4 v4 = {0u, 0u, 0u, 0u};
-  if (p < offsets[s + 1])
-    v4 = *reinterpret_cast<const u32x4 *>(x + (size_t)pair_tok[p] * d + 32 * ks +
-                                          8 * (lane >> 4));
-  *reinterpret_cast<u32x4 *>(xp + (((size_t)tile * ksteps + ks) * WAVE + lane) * 8) = v4;
 }
 
-// Flat work assignment: wavefront v of the grid takes unit v of the list
-// (slot s, row group g, token part ts) ordered by slot, then group, then
-// part (a slot has parts = ceil(n_s / 64) token parts of 64 and `groups`
-// row groups of 64 weight rows; part_base[s] is the prefix of parts).  The
-// parts of one row group are neighbours, so they usually run in one
-// workgroup on one CU and fetch the group's weights from HBM once.
+// Work list: unit v = (kept slot s, row group g, token part ts of s),
+// ordered by slot, then group, then part, so that the units that read one
+// row group's weights are neighbours (and run at about the same time on
+// one XCD, the later ones finding the weights in L2).  The units of slot s
+// are v = groups * part0_s + g * parts_s + ts, so floor(v / groups) is one
+// of s's parts and its part-table entry describes s.  One workgroup per
+// unit; its wavefronts (GU_SPLIT, DN_SPLIT) each take an equal share of the
+// contraction and their partial sums are added through LDS in a fixed
+// order.
 struct Unit {
-  int s, g, ts;
+  int u, p0, n, tile0, g;
 };
 
 // The dispatcher deals the workgroups of a launch round-robin over the
 // XCDs (workgroup b runs on XCD b % 8).  The unit list is cut into 8
 // contiguous runs, run x for XCD x, so the units that read one slot's
 // tokens or one row group's weights mostly share an L2.  Returns the unit
-// of the calling wavefront, or -1.
+// of the calling workgroup, or -1.
 __device__ __forceinline__ int xcd_unit(int units) {
-  const int per = (units + N_XCD * FF_WAVES - 1) / (N_XCD * FF_WAVES);
+  const int per = (units + N_XCD - 1) / N_XCD;
   const int local = blockIdx.x / N_XCD;
   if (local >= per) return -1;
-  // wave-uniform by construction; said so, so that every address derived
-  // from it stays scalar (a buffer resource held in vector registers would
-  // turn each load into a loop over the lanes)
-  return __builtin_amdgcn_readfirstlane(((blockIdx.x % N_XCD) * per + local) * FF_WAVES +
-                                        wave_id());
+  return (blockIdx.x % N_XCD) * per + local;
 }
 
-__device__ __forceinline__ bool find_unit(int groups, int n_sel,
-                                          const int32_t *part_base, Unit &w) {
-  const int v = xcd_unit(groups * part_base[n_sel]);
-  if (v < 0 || v >= groups * part_base[n_sel]) return false;
-  int lo = 0, hi = n_sel - 1;      // last slot with groups * part_base[s] <= v
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) / 2;
-    if (groups * part_base[mid] <= v) lo = mid; else hi = mid - 1;
-  }
-  const int parts = __builtin_amdgcn_readfirstlane(part_base[lo + 1] - part_base[lo]);
-  const int r = v - groups * __builtin_amdgcn_readfirstlane(part_base[lo]);
-  w.s = __builtin_amdgcn_readfirstlane(lo);
-  w.g = r / parts;
-  w.ts = r % parts;
+// Every value here is uniform over the workgroup, and is said to be so
+// (readfirstlane), so that the addresses derived from it stay in scalar
+// registers: a buffer resource held in vector registers would turn each
+// load into a loop over the lanes.
+__device__ __forceinline__ bool find_unit(int groups, const PartRec *parts,
+                                          const int32_t *n_parts, Unit &w) {
+  const int units = __builtin_amdgcn_readfirstlane(groups * *n_parts);
+  const int v = __builtin_amdgcn_readfirstlane(xcd_unit(units));
+  if (v < 0 || v >= units) return false;
+  const PartRec r = parts[v / groups];
+  const int u = __builtin_amdgcn_readfirstlane(r.u);
+  const int off = __builtin_amdgcn_readfirstlane(r.off);
+  const int n = __builtin_amdgcn_readfirstlane(r.n);
+  const int tile0 = __builtin_amdgcn_readfirstlane(r.tile0);
+  const int part0 = __builtin_amdgcn_readfirstlane(r.part0);
+  const int np = __builtin_amdgcn_readfirstlane(r.parts);
+  const int rel = v - groups * part0;
+  const int ts = rel % np;
+  w.g = rel / np;
+  w.u = u;
+  w.p0 = off + FFN_PART * ts;
+  w.n = min(FFN_PART, n - FFN_PART * ts);
+  w.tile0 = tile0 + (FFN_PART / 16) * ts;
   return true;
 }
 
 // Workgroups for up to `units` units: a multiple of N_XCD, so that every
 // XCD's run of xcd_unit has all its workgroups.
 inline unsigned ffn_grid(long long units) {
-  const long long per = (units + N_XCD * FF_WAVES - 1) / (N_XCD * FF_WAVES);
-  return (unsigned)(per * N_XCD);
+  return (unsigned)(((units + N_XCD - 1) / N_XCD) * N_XCD);
 }
 
-// One wavefront: FF_RT row tiles against NT token tiles, `ksteps` k-steps
-// of 32.  Token fragment (j, ks) at byte j * tstride + ks * 1024 + lane * 16
-// of resource rt.  Weights and tokens are requested D k-steps ahead of
-// their MFMAs, both at the same distance, so waiting for the oldest
+// One wavefront: FF_RT row tiles against NT token tiles over k-steps
+// k0 .. k0 + cnt - 1 (cnt a multiple of D).  Token fragment (j, ks) at
+// byte j * tstride + ks * 1024 + lane * 16 of resource rt.  Weights and
+// tokens are requested D k-steps ahead of their MFMAs, both at the same
+// distance: loads complete in issue order, so waiting for the oldest
 // k-step's data never waits for anything requested after it.
 template <int NT, int D, bool PACKED>
 __device__ __forceinline__ void stream_wave(const WeightSrc &ws, rsrc_t rt,
-                                            uint32_t tstride, int ksteps,
+                                            uint32_t tstride, int k0, int cnt,
                                             f32x4 (&acc)[FF_RT][FF_NT]) {
   const uint32_t tl = lane_id() * 16;
+  const int kend = k0 + cnt;
   bf16x8 wb[D][FF_RT], xb[D][NT];
 #pragma unroll
   for (int p = 0; p < D; ++p) {
 #pragma unroll
-    for (int t = 0; t < FF_RT; ++t) wb[p][t] = wload<PACKED>(ws, t, p);
+    for (int t = 0; t < FF_RT; ++t) wb[p][t] = wload<PACKED>(ws, t, k0 + p);
 #pragma unroll
-    for (int j = 0; j < NT; ++j) xb[p][j] = bload(rt, tl + j * tstride, (uint32_t)p * 1024u);
+    for (int j = 0; j < NT; ++j)
+      xb[p][j] = bload(rt, tl + j * tstride, (uint32_t)(k0 + p) * 1024u);
   }
-  int ks = 0;
-  for (; ks + D < ksteps; ks += D) {
+  int ks = k0;
+  for (; ks + D < kend; ks += D) {
 #pragma unroll
     for (int p = 0; p < D; ++p) {
 #pragma unroll
@@ -200,54 +212,82 @@ __device__ __forceinline__ void stream_wave(const WeightSrc &ws, rsrc_t rt,
 
 template <int NT, bool PACKED>
 __device__ __forceinline__ void stream_wave_d(const WeightSrc &ws, rsrc_t rt,
-                                              uint32_t tstride, int ksteps,
+                                              uint32_t tstride, int k0, int cnt,
                                               f32x4 (&acc)[FF_RT][FF_NT]) {
-  if (ksteps % 4 == 0) stream_wave<NT, 4, PACKED>(ws, rt, tstride, ksteps, acc);
-  else stream_wave<NT, 2, PACKED>(ws, rt, tstride, ksteps, acc);
+  if (cnt % 4 == 0) stream_wave<NT, 4, PACKED>(ws, rt, tstride, k0, cnt, acc);
+  else if (cnt % 2 == 0) stream_wave<NT, 2, PACKED>(ws, rt, tstride, k0, cnt, acc);
+  else stream_wave<NT, 1, PACKED>(ws, rt, tstride, k0, cnt, acc);
 }
 
-template <bool PACKED>
-__device__ __forceinline__ void stream_wave_nt(int nt, const WeightSrc &ws, rsrc_t rt,
-                                               uint32_t tstride, int ksteps,
-                                               f32x4 (&acc)[FF_RT][FF_NT]) {
-  switch (nt) {
-    case 1: stream_wave_d<1, PACKED>(ws, rt, tstride, ksteps, acc); break;
-    case 2: stream_wave_d<2, PACKED>(ws, rt, tstride, ksteps, acc); break;
-    case 3: stream_wave_d<3, PACKED>(ws, rt, tstride, ksteps, acc); break;
-    default: stream_wave_d<4, PACKED>(ws, rt, tstride, ksteps, acc); break;
-  }
-}
-
-__device__ __forceinline__ void zero_acc(f32x4 (&acc)[FF_RT][FF_NT]) {
+// This wavefront's share of a unit's contraction (ksteps k-steps of 32)
+// when S wavefronts split it: k-steps [w ksteps / S, (w + 1) ksteps / S);
+// possibly empty.
+template <int S, bool PACKED>
+__device__ __forceinline__ void stream_share(int nt, const WeightSrc &ws, rsrc_t rt,
+                                             uint32_t tstride, int ksteps,
+                                             f32x4 (&acc)[FF_RT][FF_NT]) {
 #pragma unroll
   for (int t = 0; t < FF_RT; ++t)
 #pragma unroll
     for (int j = 0; j < FF_NT; ++j) acc[t][j] = f32x4{0, 0, 0, 0};
+  const int w = wave_id();
+  const int k0 = __builtin_amdgcn_readfirstlane(ksteps * w / S);
+  const int cnt = __builtin_amdgcn_readfirstlane(ksteps * (w + 1) / S) - k0;
+  if (cnt <= 0) return;
+  switch (nt) {
+    case 1: stream_wave_d<1, PACKED>(ws, rt, tstride, k0, cnt, acc); break;
+    case 2: stream_wave_d<2, PACKED>(ws, rt, tstride, k0, cnt, acc); break;
+    case 3: stream_wave_d<3, PACKED>(ws, rt, tstride, k0, cnt, acc); break;
+    default: stream_wave_d<4, PACKED>(ws, rt, tstride, k0, cnt, acc); break;
+  }
+}
+
+// Partial sums of the S wavefronts: [wave][row tile][token tile][lane]
+template <int S>
+struct Partials {
+  f32x4 v[S][FF_RT][FF_NT][WAVE];
+};
+
+template <int S>
+__device__ __forceinline__ void put_partials(Partials<S> &sh, int nt,
+                                             const f32x4 (&acc)[FF_RT][FF_NT]) {
+  const int w = wave_id(), l = lane_id();
+#pragma unroll
+  for (int t = 0; t < FF_RT; ++t)
+#pragma unroll
+    for (int j = 0; j < FF_NT; ++j)
+      if (j < nt) sh.v[w][t][j][l] = acc[t][j];
+}
+
+// Sum of the partials of row tile t, token tile j, in wave order.
+template <int S>
+__device__ __forceinline__ f32x4 sum_partials(const Partials<S> &sh, int t, int j) {
+  const int l = lane_id();
+  f32x4 r = sh.v[0][t][j][l];
+#pragma unroll
+  for (int w = 1; w < S; ++w) r += sh.v[w][t][j][l];
+  return r;
 }
 
 // gate/up: row group g = gate rows 32 g .. 32 g + 31 (tiles 0, 1) and up
 // rows I + 32 g .. I + 32 g + 31 (tiles 2, 3).  Writes H in fragment order:
 // SwiGLU column i = 32 g + 16 t + 4 (l / 16) + r of pair tk sits in
 // fragment (tile of tk, k-step g), lane tk % 16 + 16 (2 t + (l / 16) / 2),
-// element 4 ((l / 16) % 2) + r.
+// element 4 ((l / 16) % 2) + r.  Wavefront w finishes the gate tiles
+// t = w, w + GU_SPLIT, .. < 2, each with its up tile t + 2.
 template <bool PACKED>
-__global__ __launch_bounds__(FF_WAVES * WAVE, 2)
-void k_gateup_bf16(int d, int I, int E, int budget, const uint16_t *__restrict__ w13,
-                   const int32_t *__restrict__ sel_ids,
-                   const int32_t *__restrict__ n_sel_p,
-                   const int32_t *__restrict__ offsets,
-                   const int32_t *__restrict__ tile_base,
-                   const int32_t *__restrict__ part_base,
+__global__ __launch_bounds__(GU_SPLIT * WAVE, 2)
+void k_gateup_bf16(int d, int I, int E, const uint16_t *__restrict__ w13,
+                   const PartRec *__restrict__ parts,
+                   const int32_t *__restrict__ n_parts,
                    const uint16_t *__restrict__ xp, uint16_t *__restrict__ hp) {
+  __shared__ Partials<GU_SPLIT> sh;
   const int groups = I / 32;
-  const int n_sel = min(max(*n_sel_p, 0), budget);
   Unit un;
-  if (!find_unit(groups, n_sel, part_base, un)) return;
-  const int u = __builtin_amdgcn_readfirstlane(sel_ids[un.s]);
+  if (!find_unit(groups, parts, n_parts, un)) return;
+  const int u = un.u, n = un.n, tile0 = un.tile0;
   if (u < 0 || u >= E) return;   // only for a plan not made by base_select
-  const int n = __builtin_amdgcn_readfirstlane(offsets[un.s + 1] - offsets[un.s]);
-  const int tbeg = FF_TOK * un.ts;
-  const int nt = min(FF_NT, (n - tbeg + 15) / 16);
+  const int nt = (n + 15) / 16;
   const int lane = lane_id(), row = lane & 15, g = un.g;
   WeightSrc ws;
   if (PACKED) {
@@ -261,54 +301,47 @@ void k_gateup_bf16(int d, int I, int E, int budget, const uint16_t *__restrict__
                           (uint32_t)(16 * d * 2));
     ws.voff = (uint32_t)row * (uint32_t)(d * 2) + (uint32_t)(lane >> 4) * 16u;
   }
-  const int tile0 = __builtin_amdgcn_readfirstlane(tile_base[un.s]) + tbeg / 16;
   const uint32_t tstride = (uint32_t)(d / 32) * 1024u;        // one tile
   const rsrc_t rt = make_rsrc(xp + (size_t)tile0 * (d / 32) * 512, (uint32_t)nt * tstride);
   f32x4 acc[FF_RT][FF_NT];
-  zero_acc(acc);
-  stream_wave_nt<PACKED>(nt, ws, rt, tstride, d / 32, acc);
+  stream_share<GU_SPLIT, PACKED>(nt, ws, rt, tstride, d / 32, acc);
+  put_partials(sh, nt, acc);
+  __syncthreads();
+  for (int t = wave_id(); t < 2; t += GU_SPLIT)
 #pragma unroll
   for (int j = 0; j < FF_NT; ++j) {
-    const int tk = tbeg + 16 * j + row;
+    const int tk = 16 * j + row;
     if (j < nt && tk < n) {
+      const f32x4 ga = sum_partials(sh, t, j), up = sum_partials(sh, t + 2, j);
+      uint16_t h[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) h[r] = f32_to_bf16(silu(ga[r]) * up[r]);
+      u32x2 pk = {(uint32_t)h[0] | ((uint32_t)h[1] << 16),
+                  (uint32_t)h[2] | ((uint32_t)h[3] << 16)};
       uint16_t *frag = hp + (((size_t)(tile0 + j) * (I / 32) + g) * WAVE) * 8;
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        uint16_t h[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          h[r] = f32_to_bf16(silu(acc[t][j][r]) * acc[t + 2][j][r]);
-        u32x2 pk = {(uint32_t)h[0] | ((uint32_t)h[1] << 16),
-                    (uint32_t)h[2] | ((uint32_t)h[3] << 16)};
-        const int l2 = row + 16 * (2 * t + (lane >> 5));
-        *reinterpret_cast<u32x2 *>(frag + l2 * 8 + 4 * ((lane >> 4) & 1)) = pk;
-      }
+      const int l2 = row + 16 * (2 * t + (lane >> 5));
+      *reinterpret_cast<u32x2 *>(frag + l2 * 8 + 4 * ((lane >> 4) & 1)) = pk;
     }
   }
 }
 
 // down: row group g = rows 64 g .. 64 g + 63 of W_d (tiles 0..3); tokens
-// are the SwiGLU activations in fragment order.
+// are the SwiGLU activations in fragment order.  Wavefront w finishes the
+// row tiles t = w, w + DN_SPLIT, ...
 template <bool PACKED>
-__global__ __launch_bounds__(FF_WAVES * WAVE, 2)
-void k_down_bf16(int d, int I, int E, int budget, const uint16_t *__restrict__ w2,
-                 const int32_t *__restrict__ sel_ids,
-                 const int32_t *__restrict__ n_sel_p,
-                 const int32_t *__restrict__ offsets,
-                 const int32_t *__restrict__ tile_base,
-                 const int32_t *__restrict__ part_base,
+__global__ __launch_bounds__(DN_SPLIT * WAVE, 2)
+void k_down_bf16(int d, int I, int E, const uint16_t *__restrict__ w2,
+                 const PartRec *__restrict__ parts,
+                 const int32_t *__restrict__ n_parts,
                  const float *__restrict__ pair_gate,
                  const uint16_t *__restrict__ hp, float *__restrict__ pairbuf) {
+  __shared__ Partials<DN_SPLIT> sh;
   const int groups = d / 64;
-  const int n_sel = min(max(*n_sel_p, 0), budget);
   Unit un;
-  if (!find_unit(groups, n_sel, part_base, un)) return;
-  const int u = __builtin_amdgcn_readfirstlane(sel_ids[un.s]);
+  if (!find_unit(groups, parts, n_parts, un)) return;
+  const int u = un.u, n = un.n, tile0 = un.tile0, p0 = un.p0;
   if (u < 0 || u >= E) return;   // only for a plan not made by base_select
-  const int p0 = __builtin_amdgcn_readfirstlane(offsets[un.s]);
-  const int n = __builtin_amdgcn_readfirstlane(offsets[un.s + 1]) - p0;
-  const int tbeg = FF_TOK * un.ts;
-  const int nt = min(FF_NT, (n - tbeg + 15) / 16);
+  const int nt = (n + 15) / 16;
   const int lane = lane_id(), row = lane & 15, g = un.g;
   WeightSrc ws;
   if (PACKED) {
@@ -321,24 +354,22 @@ void k_down_bf16(int d, int I, int E, int budget, const uint16_t *__restrict__ w
       ws.r[t] = make_rsrc(w2 + ((size_t)u * d + 64 * g + 16 * t) * I, (uint32_t)(16 * I * 2));
     ws.voff = (uint32_t)row * (uint32_t)(I * 2) + (uint32_t)(lane >> 4) * 16u;
   }
-  const int tile0 = __builtin_amdgcn_readfirstlane(tile_base[un.s]) + tbeg / 16;
   const uint32_t tstride = (uint32_t)(I / 32) * 1024u;
   const rsrc_t rt = make_rsrc(hp + (size_t)tile0 * (I / 32) * 512, (uint32_t)nt * tstride);
   f32x4 acc[FF_RT][FF_NT];
-  zero_acc(acc);
-  stream_wave_nt<PACKED>(nt, ws, rt, tstride, I / 32, acc);
+  stream_share<DN_SPLIT, PACKED>(nt, ws, rt, tstride, I / 32, acc);
+  put_partials(sh, nt, acc);
+  __syncthreads();
+  for (int t = wave_id(); t < FF_RT; t += DN_SPLIT)
 #pragma unroll
   for (int j = 0; j < FF_NT; ++j) {
-    const int tk = tbeg + 16 * j + row;
+    const int tk = 16 * j + row;
     if (j < nt && tk < n) {
+      const f32x4 o = sum_partials(sh, t, j);
       const float gt = pair_gate[p0 + tk];
-#pragma unroll
-      for (int t = 0; t < FF_RT; ++t) {
-        float4 o = {gt * acc[t][j][0], gt * acc[t][j][1], gt * acc[t][j][2],
-                    gt * acc[t][j][3]};
-        *reinterpret_cast<float4 *>(pairbuf + (size_t)(p0 + tk) * d + 64 * g + 16 * t +
-                                    4 * (lane >> 4)) = o;
-      }
+      float4 v = {gt * o[0], gt * o[1], gt * o[2], gt * o[3]};
+      *reinterpret_cast<float4 *>(pairbuf + (size_t)(p0 + tk) * d + 64 * g + 16 * t +
+                                  4 * (lane >> 4)) = v;
     }
   }
 }
@@ -435,13 +466,11 @@ void k_combine(int B, int d, int K, const int32_t *__restrict__ pair_of,
 }
 
 hipError_t launch_gather(const void *x, int B, int d, int K, int budget,
-                         const int32_t *n_sel, const int32_t *offsets,
-                         const int32_t *pair_tok, const int32_t *tile_base,
-                         void *xp, hipStream_t st) {
-  const long long waves = (long long)ffn_max_tiles(B, K, budget) * (d / 32);
+                         const PartRec *parts, const int32_t *n_parts,
+                         const int32_t *pair_tok, void *xp, hipStream_t st) {
+  const long long waves = (long long)ffn_max_parts(B, K, budget) * (d / 32);
   hipLaunchKernelGGL(k_gather, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, st,
-                     (const uint16_t *)x, d, budget, n_sel, offsets, pair_tok,
-                     tile_base, (uint16_t *)xp);
+                     (const uint16_t *)x, d, parts, n_parts, pair_tok, (uint16_t *)xp);
   return hipGetLastError();
 }
 
@@ -449,15 +478,14 @@ hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
                          int I, int E, int K, int budget, const void *w13,
                          const int32_t *sel_ids, const int32_t *n_sel,
                          const int32_t *offsets, const int32_t *pair_tok,
-                         const int32_t *tile_base, const int32_t *part_base,
+                         const PartRec *parts, const int32_t *n_parts,
                          const void *xp, void *H, hipStream_t st) {
   if (bf16) {
     const long long units = (long long)ffn_max_parts(B, K, budget) * (I / 32);
     hipLaunchKernelGGL(packed ? k_gateup_bf16<true> : k_gateup_bf16<false>,
-                       dim3(ffn_grid(units)),
-                       dim3(FF_WAVES * WAVE), 0, st, d, I, E, budget,
-                       (const uint16_t *)w13, sel_ids, n_sel, offsets, tile_base,
-                       part_base, (const uint16_t *)xp, (uint16_t *)H);
+                       dim3(ffn_grid(units)), dim3(GU_SPLIT * WAVE), 0, st, d, I, E,
+                       (const uint16_t *)w13, parts, n_parts, (const uint16_t *)xp,
+                       (uint16_t *)H);
   } else {
     hipLaunchKernelGGL(k_gateup_f32, dim3(budget, (I + F32_ROWS - 1) / F32_ROWS),
                        dim3(F32_ROWS * F32_TG), 0, st, (const float *)x, d, I,
@@ -470,16 +498,15 @@ hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
 hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K,
                        int budget, const void *w2, const int32_t *sel_ids,
                        const int32_t *n_sel, const int32_t *offsets,
-                       const int32_t *tile_base, const int32_t *part_base,
+                       const PartRec *parts, const int32_t *n_parts,
                        const float *pair_gate, const void *H, float *pairbuf,
                        hipStream_t st) {
   if (bf16) {
     const long long units = (long long)ffn_max_parts(B, K, budget) * (d / 64);
     hipLaunchKernelGGL(packed ? k_down_bf16<true> : k_down_bf16<false>,
-                       dim3(ffn_grid(units)),
-                       dim3(FF_WAVES * WAVE), 0, st, d, I, E, budget,
-                       (const uint16_t *)w2, sel_ids, n_sel, offsets, tile_base,
-                       part_base, pair_gate, (const uint16_t *)H, pairbuf);
+                       dim3(ffn_grid(units)), dim3(DN_SPLIT * WAVE), 0, st, d, I, E,
+                       (const uint16_t *)w2, parts, n_parts, pair_gate,
+                       (const uint16_t *)H, pairbuf);
   } else {
     hipLaunchKernelGGL(k_down_f32, dim3(budget, (d + F32_ROWS - 1) / F32_ROWS),
                        dim3(F32_ROWS * F32_TG), 0, st, d, I, E,

@@ -19,13 +19,34 @@ inline int ffn_max_parts(int B, int K, int budget) {
   return (B * K + FFN_PART - 1) / FFN_PART + budget;
 }
 
-hipError_t launch_route_logits(bool bf16, const void *x, int B, int d,
-                               const float *W, const float *beta, int E,
-                               float *logits, hipStream_t st);
-hipError_t launch_token(bool bf16, const void *x, int B, int d, int E, int K,
-                        int norm_topk, const float *logits, int32_t *ids,
-                        float *w, const float *A, const float *bp, float *cost,
-                        int mode, hipStream_t st);
+// The FFN's part table: entry q (one per 64-token part) describes the kept
+// slot s that part q belongs to, so that any FFN work unit decodes from the
+// one entry:
+//   u      the slot's expert
+//   off    its first pair (pairs off .. off + n - 1 in the compacted order)
+//   n      its pair count (>= 1)
+//   tile0  its first 16-pair tile in the fragment-ordered operands
+//   part0  its first part (the slot's parts are part0 .. part0 + parts - 1;
+//          part part0 + i covers its pairs 64 i .. 64 i + 63)
+//   parts  ceil(n / 64)
+struct alignas(32) PartRec {
+  int32_t u, off, n, tile0, part0, parts, pad0, pad1;
+};
+
+// rows: n_router of W_r (-> logits [B][n_router], + beta) then n_pred of A
+// (-> q [B][n_pred]); ss [B] = ||x||^2 when non-null
+hipError_t launch_scores(bool bf16, const void *x, int B, int d, const float *Wr,
+                         const float *beta, int n_router, const float *A,
+                         int n_pred, float *logits, float *q, float *ss,
+                         hipStream_t st);
+// mode bit 0: top-K + weights from logits; bit 1: costs from q / ss
+hipError_t launch_tail(int B, int E, int K, int norm_topk, const float *logits,
+                       const float *q, const float *ss, const float *bp,
+                       int32_t *ids, float *w, float *cost, int mode,
+                       hipStream_t st);
+hipError_t launch_predict(bool bf16, const void *x, int B, int d, int E, int K,
+                          const int32_t *ids, const float *w, const float *A,
+                          const float *bp, float *cost, hipStream_t st);
 hipError_t launch_select(int B, int K, int E, const int32_t *ids,
                          const float *cost, int budget, float *scores,
                          int32_t *counts, int32_t *sel_ids, int32_t *n_sel,
@@ -39,24 +60,23 @@ hipError_t launch_compact(int B, int K, int budget, const int32_t *exec_ids,
                           const float *exec_gates, const int32_t *slot_of,
                           const int32_t *n_sel, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
-                          int32_t *pair_of, int32_t *tile_base,
-                          int32_t *part_base, hipStream_t st);
+                          int32_t *pair_of, const int32_t *sel_ids,
+                          PartRec *parts, int32_t *n_parts, hipStream_t st);
 hipError_t launch_gather(const void *x, int B, int d, int K, int budget,
-                         const int32_t *n_sel, const int32_t *offsets,
-                         const int32_t *pair_tok, const int32_t *tile_base,
-                         void *xp, hipStream_t st);
+                         const PartRec *parts, const int32_t *n_parts,
+                         const int32_t *pair_tok, void *xp, hipStream_t st);
 hipError_t launch_pack(const void *w13, const void *w2, void *w13p, void *w2p,
                        int E, int d, int I, hipStream_t st);
 hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
                          int I, int E, int K, int budget, const void *w13,
                          const int32_t *sel_ids, const int32_t *n_sel,
                          const int32_t *offsets, const int32_t *pair_tok,
-                         const int32_t *tile_base, const int32_t *part_base,
+                         const PartRec *parts, const int32_t *n_parts,
                          const void *xp, void *H, hipStream_t st);
 hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K,
                        int budget, const void *w2, const int32_t *sel_ids,
                        const int32_t *n_sel, const int32_t *offsets,
-                       const int32_t *tile_base, const int32_t *part_base,
+                       const PartRec *parts, const int32_t *n_parts,
                        const float *pair_gate, const void *H, float *pairbuf,
                        hipStream_t st);
 hipError_t launch_combine(bool bf16, int B, int d, int K,

@@ -18,61 +18,93 @@
 namespace basek {
 
 constexpr int SEL_THREADS = 1024;
+constexpr int SEL_PAD = WAVE + 1;                 // LDS row of one chunk tree
+constexpr int SEL_V = 2 * 128 * SEL_PAD;          // chunk-matrix capacity (floats)
 
+// One workgroup.  Chunk c (tokens 64c .. 64c + 63) of expert u is the row
+// V[c][u][0..63] (position j: the cost of token 64c + j if it routes u, else
+// +0); one thread per (chunk, expert) adds its row by the halving tree, and
+// the chunk sums are added to D_hat_u in ascending chunk order.  The kept
+// set is ranked with 64-bit keys whose unsigned order is (D_hat desc, index
+// asc).
 __global__ __launch_bounds__(SEL_THREADS)
 void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
               const float *__restrict__ cost, int budget,
               float *__restrict__ scores, int32_t *__restrict__ counts,
               int32_t *__restrict__ sel_ids, int32_t *__restrict__ n_sel_out,
               int32_t *__restrict__ slot_of) {
-  __shared__ float V[MAX_E * WAVE];   // chunk matrix: expert x token-in-chunk
+  __shared__ float V[SEL_V];
+  __shared__ float CS[SEL_THREADS];
   __shared__ float D[MAX_E];
   __shared__ int cnt[MAX_E];
+  __shared__ uint64_t key[MAX_E];
+  __shared__ int rnk[MAX_E];
   __shared__ int n_union;
-  const int tid = threadIdx.x, lane = lane_id(), wave = wave_id();
-  const int nwaves = SEL_THREADS / WAVE;
+  const int tid = threadIdx.x;
 
-  for (int u = tid; u < E; u += SEL_THREADS) { cnt[u] = 0; D[u] = 0.0f; }
+  for (int u = tid; u < E; u += SEL_THREADS) { cnt[u] = 0; D[u] = 0.0f; rnk[u] = 0; }
   if (tid == 0) n_union = 0;
-  __syncthreads();
-  for (int p = tid; p < B * K; p += SEL_THREADS) {
-    const int u = ids[p];
-    if (u >= 0 && u < E) atomicAdd(&cnt[u], 1);
-  }
-
   const int nchunks = (B + WAVE - 1) / WAVE;
-  for (int c = 0; c < nchunks; ++c) {
-    for (int i = tid; i < E * WAVE; i += SEL_THREADS) V[i] = 0.0f;
+  // chunks per batch: bounded by V, by one thread per token and by one
+  // thread per (chunk, expert)
+  const int cb = max(1, min(min(nchunks, SEL_V / (E * SEL_PAD)),
+                            min(SEL_THREADS / WAVE, SEL_THREADS / E)));
+  for (int c0 = 0; c0 < nchunks; c0 += cb) {
+    const int nb = min(cb, nchunks - c0);
+    for (int i = tid; i < nb * E * SEL_PAD; i += SEL_THREADS) V[i] = 0.0f;
     __syncthreads();
-    for (int q = tid; q < WAVE * K; q += SEL_THREADS) {
-      const int t = c * WAVE + q / K;
-      if (t < B) {
-        const int u = ids[(size_t)t * K + q % K];
-        if (u >= 0 && u < E) V[u * WAVE + (t - c * WAVE)] = cost[(size_t)t * K + q % K];
+    // one thread per token: its routes in rank order (a repeated expert
+    // keeps its last cost, and counts every time)
+    const int j = tid % WAVE, cl = tid / WAVE, t = (c0 + cl) * WAVE + j;
+    if (cl < nb && t < B) {
+      for (int k = 0; k < K; ++k) {
+        const int u = ids[(size_t)t * K + k];
+        if (u >= 0 && u < E) {
+          V[(cl * E + u) * SEL_PAD + j] = cost[(size_t)t * K + k];
+          atomicAdd(&cnt[u], 1);
+        }
       }
     }
     __syncthreads();
-    // row u always belongs to the same wavefront, so chunks are added to
-    // D[u] in ascending order
-    for (int u = wave; u < E; u += nwaves) {
-      const float s = wave_tree_sum(V[u * WAVE + lane]);
-      if (lane == 0) D[u] = (c == 0) ? s : D[u] + s;
+    if (tid < nb * E) {
+      float v[WAVE];
+#pragma unroll
+      for (int q = 0; q < WAVE; ++q) v[q] = V[tid * SEL_PAD + q];
+#pragma unroll
+      for (int h = WAVE / 2; h >= 1; h >>= 1)
+#pragma unroll
+        for (int q = 0; q < h; ++q) v[q] = v[q] + v[q + h];
+      CS[tid] = v[0];
     }
+    __syncthreads();
+    for (int u = tid; u < E; u += SEL_THREADS)
+      for (int c = 0; c < nb; ++c)
+        D[u] = (c0 + c == 0) ? CS[c * E + u] : D[u] + CS[c * E + u];
     __syncthreads();
   }
 
-  for (int u = tid; u < E; u += SEL_THREADS)
+  for (int u = tid; u < E; u += SEL_THREADS) {
+    key[u] = cnt[u] > 0 ? rank_key(D[u], u) : 0;   // 0: ranks after every expert
     if (cnt[u] > 0) atomicAdd(&n_union, 1);
+  }
   __syncthreads();
   const int n_sel = min(budget, n_union);
+  {
+    // four threads per expert, each over a quarter of the candidates
+    const int u = tid >> 2, part = tid & 3;
+    if (u < E && cnt[u] > 0) {
+      const uint64_t ku = key[u];
+      int r = 0;
+      for (int v = part; v < E; v += 4) r += key[v] > ku;
+      atomicAdd(&rnk[u], r);
+    }
+  }
+  __syncthreads();
   for (int u = tid; u < E; u += SEL_THREADS) {
     int slot = -1;
-    if (cnt[u] > 0) {
-      const float du = D[u];
-      int r = 0;
-      for (int v = 0; v < E; ++v)
-        r += (cnt[v] > 0) && ranks_before(D[v], v, du, u);
-      if (r < n_sel) { slot = r; sel_ids[r] = u; }
+    if (cnt[u] > 0 && rnk[u] < n_sel) {
+      slot = rnk[u];
+      sel_ids[slot] = u;
     }
     slot_of[u] = slot;
     scores[u] = D[u];
@@ -84,103 +116,105 @@ void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
 
 constexpr int BF_WAVES = 4;
 
+// One wavefront per token.  The kept experts (slot_of >= 0) are packed into
+// an LDS list with their keys (logit, index) for this token; each is ranked
+// among them, and the first min(K, n_sel) by rank are executed in rank
+// order.  Under the drop rule the token executes its routed experts that
+// were kept, in routing order.  Gates: exp(l_v - l_max) over the original
+// denominator (its top-K, or all E for a plain softmax router) or, with
+// renormalisation, over the executed experts.
 __global__ __launch_bounds__(BF_WAVES * WAVE)
 void k_backfill(int B, int E, int K, int norm_topk, int flags,
                 const float *__restrict__ logits, const int32_t *__restrict__ ids,
                 const int32_t *__restrict__ slot_of,
                 const int32_t *__restrict__ n_sel_p,
                 int32_t *__restrict__ exec_ids, float *__restrict__ exec_gates) {
-  const int lane = lane_id();
-  const int t = blockIdx.x * BF_WAVES + wave_id();
-  if (t >= B) return;
+  __shared__ __attribute__((aligned(16))) uint64_t kk[BF_WAVES][MAX_E];
+  __shared__ int ke[BF_WAVES][MAX_E];
+  __shared__ int xs[BF_WAVES][MAX_K];
+  __shared__ float num_s[BF_WAVES][MAX_K];
+  __shared__ float den_s[BF_WAVES][MAX_K];
+  __shared__ int nx_s[BF_WAVES];
+  const int lane = lane_id(), wv = wave_id();
+  const int t = blockIdx.x * BF_WAVES + wv;
+  const int tc = min(t, B - 1);          // every wavefront takes part in the barriers
   const int n_sel = *n_sel_p;
-  const float *lt = logits + (size_t)t * E;
+  const float *lt = logits + (size_t)tc * E;
 
-  int R[MAX_K];
-#pragma unroll
-  for (int k = 0; k < MAX_K; ++k) {
-    int u = (k < K) ? ids[(size_t)t * K + k] : 0;
-    R[k] = (u >= 0 && u < E) ? u : 0;
+  // lane k < K: routed expert k (out-of-range ids read expert 0)
+  int r_k = 0;
+  if (lane < K) {
+    const int u = ids[(size_t)tc * K + lane];
+    r_k = (u >= 0 && u < E) ? u : 0;
   }
-  const float lmax = lt[R[0]];
+  const int r0 = __shfl(r_k, 0, WAVE);
+  const float lmax = lt[r0];
 
-  int X[MAX_K];
-  int nx = 0;
+  if (flags & 2) {   // drop: the routed experts that were kept, routing order
+    const bool kept = lane < K && slot_of[r_k] >= 0;
+    const uint64_t m = __ballot(kept);
+    if (kept) xs[wv][__popcll(m & ((1ull << lane) - 1))] = r_k;
+    if (lane == 0) nx_s[wv] = __popcll(m);
+  } else {           // backfill: first min(K, n_sel) kept experts by rank
+    int base = 0;
 #pragma unroll
-  for (int k = 0; k < MAX_K; ++k) X[k] = -1;
-
-  if (flags & 2) {   // drop: the routed experts that were kept, rank order
-#pragma unroll
-    for (int k = 0; k < MAX_K; ++k)
-      if (k < K && slot_of[R[k]] >= 0) {
-#pragma unroll
-        for (int q = 0; q < MAX_K; ++q)
-          if (q == nx) X[q] = R[k];
-        ++nx;
-      }
-  } else {           // backfill: first min(K, n_sel) kept experts in rank order
-    float lv[4];
-    bool cand[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < MAX_E / WAVE; ++i) {
       const int e = lane + WAVE * i;
-      cand[i] = (e < E) && slot_of[e] >= 0;
-      lv[i] = (e < E) ? lt[e] : 0.0f;
-    }
-    const int kp = min(K, n_sel);
-#pragma unroll
-    for (int k = 0; k < MAX_K; ++k) {
-      if (k < kp && nx == k) {
-        float bv = -INFINITY;
-        int bi = 0x7FFFFFFF;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int e = lane + WAVE * i;
-          if (cand[i] && ranks_before(lv[i], e, bv, bi)) { bv = lv[i]; bi = e; }
-        }
-        wave_argbest(bv, bi);
-        if (bi < E) {   // a kept expert was left (always, for a consistent plan)
-          X[k] = bi;
-          nx = k + 1;
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (lane + WAVE * i == bi) cand[i] = false;
+      const bool kept = e < E && slot_of[e] >= 0;
+      const uint64_t m = __ballot(kept);
+      if (kept) {
+        const int pos = base + __popcll(m & ((1ull << lane) - 1));
+        kk[wv][pos] = rank_key(lt[e], e);
+        ke[wv][pos] = e;
       }
+      base += __popcll(m);
+    }
+    const int n_kept = base;
+    if (lane == 0) nx_s[wv] = min(min(K, n_sel), n_kept);
+    if (n_kept & 1) { if (lane == 0) kk[wv][n_kept] = 0; }
+    __syncthreads();
+    const int kp = min(K, n_sel);
+    for (int s = lane; s < n_kept; s += WAVE) {
+      const uint64_t ks = kk[wv][s];
+      int r = 0;
+      for (int f = 0; f < n_kept; f += 2) {
+        const u32x4 o = *reinterpret_cast<const u32x4 *>(&kk[wv][f]);
+        r += (((uint64_t)o.y << 32 | o.x) > ks);
+        r += (((uint64_t)o.w << 32 | o.z) > ks);
+      }
+      if (r < kp) xs[wv][r] = ke[wv][s];
     }
   }
+  __syncthreads();
+  const int nx = nx_s[wv];
 
   // gates: numerators exp(l_v - l_max); denominator per flags
-  float num[MAX_K];
-#pragma unroll
-  for (int j = 0; j < MAX_K; ++j)
-    num[j] = (j < nx) ? base_exp(lt[X[j]] - lmax) : 0.0f;
+  float num = 0.0f;
+  if (lane < nx) {
+    num = base_exp(lt[xs[wv][lane]] - lmax);
+    num_s[wv][lane] = num;
+  }
+  if (lane < K) den_s[wv][lane] = base_exp(lt[r_k] - lmax);
+  __syncthreads();
   float S;
-  if (flags & 1) {
+  if (flags & 1) {          // renormalised over the executed experts
     S = 0.0f;
-#pragma unroll
-    for (int j = 0; j < MAX_K; ++j)
-      if (j < nx) S = S + num[j];
-  } else if (norm_topk) {
+    for (int j = 0; j < nx; ++j) S = S + num_s[wv][j];
+  } else if (norm_topk) {   // the router's top-K denominator
     S = 0.0f;
-#pragma unroll
-    for (int k = 0; k < MAX_K; ++k)
-      if (k < K) S = S + base_exp(lt[R[k]] - lmax);
-  } else {
+    for (int k = 0; k < K; ++k) S = S + den_s[wv][k];
+  } else {                  // the router's full softmax denominator
     float part = 0.0f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < MAX_E / WAVE; ++i) {
       const int e = lane + WAVE * i;
       if (e < E) part = part + base_exp(lt[e] - lmax);
     }
     S = wave_tree_sum(part);
   }
-#pragma unroll
-  for (int j = 0; j < MAX_K; ++j) {
-    if (j < K && lane == j) {
-      exec_ids[(size_t)t * K + j] = (j < nx) ? X[j] : -1;
-      exec_gates[(size_t)t * K + j] = (j < nx) ? num[j] / S : 0.0f;
-    }
+  if (t < B && lane < K) {
+    exec_ids[(size_t)t * K + lane] = (lane < nx) ? xs[wv][lane] : -1;
+    exec_gates[(size_t)t * K + lane] = (lane < nx) ? num / S : 0.0f;
   }
 }
 
@@ -222,7 +256,8 @@ void k_compact(int B, int K, int budget, const int32_t *__restrict__ exec_ids,
                const int32_t *__restrict__ n_sel_p,
                int32_t *__restrict__ offsets, int32_t *__restrict__ pair_tok,
                float *__restrict__ pair_gate, int32_t *__restrict__ pair_of,
-               int32_t *__restrict__ tile_base, int32_t *__restrict__ part_base) {
+               const int32_t *__restrict__ sel_ids, PartRec *__restrict__ parts,
+               int32_t *__restrict__ n_parts) {
   // bits[s][w]: bit (t & 31) of word w = t >> 5 is set when token t runs slot s
   __shared__ uint32_t bits[MAX_E * CP_WORDS];
   __shared__ int pre[MAX_E * CP_WORDS];
@@ -264,10 +299,20 @@ void k_compact(int B, int K, int budget, const int32_t *__restrict__ exec_ids,
     wave_scan_slots(cnt, n_sel, FFN_PART, pb);    // FFN token parts
   }
   __syncthreads();
-  for (int s = tid; s <= budget; s += CP_THREADS) {
-    tile_base[s] = (s < n_sel) ? tb[s] : tb[MAX_E];
-    part_base[s] = (s < n_sel) ? pb[s] : pb[MAX_E];
+  // the FFN's part table: every part of slot s gets the slot's entry
+  for (int s = wave_id(); s < n_sel; s += CP_THREADS / WAVE) {
+    const int np = pb[s + 1] - pb[s];
+    PartRec r;
+    r.u = sel_ids[s];
+    r.off = off[s];
+    r.n = cnt[s];
+    r.tile0 = tb[s];
+    r.part0 = pb[s];
+    r.parts = np;
+    r.pad0 = r.pad1 = 0;
+    for (int i = lane; i < np; i += WAVE) parts[pb[s] + i] = r;
   }
+  if (tid == 0) *n_parts = pb[MAX_E];
   const int total = off[MAX_E];
   for (int s = tid; s <= budget; s += CP_THREADS)
     offsets[s] = (s < n_sel) ? off[s] : total;
@@ -313,11 +358,11 @@ hipError_t launch_compact(int B, int K, int budget, const int32_t *exec_ids,
                           const float *exec_gates, const int32_t *slot_of,
                           const int32_t *n_sel, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
-                          int32_t *pair_of, int32_t *tile_base,
-                          int32_t *part_base, hipStream_t st) {
+                          int32_t *pair_of, const int32_t *sel_ids,
+                          PartRec *parts, int32_t *n_parts, hipStream_t st) {
   hipLaunchKernelGGL(k_compact, dim3(1), dim3(CP_THREADS), 0, st, B, K, budget,
                      exec_ids, exec_gates, slot_of, n_sel, offsets, pair_tok,
-                     pair_gate, pair_of, tile_base, part_base);
+                     pair_gate, pair_of, sel_ids, parts, n_parts);
   return hipGetLastError();
 }
 

@@ -1,0 +1,292 @@
+// Router logits, predictor dot products and the per-token tail of the
+// scoring path (Sec. 3.1 router; Sec. 3.4, eq. log_energy_predictor).
+//
+// k_scores  every dot product the scoring path needs for a batch, as a tiled
+//           batch x rows product: rows are the router matrix (logit
+//           l[t][e] = x_t . W_r[e] + beta_e) and the predictor matrix
+//           (q[t][e] = x_t . a_e, for every expert: the dense product costs
+//           about as much as the router and does not wait for top-K), plus
+//           ||x_t||^2.
+// k_tail    one wavefront per token: top-K by exact ranks, router weights,
+//           then the cost of each routed pair, cost = w^2 exp(q[t][u] /
+//           ||x_t|| + b_u), one lane per pair.
+//
+// Fixed fp32 order of every dot product of length d: partial j (0..63) owns
+// the elements 256m + 4j + r (r = 0..3) and accumulates them in ascending
+// element order with single-rounding FMA from +0; the 64 partials are then
+// joined by the halving tree "s[j] = s[j] + s[j + h], j < h" for h = 32 ..
+// 1.  Here lane j of a wavefront holds partial j of up to 72 dot products at
+// once; the trees run through LDS (a transpose), one dot product per lane.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace basek {
+
+constexpr int SC_T = 8;        // tokens per wavefront tile
+constexpr int SC_R = 8;        // matrix rows per wavefront tile
+constexpr int SC_WAVES = 4;    // wavefronts per workgroup (row direction)
+constexpr int SC_DOTS = SC_T * SC_R + SC_T;   // + ||x||^2 of the tile's tokens
+constexpr int SC_PAD = WAVE + 1;              // LDS row of one dot's partials
+
+// The halving tree over 64 values held by one lane.
+__device__ __forceinline__ float tree64(float (&s)[WAVE]) {
+#pragma unroll
+  for (int h = WAVE / 2; h >= 1; h >>= 1)
+#pragma unroll
+    for (int j = 0; j < h; ++j) s[j] = s[j] + s[j + h];
+  return s[0];
+}
+
+// Lane i: the tree of row i of P (64 partials of one dot product).
+__device__ __forceinline__ float lds_tree(const float *P, int i) {
+  float s[WAVE];
+#pragma unroll
+  for (int j = 0; j < WAVE; ++j) s[j] = P[i * SC_PAD + j];
+  return tree64(s);
+}
+
+template <typename XT> struct XChunk;
+template <> struct XChunk<uint16_t> {
+  u32x2 v;
+  __device__ __forceinline__ void load(const uint16_t *p) { v = *reinterpret_cast<const u32x2 *>(p); }
+  __device__ __forceinline__ float at(int r) const {
+    const uint32_t w = (r < 2) ? v.x : v.y;
+    return __uint_as_float((r & 1) ? (w & 0xFFFF0000u) : (w << 16));
+  }
+};
+template <> struct XChunk<float> {
+  float4 v;
+  __device__ __forceinline__ void load(const float *p) { v = *reinterpret_cast<const float4 *>(p); }
+  __device__ __forceinline__ float at(int r) const {
+    return r == 0 ? v.x : r == 1 ? v.y : r == 2 ? v.z : v.w;
+  }
+};
+
+// rows r < n_router: W_r (logits, + beta); n_router <= r < n_router + n_pred:
+// the predictor matrix A (q).  With ss != nullptr the wavefronts of row
+// tile 0 also produce ||x_t||^2.  Grid (ceil(B / 8), ceil(rows / 32)).
+template <typename XT>
+__global__ __launch_bounds__(SC_WAVES * WAVE)
+void k_scores(const XT *__restrict__ x, int B, int d,
+              const float *__restrict__ Wr, const float *__restrict__ beta,
+              int n_router, const float *__restrict__ A, int n_pred,
+              float *__restrict__ logits, float *__restrict__ q,
+              float *__restrict__ ss) {
+  __shared__ float P[SC_WAVES][SC_DOTS * SC_PAD];
+  const int lane = lane_id(), wv = wave_id();
+  const int rows = n_router + n_pred;
+  const int t0 = blockIdx.x * SC_T;
+  const int r0 = __builtin_amdgcn_readfirstlane((blockIdx.y * SC_WAVES + wv) * SC_R);
+  const bool do_ss = ss != nullptr && r0 == 0;
+
+  const XT *xr[SC_T];
+#pragma unroll
+  for (int a = 0; a < SC_T; ++a) xr[a] = x + (size_t)min(t0 + a, B - 1) * d;
+  const float *wr[SC_R];
+#pragma unroll
+  for (int b = 0; b < SC_R; ++b) {
+    const int r = min(r0 + b, rows - 1);
+    wr[b] = r < n_router ? Wr + (size_t)r * d : A + (size_t)(r - n_router) * d;
+  }
+
+  float acc[SC_T][SC_R], sacc[SC_T];
+#pragma unroll
+  for (int a = 0; a < SC_T; ++a) {
+    sacc[a] = 0.0f;
+#pragma unroll
+    for (int b = 0; b < SC_R; ++b) acc[a][b] = 0.0f;
+  }
+  // chunk m + 256 is requested before chunk m is consumed
+  XChunk<XT> xc[2][SC_T];
+  float4 wc[2][SC_R];
+  // row pointers are wave-uniform (scalar); the lane's elements sit at 4 lane
+  const int lo = 4 * lane;
+#pragma unroll
+  for (int a = 0; a < SC_T; ++a) xc[0][a].load(xr[a] + lo);
+#pragma unroll
+  for (int b = 0; b < SC_R; ++b) wc[0][b] = *reinterpret_cast<const float4 *>(wr[b] + lo);
+  for (int m = 0; m < d; m += 512) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int mn = m + 256 * (h + 1);
+      if (mn < d) {
+#pragma unroll
+        for (int a = 0; a < SC_T; ++a) xc[h ^ 1][a].load(xr[a] + mn + lo);
+#pragma unroll
+        for (int b = 0; b < SC_R; ++b)
+          wc[h ^ 1][b] = *reinterpret_cast<const float4 *>(wr[b] + mn + lo);
+      }
+      if (m + 256 * h < d) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+#pragma unroll
+          for (int a = 0; a < SC_T; ++a) {
+            const float xv = xc[h][a].at(r);
+#pragma unroll
+            for (int b = 0; b < SC_R; ++b) {
+              const float4 w4 = wc[h][b];
+              const float wv4 = r == 0 ? w4.x : r == 1 ? w4.y : r == 2 ? w4.z : w4.w;
+              acc[a][b] = __builtin_fmaf(xv, wv4, acc[a][b]);
+            }
+            if (do_ss) sacc[a] = __builtin_fmaf(xv, xv, sacc[a]);
+          }
+        }
+      }
+    }
+  }
+
+  float *Pw = P[wv];
+#pragma unroll
+  for (int a = 0; a < SC_T; ++a) {
+#pragma unroll
+    for (int b = 0; b < SC_R; ++b) Pw[(a * SC_R + b) * SC_PAD + lane] = acc[a][b];
+    Pw[(SC_T * SC_R + a) * SC_PAD + lane] = sacc[a];
+  }
+  __syncthreads();
+  {
+    const float v = lds_tree(Pw, lane);          // dot product `lane` of the tile
+    const int t = t0 + lane / SC_R, r = r0 + lane % SC_R;
+    if (t < B && r < rows) {
+      if (r < n_router)
+        logits[(size_t)t * n_router + r] = beta ? v + beta[r] : v;
+      else
+        q[(size_t)t * n_pred + (r - n_router)] = v;
+    }
+  }
+  if (do_ss && lane < SC_T) {
+    const float v = lds_tree(Pw, SC_T * SC_R + lane);
+    if (t0 + lane < B) ss[t0 + lane] = v;
+  }
+}
+
+constexpr int TL_WAVES = 4;    // tokens (wavefronts) per workgroup
+
+
+// mode bit 0: route (top-K and weights from the logits into ids / w)
+// mode bit 1: costs from q, ss and the routed pairs (ids / w, read back when
+//             bit 0 is off)
+__global__ __launch_bounds__(TL_WAVES * WAVE)
+void k_tail(int B, int E, int K, int norm_topk, const float *__restrict__ logits,
+            const float *__restrict__ q, const float *__restrict__ ss,
+            const float *__restrict__ bp, int32_t *__restrict__ ids_io,
+            float *__restrict__ w_io, float *__restrict__ cost, int mode) {
+  __shared__ __attribute__((aligned(16))) uint64_t keys[TL_WAVES][MAX_E];
+  __shared__ float lrow[TL_WAVES][MAX_E];
+  __shared__ int top[TL_WAVES][MAX_K];
+  __shared__ float eps_s[TL_WAVES][MAX_K];
+  const int lane = lane_id(), wv = wave_id();
+  const int t = blockIdx.x * TL_WAVES + wv;
+  const int tc = min(t, B - 1);            // every wavefront takes part in the barriers
+  const bool live = t < B;
+  const float *lt = logits + (size_t)tc * E;
+
+  int my_id = 0;       // lane k < K: routed expert k
+  float my_w = 0.0f;   // and its weight
+  if (mode & 1) {
+    float lv[MAX_E / WAVE];
+    uint64_t kv[MAX_E / WAVE];
+#pragma unroll
+    for (int i = 0; i < MAX_E / WAVE; ++i) {
+      const int e = lane + WAVE * i;
+      lv[i] = (e < E) ? lt[e] : 0.0f;
+      kv[i] = rank_key(lv[i], e);
+      if (e < E) lrow[wv][e] = lv[i];
+      if (e < ((E + 1) & ~1)) keys[wv][e] = (e < E) ? kv[i] : 0;   // 0 ranks last
+    }
+    __syncthreads();
+    // rank of (l_e, e) in the order (logit desc, index asc) among all E
+#pragma unroll
+    for (int i = 0; i < MAX_E / WAVE; ++i) {
+      const int e = lane + WAVE * i;
+      if (i * WAVE < E) {
+        int rank = 0;
+        for (int f = 0; f < E; f += 2) {
+          const u32x4 o = *reinterpret_cast<const u32x4 *>(&keys[wv][f]);
+          rank += (((uint64_t)o.y << 32 | o.x) > kv[i]);
+          rank += (((uint64_t)o.w << 32 | o.z) > kv[i]);
+        }
+        if (e < E && rank < K) top[wv][rank] = e;
+      }
+    }
+    __syncthreads();
+    const float lmax = lrow[wv][top[wv][0]];
+    if (lane < K) {
+      my_id = top[wv][lane];
+      eps_s[wv][lane] = base_exp(lrow[wv][my_id] - lmax);
+    }
+    __syncthreads();
+    float S;
+    if (norm_topk) {
+      S = 0.0f;
+      for (int k = 0; k < K; ++k) S = S + eps_s[wv][k];
+    } else {
+      float part = 0.0f;
+#pragma unroll
+      for (int i = 0; i < MAX_E / WAVE; ++i) {
+        const int e = lane + WAVE * i;
+        if (e < E) part = part + base_exp(lv[i] - lmax);
+      }
+      S = wave_tree_sum(part);
+    }
+    if (lane < K) {
+      my_w = eps_s[wv][lane] / S;
+      if (live) {
+        ids_io[(size_t)t * K + lane] = my_id;
+        w_io[(size_t)t * K + lane] = my_w;
+      }
+    }
+  } else if (lane < K) {
+    my_id = ids_io[(size_t)tc * K + lane];
+    my_w = w_io[(size_t)tc * K + lane];
+  }
+
+  if ((mode & 2) && live && lane < K) {
+    const int u = (my_id >= 0 && my_id < E) ? my_id : 0;   // out-of-range ids read row 0
+    const float s2 = ss[t];
+    float inv = 0.0f;
+    if (s2 > 0.0f) {
+      const float rt = sqrtf(s2);
+      inv = 1.0f / rt;
+    }
+    float s = q[(size_t)t * E + u] * inv;
+    s = s + bp[u];
+    const float w2 = my_w * my_w;
+    cost[(size_t)t * K + lane] = w2 * base_exp(s);
+  }
+}
+
+template <typename XT>
+static void launch_scores_t(const XT *x, int B, int d, const float *Wr,
+                            const float *beta, int n_router, const float *A,
+                            int n_pred, float *logits, float *q, float *ss,
+                            hipStream_t st) {
+  const int rows = n_router + n_pred;
+  dim3 grid((B + SC_T - 1) / SC_T, (rows + SC_R * SC_WAVES - 1) / (SC_R * SC_WAVES));
+  hipLaunchKernelGGL(k_scores<XT>, grid, dim3(SC_WAVES * WAVE), 0, st, x, B, d,
+                     Wr, beta, n_router, A, n_pred, logits, q, ss);
+}
+
+hipError_t launch_scores(bool bf16, const void *x, int B, int d, const float *Wr,
+                         const float *beta, int n_router, const float *A,
+                         int n_pred, float *logits, float *q, float *ss,
+                         hipStream_t st) {
+  if (bf16)
+    launch_scores_t((const uint16_t *)x, B, d, Wr, beta, n_router, A, n_pred,
+                    logits, q, ss, st);
+  else
+    launch_scores_t((const float *)x, B, d, Wr, beta, n_router, A, n_pred,
+                    logits, q, ss, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_tail(int B, int E, int K, int norm_topk, const float *logits,
+                       const float *q, const float *ss, const float *bp,
+                       int32_t *ids, float *w, float *cost, int mode,
+                       hipStream_t st) {
+  hipLaunchKernelGGL(k_tail, dim3((B + TL_WAVES - 1) / TL_WAVES),
+                     dim3(TL_WAVES * WAVE), 0, st, B, E, K, norm_topk, logits,
+                     q, ss, bp, ids, w, cost, mode);
+  return hipGetLastError();
+}
+
+}  // namespace basek
