@@ -13,10 +13,13 @@ Weights are resident in HBM before timing starts.  Steps rotate over
 decode step walks a model's layer stack, so the kept experts of a step are
 not still in the 256 MiB Infinity Cache from the previous steps.
 
-Prints ONE JSON line: the step latency in microseconds (``value``), the
-roofline of the dominant kernel (FFN gate/up: kept experts' gate and up rows
-against 8 TB/s of HBM3E), per-stage times from HIP events recorded by the
-library between its kernels, and the CPU oracle timed on a bounded sample.
+Prints ONE JSON line: the step latency in microseconds (``value``, K steps
+with nothing else on the stream), the roofline of the dominant kernel (FFN
+gate/up: kept experts' gate and up rows against 8 TB/s of HBM3E), per-kernel
+times from HIP events attached by the library to each kernel's own dispatch
+(a second pass over the same K steps), the cost of plain top-K routing on
+the same layers (for BASE's overhead), and the CPU oracle timed on a
+bounded sample.
 """
 from __future__ import annotations
 
@@ -224,9 +227,7 @@ def main():
             raise RuntimeError(bd.status_string(st))
 
     hip = hip_runtime()
-    n_ev = bd.N_STAGES + 1
-    stage_ev = [[new_event(hip) for _ in range(n_ev)] for _ in range(args.steps)]
-    ev_keep = [(ctypes.c_void_p * n_ev)(*row) for row in stage_ev]
+    n_ev = 2 * bd.N_STAGES
     t_start, t_end = new_event(hip), new_event(hip)
 
     print(f"[bench] {args.workload} B={B} B_e={budget} layers={len(layers)} "
@@ -235,7 +236,19 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
-    # timed region: K steps, stage events recorded by the library
+    # timed region: K steps, nothing else on the stream
+    torch.cuda.synchronize()
+    hip.hipEventRecord(t_start, sptr)
+    for i in range(args.steps):
+        step(i)
+    hip.hipEventRecord(t_end, sptr)
+    torch.cuda.synchronize()
+    us_step = elapsed_ms(hip, t_start, t_end) * 1e3 / args.steps
+
+    # the same K steps, each kernel timed by events attached to its own
+    # dispatch (the library's stage events): per-kernel durations
+    stage_ev = [[new_event(hip) for _ in range(n_ev)] for _ in range(args.steps)]
+    ev_keep = [(ctypes.c_void_p * n_ev)(*row) for row in stage_ev]
     torch.cuda.synchronize()
     hip.hipEventRecord(t_start, sptr)
     for i in range(args.steps):
@@ -244,24 +257,33 @@ def main():
     lib.base_set_stage_events(None, 0)
     hip.hipEventRecord(t_end, sptr)
     torch.cuda.synchronize()
-    total_ms = elapsed_ms(hip, t_start, t_end)
-    us_step = total_ms * 1e3 / args.steps
-
+    us_step_timed = elapsed_ms(hip, t_start, t_end) * 1e3 / args.steps
     stage_us = np.zeros((args.steps, bd.N_STAGES))
     for i in range(args.steps):
         for s in range(bd.N_STAGES):
-            stage_us[i, s] = elapsed_ms(hip, stage_ev[i][s], stage_ev[i][s + 1]) * 1e3
+            stage_us[i, s] = elapsed_ms(hip, stage_ev[i][2 * s], stage_ev[i][2 * s + 1]) * 1e3
     stage_mean = {bd.STAGES[s]: round(float(stage_us[:, s].mean()), 2)
                   for s in range(bd.N_STAGES)}
 
-    # same steps without stage events, for the event overhead
-    torch.cuda.synchronize()
-    hip.hipEventRecord(t_start, sptr)
+    # what plain top-K routing costs on the same layers (base_route: the
+    # router-only score kernel and the top-K tail), timed the same way
+    logits_r = torch.empty(B, shape.E, dtype=torch.float32, device=dev)
+    ids_r = torch.empty(B, shape.K, dtype=torch.int32, device=dev)
+    w_r = torch.empty(B, shape.K, dtype=torch.float32, device=dev)
+    route_us = np.zeros((args.steps, 2))
     for i in range(args.steps):
-        step(i)
-    hip.hipEventRecord(t_end, sptr)
+        _, desc = layers[i % len(layers)]
+        lib.base_set_stage_events(ev_keep[i], n_ev)
+        st = lib.base_route(ctypes.byref(desc), x.data_ptr(), B, logits_r.data_ptr(),
+                            ids_r.data_ptr(), w_r.data_ptr(), sptr)
+        if st != 0:
+            raise RuntimeError(bd.status_string(st))
+    lib.base_set_stage_events(None, 0)
     torch.cuda.synchronize()
-    us_step_plain = elapsed_ms(hip, t_start, t_end) * 1e3 / args.steps
+    for i in range(args.steps):
+        for s in range(2):
+            route_us[i, s] = elapsed_ms(hip, stage_ev[i][2 * s], stage_ev[i][2 * s + 1]) * 1e3
+    route_scores_us, route_tail_us = (float(v) for v in route_us.mean(axis=0))
 
     # plan of the last step (for the algorithmic byte count)
     def read_i32(ptr, n):
@@ -276,9 +298,13 @@ def main():
     ffn_us = stage_mean["ffn_gateup"] + stage_mean["ffn_down"]
     achieved = gu_bytes / (gu_us * 1e-6) / 1e9
     traffic = stored_traffic(args.workload, budget)
-    scoring_us = (stage_mean["topk_predict"] + stage_mean["aggregate_select"])
-    kernel_sum = float(sum(stage_mean.values()))
-
+    # BASE's own additions to a routed MoE step: the predictor (the part of
+    # the score and tail kernels beyond plain routing) and aggregation +
+    # selection
+    predict_us = (stage_mean["scores"] - route_scores_us) + (stage_mean["tail"] - route_tail_us)
+    pas_us = predict_us + stage_mean["select"]
+    pre_ffn_us = sum(stage_mean[k] for k in ("scores", "tail", "select", "backfill",
+                                             "compact", "gather"))
     out = {
         "metric": METRIC,
         "value": round(us_step, 2),
@@ -319,13 +345,16 @@ def main():
         },
         "stages_us": stage_mean,
         "overhead": {
-            "predict_aggregate_select_us": round(scoring_us, 2),
-            "predict_aggregate_select_frac": round(scoring_us / us_step, 4),
-            "route_to_compact_us": round(kernel_sum - ffn_us - stage_mean["combine"], 2),
-            "route_to_compact_frac": round(
-                (kernel_sum - ffn_us - stage_mean["combine"]) / us_step, 4),
+            "predict_us": round(predict_us, 2),
+            "aggregate_select_us": stage_mean["select"],
+            "predict_aggregate_select_us": round(pas_us, 2),
+            "predict_aggregate_select_frac": round(pas_us / us_step, 4),
+            "plain_routing_us": round(route_scores_us + route_tail_us, 2),
+            "pre_ffn_kernels_us": round(pre_ffn_us, 2),
+            "pre_ffn_frac": round(pre_ffn_us / us_step, 4),
         },
-        "us_per_step_without_stage_events": round(us_step_plain, 2),
+        "kernel_sum_us": round(float(sum(stage_mean.values())), 2),
+        "us_per_step_with_kernel_events": round(us_step_timed, 2),
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)

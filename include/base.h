@@ -226,17 +226,23 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
 base_status base_pack_experts(const base_layer *L, void *w13_packed,
                               void *w2_packed, void *stream);
 
-/* Stage timing for profiling.  `events` holds BASE_N_STAGES + 1 hipEvent_t
+/* Kernel timing for profiling.  `events` holds 2 * BASE_N_STAGES hipEvent_t
  * handles created by the caller (hipEventCreate), or is NULL to switch
- * timing off (n_events is then ignored).  While set, base_decode_layer
- * records events[i] on its stream right before stage i and
- * events[BASE_N_STAGES] after the last one, so hipEventElapsedTime of
- * consecutive events gives each kernel's duration.  Stages: 0 router
- * logits, 1 top-K + predicted costs, 2 aggregation + selection, 3 backfill,
- * 4 compaction, 5 FFN gate/up, 6 FFN down, 7 combine.  The setting belongs
+ * timing off (n_events is then ignored).  While set, the calls that run a
+ * stage launch its kernel with events[2 i] and events[2 i + 1] attached to
+ * the kernel's own dispatch (hipExtLaunchKernel): hipEventElapsedTime of
+ * the pair is that kernel's execution time, with nothing added to the
+ * stream between kernels.  A stage without a kernel for the layer's dtype
+ * (the gather of an fp32 layer) records its pair back to back.  Stages, one
+ * kernel each: 0 scores (router logits, predictor dot products, norms),
+ * 1 tail (top-K, router weights, predicted costs), 2 aggregation +
+ * selection, 3 backfill + gates, 4 compaction, 5 token gather, 6 FFN
+ * gate/up, 7 FFN down, 8 combine.  base_decode_layer runs all of them;
+ * base_route stages 0 and 1, base_select stage 2, base_moe_forward 3 to 8
+ * (base_predict_cost runs its own kernel, untimed).  The setting belongs
  * to the calling host thread; the caller keeps the events alive while it
- * is set.  Returns BASE_ERR_SHAPE if n_events != BASE_N_STAGES + 1. */
-#define BASE_N_STAGES 8
+ * is set.  Returns BASE_ERR_SHAPE if n_events != 2 * BASE_N_STAGES. */
+#define BASE_N_STAGES 9
 base_status base_set_stage_events(void *const *events, int32_t n_events);
 
 /* Static description of a status code. */

@@ -22,9 +22,9 @@ FILL_BACKFILL, FILL_DROP = 0, 2
 EXPORTS = ("base_workspace_bytes", "base_route", "base_predict_cost",
            "base_select", "base_moe_forward", "base_decode_layer",
            "base_pack_experts", "base_set_stage_events", "base_status_string")
-N_STAGES = 8
-STAGES = ("route_logits", "topk_predict", "aggregate_select", "backfill",
-          "compact", "ffn_gateup", "ffn_down", "combine")
+N_STAGES = 9     # one kernel each; base_set_stage_events takes 2 events per stage
+STAGES = ("scores", "tail", "select", "backfill", "compact", "gather",
+          "ffn_gateup", "ffn_down", "combine")
 
 _vp = ctypes.c_void_p
 _i32 = ctypes.c_int32
@@ -213,7 +213,8 @@ def packed_layer(layer: "Layer", K: int, stream=None) -> "Layer":
 
 
 def base_set_stage_events(events):
-    """events: a sequence of N_STAGES + 1 raw hipEvent_t handles, or None."""
+    """events: a sequence of 2 * N_STAGES raw hipEvent_t handles (start and
+    end of each stage's kernel), or None."""
     if events is None:
         _check(load().base_set_stage_events(None, 0))
         return None

@@ -110,11 +110,23 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
   return o;
 }
 
-// stage timing (base_set_stage_events), per host thread
+// kernel timing (base_set_stage_events), per host thread
 thread_local void *const *g_stage_events = nullptr;
+thread_local KernelEvents g_next;
 
-void mark(int stage, hipStream_t st) {
-  if (g_stage_events) (void)hipEventRecord((hipEvent_t)g_stage_events[stage], st);
+// the events of stage i go to the next kernel launched
+void stage(int i) {
+  if (g_stage_events)
+    g_next = {(hipEvent_t)g_stage_events[2 * i], (hipEvent_t)g_stage_events[2 * i + 1]};
+}
+
+// a stage that launched no kernel records its pair back to back
+void stage_end(hipStream_t st) {
+  if (g_next.start) {
+    (void)hipEventRecord(g_next.start, st);
+    (void)hipEventRecord(g_next.stop, st);
+    g_next = {};
+  }
 }
 
 template <typename T>
@@ -128,7 +140,7 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
                         const int32_t *sel_ids, const int32_t *n_sel,
                         const int32_t *slot_of, int32_t bc, int32_t flags,
                         const void *residual, void *y, void *ws,
-                        const Layout &o, hipStream_t st, bool timed) {
+                        const Layout &o, hipStream_t st) {
   const bool bf16 = L->dtype == BASE_BF16;
   int32_t *exec_ids = at<int32_t>(ws, o.exec_ids);
   float *exec_gates = at<float>(ws, o.exec_gates);
@@ -136,31 +148,37 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
   int32_t *pair_tok = at<int32_t>(ws, o.pair_tok);
   float *pair_gate = at<float>(ws, o.pair_gate);
   int32_t *pair_of = at<int32_t>(ws, o.pair_of);
-  if (timed) mark(3, st);
+  stage(3);
   HIP_TRY(launch_backfill(B, L->E, L->K, L->norm_topk, flags, logits, ids,
                           slot_of, n_sel, exec_ids, exec_gates, st));
-  if (timed) mark(4, st);
+  stage_end(st);
+  stage(4);
   PartRec *parts = at<PartRec>(ws, o.parts);
   int32_t *n_parts = at<int32_t>(ws, o.n_parts);
   HIP_TRY(launch_compact(B, L->K, bc, exec_ids, exec_gates, slot_of, n_sel,
                          offsets, pair_tok, pair_gate, pair_of, sel_ids, parts,
                          n_parts, st));
-  if (timed) mark(5, st);
+  stage_end(st);
+  stage(5);
   if (bf16)
     HIP_TRY(launch_gather(x, B, L->d, L->K, bc, parts, n_parts, pair_tok,
                           at<void>(ws, o.xp), st));
+  stage_end(st);
+  stage(6);
   const bool packed = L->w_layout == BASE_W_PACKED;
   HIP_TRY(launch_gateup(bf16, packed, x, B, L->d, L->I, L->E, L->K, bc, L->w13,
                         sel_ids, n_sel, offsets, pair_tok, parts, n_parts,
                         at<void>(ws, o.xp), at<void>(ws, o.H), st));
-  if (timed) mark(6, st);
+  stage_end(st);
+  stage(7);
   HIP_TRY(launch_down(bf16, packed, B, L->d, L->I, L->E, L->K, bc, L->w2,
                       sel_ids, n_sel, offsets, parts, n_parts, pair_gate,
                       at<void>(ws, o.H), at<float>(ws, o.pairbuf), st));
-  if (timed) mark(7, st);
+  stage_end(st);
+  stage(8);
   HIP_TRY(launch_combine(bf16, B, L->d, L->K, pair_of, at<float>(ws, o.pairbuf),
                          residual, y, st));
-  if (timed) mark(8, st);
+  stage_end(st);
   return BASE_OK;
 }
 
@@ -193,6 +211,10 @@ base_status check_ws(const base_layer *L, int32_t B, int32_t bc, void *ws,
 
 }  // namespace
 
+namespace basek {
+KernelEvents &kernel_events() { return g_next; }
+}  // namespace basek
+
 extern "C" {
 
 size_t base_workspace_bytes(const base_layer *L, int32_t B, int32_t budget) {
@@ -210,10 +232,14 @@ base_status base_route(const base_layer *L, const void *x, int32_t B,
   BASE_TRY(check_ptr(topk_w, 4));
   hipStream_t st = (hipStream_t)stream;
   const bool bf16 = L->dtype == BASE_BF16;
+  stage(0);
   HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
                         nullptr, 0, logits, nullptr, nullptr, st));
+  stage_end(st);
+  stage(1);
   HIP_TRY(launch_tail(B, L->E, L->K, L->norm_topk, logits, nullptr, nullptr,
                       nullptr, topk_ids, topk_w, nullptr, 1, st));
+  stage_end(st);
   return BASE_OK;
 }
 
@@ -245,8 +271,10 @@ base_status base_select(const base_layer *L, int32_t B, const int32_t *topk_ids,
   BASE_TRY(check_ptr(n_sel, 4));
   BASE_TRY(check_ptr(slot_of_expert, 4));
   const int32_t bc = budget < L->E ? budget : L->E;
+  stage(2);
   HIP_TRY(launch_select(B, L->K, L->E, topk_ids, cost, bc, scores, counts,
                         sel_ids, n_sel, slot_of_expert, (hipStream_t)stream));
+  stage_end((hipStream_t)stream);
   return BASE_OK;
 }
 
@@ -273,7 +301,7 @@ base_status base_moe_forward(const base_layer *L, const void *x, int32_t B,
   const Layout o = layout(L, B, bc);
   BASE_TRY(run_forward(L, x, B, logits, topk_ids, sel_ids, n_sel,
                        slot_of_expert, bc, flags, residual, y, ws, o,
-                       (hipStream_t)stream, false));
+                       (hipStream_t)stream));
   fill_plan(plan_out, ws, o, false);
   return BASE_OK;
 }
@@ -303,17 +331,20 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
   int32_t *slot = at<int32_t>(ws, o.slot_of);
   float *q = at<float>(ws, o.q);
   float *ss = at<float>(ws, o.ss);
-  mark(0, st);
+  stage(0);
   HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
                         L->pred_a, L->E, logits, q, ss, st));
-  mark(1, st);
+  stage_end(st);
+  stage(1);
   HIP_TRY(launch_tail(B, L->E, L->K, L->norm_topk, logits, q, ss, L->pred_b,
                       ids, w, cost, 3, st));
-  mark(2, st);
+  stage_end(st);
+  stage(2);
   HIP_TRY(launch_select(B, L->K, L->E, ids, cost, bc, at<float>(ws, o.scores),
                         at<int32_t>(ws, o.counts), sel, nsel, slot, st));
+  stage_end(st);
   BASE_TRY(run_forward(L, x, B, logits, ids, sel, nsel, slot, bc, flags,
-                       residual, y, ws, o, st, true));
+                       residual, y, ws, o, st));
   fill_plan(plan_out, ws, o, true);
   return BASE_OK;
 }
@@ -336,7 +367,7 @@ base_status base_set_stage_events(void *const *events, int32_t n_events) {
     g_stage_events = nullptr;
     return BASE_OK;
   }
-  if (n_events != BASE_N_STAGES + 1) return BASE_ERR_SHAPE;
+  if (n_events != 2 * BASE_N_STAGES) return BASE_ERR_SHAPE;
   for (int i = 0; i < n_events; ++i)
     if (!events[i]) return BASE_ERR_NULL;
   g_stage_events = events;

@@ -469,7 +469,7 @@ hipError_t launch_gather(const void *x, int B, int d, int K, int budget,
                          const PartRec *parts, const int32_t *n_parts,
                          const int32_t *pair_tok, void *xp, hipStream_t st) {
   const long long waves = (long long)ffn_max_parts(B, K, budget) * (d / 32);
-  hipLaunchKernelGGL(k_gather, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, st,
+  launch_k(k_gather, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, st,
                      (const uint16_t *)x, d, parts, n_parts, pair_tok, (uint16_t *)xp);
   return hipGetLastError();
 }
@@ -482,12 +482,12 @@ hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
                          const void *xp, void *H, hipStream_t st) {
   if (bf16) {
     const long long units = (long long)ffn_max_parts(B, K, budget) * (I / 32);
-    hipLaunchKernelGGL(packed ? k_gateup_bf16<true> : k_gateup_bf16<false>,
+    launch_k(packed ? k_gateup_bf16<true> : k_gateup_bf16<false>,
                        dim3(ffn_grid(units)), dim3(GU_SPLIT * WAVE), 0, st, d, I, E,
                        (const uint16_t *)w13, parts, n_parts, (const uint16_t *)xp,
                        (uint16_t *)H);
   } else {
-    hipLaunchKernelGGL(k_gateup_f32, dim3(budget, (I + F32_ROWS - 1) / F32_ROWS),
+    launch_k(k_gateup_f32, dim3(budget, (I + F32_ROWS - 1) / F32_ROWS),
                        dim3(F32_ROWS * F32_TG), 0, st, (const float *)x, d, I,
                        E, (const float *)w13, sel_ids, n_sel, offsets, pair_tok,
                        (float *)H);
@@ -503,12 +503,12 @@ hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K
                        hipStream_t st) {
   if (bf16) {
     const long long units = (long long)ffn_max_parts(B, K, budget) * (d / 64);
-    hipLaunchKernelGGL(packed ? k_down_bf16<true> : k_down_bf16<false>,
+    launch_k(packed ? k_down_bf16<true> : k_down_bf16<false>,
                        dim3(ffn_grid(units)), dim3(DN_SPLIT * WAVE), 0, st, d, I, E,
                        (const uint16_t *)w2, parts, n_parts, pair_gate,
                        (const uint16_t *)H, pairbuf);
   } else {
-    hipLaunchKernelGGL(k_down_f32, dim3(budget, (d + F32_ROWS - 1) / F32_ROWS),
+    launch_k(k_down_f32, dim3(budget, (d + F32_ROWS - 1) / F32_ROWS),
                        dim3(F32_ROWS * F32_TG), 0, st, d, I, E,
                        (const float *)w2, sel_ids, n_sel, offsets, pair_gate,
                        (const float *)H, pairbuf);
@@ -521,10 +521,10 @@ hipError_t launch_combine(bool bf16, int B, int d, int K,
                           const void *residual, void *y, hipStream_t st) {
   dim3 grid(B, (d + CB_THREADS * 4 - 1) / (CB_THREADS * 4));
   if (bf16)
-    hipLaunchKernelGGL(k_combine<true>, grid, dim3(CB_THREADS), 0, st, B, d, K,
+    launch_k(k_combine<true>, grid, dim3(CB_THREADS), 0, st, B, d, K,
                        pair_of, pairbuf, residual, y);
   else
-    hipLaunchKernelGGL(k_combine<false>, grid, dim3(CB_THREADS), 0, st, B, d, K,
+    launch_k(k_combine<false>, grid, dim3(CB_THREADS), 0, st, B, d, K,
                        pair_of, pairbuf, residual, y);
   return hipGetLastError();
 }

@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stdint.h>
 
 namespace basek {
@@ -11,6 +12,22 @@ constexpr int MAX_K = 16;     // experts per token
 constexpr int MAX_E = 256;    // experts per layer
 constexpr int MAX_B = 1024;   // tokens per batch
 constexpr int FFN_PART = 64;  // tokens of one FFN wavefront (4 MFMA tiles)
+
+// Events attached to the next kernel launch (per host thread): when set,
+// launch_k hands them to the dispatch itself, which records `start` as the
+// kernel begins and `stop` as it ends, then clears them.
+struct KernelEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+KernelEvents &kernel_events();
+
+template <typename F, typename... Args>
+inline void launch_k(F kernel, dim3 grid, dim3 block, uint32_t shm, hipStream_t st,
+                     Args... args) {
+  KernelEvents &ev = kernel_events();
+  hipExtLaunchKernelGGL(kernel, grid, block, shm, st, ev.start, ev.stop, 0, args...);
+  ev.start = ev.stop = nullptr;
+}
 
 // Upper bounds (host-known) of the FFN token tiling for a batch: 16-pair
 // tiles and 64-token parts over all kept slots.

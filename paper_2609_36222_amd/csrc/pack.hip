@@ -36,13 +36,13 @@ void k_pack(const uint16_t *__restrict__ src, uint16_t *__restrict__ dst,
 hipError_t launch_pack(const void *w13, const void *w2, void *w13p, void *w2p,
                        int E, int d, int I, hipStream_t st) {
   const long long s13 = (long long)E * 2 * I * d / 8;
-  hipLaunchKernelGGL(k_pack, dim3((unsigned)((s13 + 255) / 256)), dim3(256), 0,
+  launch_k(k_pack, dim3((unsigned)((s13 + 255) / 256)), dim3(256), 0,
                      st, (const uint16_t *)w13, (uint16_t *)w13p, s13, 2 * I, d,
                      I / 32, I, 1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const long long s2 = (long long)E * d * I / 8;
-  hipLaunchKernelGGL(k_pack, dim3((unsigned)((s2 + 255) / 256)), dim3(256), 0,
+  launch_k(k_pack, dim3((unsigned)((s2 + 255) / 256)), dim3(256), 0,
                      st, (const uint16_t *)w2, (uint16_t *)w2p, s2, d, I, d / 64, I, 0);
   return hipGetLastError();
 }

@@ -57,13 +57,20 @@ void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
     // keeps its last cost, and counts every time)
     const int j = tid % WAVE, cl = tid / WAVE, t = (c0 + cl) * WAVE + j;
     if (cl < nb && t < B) {
-      for (int k = 0; k < K; ++k) {
-        const int u = ids[(size_t)t * K + k];
-        if (u >= 0 && u < E) {
-          V[(cl * E + u) * SEL_PAD + j] = cost[(size_t)t * K + k];
-          atomicAdd(&cnt[u], 1);
+      int uk[MAX_K];
+      float ck[MAX_K];
+#pragma unroll
+      for (int k = 0; k < MAX_K; ++k)
+        if (k < K) {
+          uk[k] = ids[(size_t)t * K + k];
+          ck[k] = cost[(size_t)t * K + k];
         }
-      }
+#pragma unroll
+      for (int k = 0; k < MAX_K; ++k)
+        if (k < K && uk[k] >= 0 && uk[k] < E) {
+          V[(cl * E + uk[k]) * SEL_PAD + j] = ck[k];
+          atomicAdd(&cnt[uk[k]], 1);
+        }
     }
     __syncthreads();
     if (tid < nb * E) {
@@ -265,24 +272,36 @@ void k_compact(int B, int K, int budget, const int32_t *__restrict__ exec_ids,
   __shared__ int off[MAX_E + 1];
   __shared__ int tb[MAX_E + 1];
   __shared__ int pb[MAX_E + 1];
+  __shared__ int sel_s[MAX_E];
   const int tid = threadIdx.x, lane = lane_id();
-  const int n_sel = min(max(*n_sel_p, 0), budget);
   const int nwords = (B + 31) / 32;
-
-  for (int i = tid; i < n_sel * CP_WORDS; i += CP_THREADS) bits[i] = 0u;
-  __syncthreads();
   const int t = tid;
+  // every independent load first: the token's executed experts and gates,
+  // the kept list, n_sel
+  int u_of[MAX_K];
+  float g_of[MAX_K];
+#pragma unroll
+  for (int j = 0; j < MAX_K; ++j) {
+    u_of[j] = -1;
+    g_of[j] = 0.0f;
+    if (t < B && j < K) {
+      u_of[j] = exec_ids[(size_t)t * K + j];
+      g_of[j] = exec_gates[(size_t)t * K + j];
+    }
+  }
+  if (tid < budget) sel_s[tid] = sel_ids[tid];
+  const int n_sel = min(max(*n_sel_p, 0), budget);
+  for (int i = tid; i < budget * CP_WORDS; i += CP_THREADS) bits[i] = 0u;
   int s_of[MAX_K];
 #pragma unroll
   for (int j = 0; j < MAX_K; ++j) {
-    int s = -1;
-    if (t < B && j < K) {
-      const int u = exec_ids[(size_t)t * K + j];
-      if (u >= 0) s = slot_of[u];
-    }
+    const int s = (u_of[j] >= 0) ? slot_of[u_of[j]] : -1;
     s_of[j] = (s >= 0 && s < n_sel) ? s : -1;
-    if (s_of[j] >= 0) atomicOr(&bits[s_of[j] * CP_WORDS + (t >> 5)], 1u << (t & 31));
   }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < MAX_K; ++j)
+    if (s_of[j] >= 0) atomicOr(&bits[s_of[j] * CP_WORDS + (t >> 5)], 1u << (t & 31));
   __syncthreads();
   for (int s = tid; s < n_sel; s += CP_THREADS) {
     int run = 0;
@@ -303,7 +322,7 @@ void k_compact(int B, int K, int budget, const int32_t *__restrict__ exec_ids,
   for (int s = wave_id(); s < n_sel; s += CP_THREADS / WAVE) {
     const int np = pb[s + 1] - pb[s];
     PartRec r;
-    r.u = sel_ids[s];
+    r.u = sel_s[s];
     r.off = off[s];
     r.n = cnt[s];
     r.tile0 = tb[s];
@@ -326,7 +345,7 @@ void k_compact(int B, int K, int budget, const int32_t *__restrict__ exec_ids,
           const uint32_t below = bits[s * CP_WORDS + (t >> 5)] & ((1u << (t & 31)) - 1u);
           p = off[s] + pre[s * CP_WORDS + (t >> 5)] + __popc(below);
           pair_tok[p] = t;
-          pair_gate[p] = exec_gates[(size_t)t * K + j];
+          pair_gate[p] = g_of[j];
         }
         pair_of[(size_t)t * K + j] = p;
       }
@@ -338,7 +357,7 @@ hipError_t launch_select(int B, int K, int E, const int32_t *ids,
                          const float *cost, int budget, float *scores,
                          int32_t *counts, int32_t *sel_ids, int32_t *n_sel,
                          int32_t *slot_of, hipStream_t st) {
-  hipLaunchKernelGGL(k_select, dim3(1), dim3(SEL_THREADS), 0, st, B, K, E, ids,
+  launch_k(k_select, dim3(1), dim3(SEL_THREADS), 0, st, B, K, E, ids,
                      cost, budget, scores, counts, sel_ids, n_sel, slot_of);
   return hipGetLastError();
 }
@@ -348,7 +367,7 @@ hipError_t launch_backfill(int B, int E, int K, int norm_topk, int flags,
                            const int32_t *slot_of, const int32_t *n_sel,
                            int32_t *exec_ids, float *exec_gates,
                            hipStream_t st) {
-  hipLaunchKernelGGL(k_backfill, dim3((B + BF_WAVES - 1) / BF_WAVES),
+  launch_k(k_backfill, dim3((B + BF_WAVES - 1) / BF_WAVES),
                      dim3(BF_WAVES * WAVE), 0, st, B, E, K, norm_topk, flags,
                      logits, ids, slot_of, n_sel, exec_ids, exec_gates);
   return hipGetLastError();
@@ -360,7 +379,7 @@ hipError_t launch_compact(int B, int K, int budget, const int32_t *exec_ids,
                           int32_t *pair_tok, float *pair_gate,
                           int32_t *pair_of, const int32_t *sel_ids,
                           PartRec *parts, int32_t *n_parts, hipStream_t st) {
-  hipLaunchKernelGGL(k_compact, dim3(1), dim3(CP_THREADS), 0, st, B, K, budget,
+  launch_k(k_compact, dim3(1), dim3(CP_THREADS), 0, st, B, K, budget,
                      exec_ids, exec_gates, slot_of, n_sel, offsets, pair_tok,
                      pair_gate, pair_of, sel_ids, parts, n_parts);
   return hipGetLastError();

@@ -92,10 +92,10 @@ hipError_t launch_predict(bool bf16, const void *x, int B, int d, int E, int K,
                           const float *bp, float *cost, hipStream_t st) {
   dim3 grid((B + TOK_WAVES - 1) / TOK_WAVES);
   if (bf16)
-    hipLaunchKernelGGL(k_token<uint16_t>, grid, dim3(TOK_WAVES * WAVE), 0, st,
+    launch_k(k_token<uint16_t>, grid, dim3(TOK_WAVES * WAVE), 0, st,
                        (const uint16_t *)x, B, d, E, K, ids, w, A, bp, cost);
   else
-    hipLaunchKernelGGL(k_token<float>, grid, dim3(TOK_WAVES * WAVE), 0, st,
+    launch_k(k_token<float>, grid, dim3(TOK_WAVES * WAVE), 0, st,
                        (const float *)x, B, d, E, K, ids, w, A, bp, cost);
   return hipGetLastError();
 }

@@ -262,7 +262,7 @@ static void launch_scores_t(const XT *x, int B, int d, const float *Wr,
                             hipStream_t st) {
   const int rows = n_router + n_pred;
   dim3 grid((B + SC_T - 1) / SC_T, (rows + SC_R * SC_WAVES - 1) / (SC_R * SC_WAVES));
-  hipLaunchKernelGGL(k_scores<XT>, grid, dim3(SC_WAVES * WAVE), 0, st, x, B, d,
+  launch_k(k_scores<XT>, grid, dim3(SC_WAVES * WAVE), 0, st, x, B, d,
                      Wr, beta, n_router, A, n_pred, logits, q, ss);
 }
 
@@ -283,7 +283,7 @@ hipError_t launch_tail(int B, int E, int K, int norm_topk, const float *logits,
                        const float *q, const float *ss, const float *bp,
                        int32_t *ids, float *w, float *cost, int mode,
                        hipStream_t st) {
-  hipLaunchKernelGGL(k_tail, dim3((B + TL_WAVES - 1) / TL_WAVES),
+  launch_k(k_tail, dim3((B + TL_WAVES - 1) / TL_WAVES),
                      dim3(TL_WAVES * WAVE), 0, st, B, E, K, norm_topk, logits,
                      q, ss, bp, ids, w, cost, mode);
   return hipGetLastError();

@@ -172,3 +172,15 @@ def test_pack_validation(lib):
     assert f(layer(), b=FAKE + 8) == ALIGN
     assert f(layer(w13=0)) == NULL
     assert f(layer(I=100)) == SHAPE
+
+
+def test_stage_events_validation(lib):
+    arr = (ctypes.c_void_p * (2 * bd.N_STAGES))(*([FAKE] * (2 * bd.N_STAGES)))
+    assert lib.base_set_stage_events(arr, 2 * bd.N_STAGES - 1) == SHAPE
+    assert lib.base_set_stage_events(arr, bd.N_STAGES + 1) == SHAPE
+    arr[3] = None
+    assert lib.base_set_stage_events(arr, 2 * bd.N_STAGES) == NULL
+    assert lib.base_set_stage_events(None, 0) == OK
+    assert len(bd.STAGES) == bd.N_STAGES
+    with open(os.path.join(ROOT, "include", "base.h")) as f:
+        assert re.search(r"#define BASE_N_STAGES %d\b" % bd.N_STAGES, f.read())
