@@ -155,7 +155,7 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
   stage(4);
   PartRec *parts = at<PartRec>(ws, o.parts);
   int32_t *n_parts = at<int32_t>(ws, o.n_parts);
-  HIP_TRY(launch_compact(B, L->K, bc, exec_ids, exec_gates, slot_of, n_sel,
+  HIP_TRY(launch_compact(B, L->K, L->E, bc, exec_ids, exec_gates, slot_of, n_sel,
                          offsets, pair_tok, pair_gate, pair_of, sel_ids, parts,
                          n_parts, st));
   stage_end(st);

@@ -20,6 +20,21 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (WAVE - 1); }
 __device__ __forceinline__ int wave_id() { return threadIdx.x / WAVE; }
+// the same, known to the compiler to be uniform over the wavefront (values
+// derived from it stay in scalar registers)
+__device__ __forceinline__ int wave_id_u() {
+  return __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
+}
+
+// LDS writes of this wavefront complete, then the workgroup meets.  Unlike
+// __syncthreads() this does not wait for the wavefront's global loads, so
+// loads requested ahead stay in flight across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0); vmcnt, expcnt: no wait
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+}
 
 // ---------------------------------------------------------------- bf16 ---
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) {

@@ -73,7 +73,7 @@ hipError_t launch_backfill(int B, int E, int K, int norm_topk, int flags,
                            const int32_t *slot_of, const int32_t *n_sel,
                            int32_t *exec_ids, float *exec_gates,
                            hipStream_t st);
-hipError_t launch_compact(int B, int K, int budget, const int32_t *exec_ids,
+hipError_t launch_compact(int B, int K, int E, int budget, const int32_t *exec_ids,
                           const float *exec_gates, const int32_t *slot_of,
                           const int32_t *n_sel, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,

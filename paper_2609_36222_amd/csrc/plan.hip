@@ -33,42 +33,46 @@ void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
               float *__restrict__ scores, int32_t *__restrict__ counts,
               int32_t *__restrict__ sel_ids, int32_t *__restrict__ n_sel_out,
               int32_t *__restrict__ slot_of) {
-  __shared__ float V[SEL_V];
+  __shared__ __attribute__((aligned(16))) float V[SEL_V];
   __shared__ float CS[SEL_THREADS];
   __shared__ float D[MAX_E];
   __shared__ int cnt[MAX_E];
   __shared__ uint64_t key[MAX_E];
   __shared__ int rnk[MAX_E];
   __shared__ int n_union;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = lane_id();
 
-  for (int u = tid; u < E; u += SEL_THREADS) { cnt[u] = 0; D[u] = 0.0f; rnk[u] = 0; }
+  // thread t holds the routes of token t (B <= SEL_THREADS), loaded once
+  int uk[MAX_K];
+  float ck[MAX_K];
+#pragma unroll
+  for (int k = 0; k < MAX_K; ++k) {
+    uk[k] = -1;
+    ck[k] = 0.0f;
+    if (k < K && tid < B) {
+      uk[k] = ids[(size_t)tid * K + k];
+      ck[k] = cost[(size_t)tid * K + k];
+    }
+  }
+  for (int u = tid; u < E; u += SEL_THREADS) { cnt[u] = 0; D[u] = 0.0f; }
   if (tid == 0) n_union = 0;
   const int nchunks = (B + WAVE - 1) / WAVE;
-  // chunks per batch: bounded by V, by one thread per token and by one
-  // thread per (chunk, expert)
-  const int cb = max(1, min(min(nchunks, SEL_V / (E * SEL_PAD)),
-                            min(SEL_THREADS / WAVE, SEL_THREADS / E)));
+  // chunks per batch: bounded by V and by one thread per (chunk, expert)
+  const int cb = max(1, min(min(nchunks, SEL_V / (E * SEL_PAD)), SEL_THREADS / E));
   for (int c0 = 0; c0 < nchunks; c0 += cb) {
     const int nb = min(cb, nchunks - c0);
-    for (int i = tid; i < nb * E * SEL_PAD; i += SEL_THREADS) V[i] = 0.0f;
+    const int nv = min(SEL_V, (nb * E * SEL_PAD + 3) & ~3) / 4;
+    for (int i = tid; i < nv; i += SEL_THREADS)
+      reinterpret_cast<float4 *>(V)[i] = float4{0.0f, 0.0f, 0.0f, 0.0f};
     __syncthreads();
-    // one thread per token: its routes in rank order (a repeated expert
-    // keeps its last cost, and counts every time)
-    const int j = tid % WAVE, cl = tid / WAVE, t = (c0 + cl) * WAVE + j;
-    if (cl < nb && t < B) {
-      int uk[MAX_K];
-      float ck[MAX_K];
-#pragma unroll
-      for (int k = 0; k < MAX_K; ++k)
-        if (k < K) {
-          uk[k] = ids[(size_t)t * K + k];
-          ck[k] = cost[(size_t)t * K + k];
-        }
+    // the routes in rank order (a repeated expert keeps its last cost, and
+    // counts every time)
+    const int cl = tid / WAVE - c0;
+    if (tid < B && cl >= 0 && cl < nb) {
 #pragma unroll
       for (int k = 0; k < MAX_K; ++k)
         if (k < K && uk[k] >= 0 && uk[k] < E) {
-          V[(cl * E + uk[k]) * SEL_PAD + j] = ck[k];
+          V[(cl * E + uk[k]) * SEL_PAD + lane] = ck[k];
           atomicAdd(&cnt[uk[k]], 1);
         }
     }
@@ -90,21 +94,25 @@ void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
     __syncthreads();
   }
 
-  for (int u = tid; u < E; u += SEL_THREADS) {
-    key[u] = cnt[u] > 0 ? rank_key(D[u], u) : 0;   // 0: ranks after every expert
-    if (cnt[u] > 0) atomicAdd(&n_union, 1);
+  for (int u = tid; u < ((E + WAVE - 1) & ~(WAVE - 1)); u += SEL_THREADS) {
+    const bool in = u < E && cnt[u] > 0;
+    if (u < E) key[u] = in ? rank_key(D[u], u) : 0;   // 0: ranks after every expert
+    const uint64_t m = __ballot(in);
+    if (lane == 0 && m) atomicAdd(&n_union, (int)__popcll(m));
   }
   __syncthreads();
   const int n_sel = min(budget, n_union);
   {
-    // four threads per expert, each over a quarter of the candidates
-    const int u = tid >> 2, part = tid & 3;
+    // tpe consecutive threads per expert, each over a share of the keys
+    const int tpe = E <= 64 ? 16 : E <= 128 ? 8 : 4;
+    const int u = tid / tpe, part = tid % tpe;
+    int r = 0;
     if (u < E && cnt[u] > 0) {
       const uint64_t ku = key[u];
-      int r = 0;
-      for (int v = part; v < E; v += 4) r += key[v] > ku;
-      atomicAdd(&rnk[u], r);
+      for (int v = part; v < E; v += tpe) r += key[v] > ku;
     }
+    for (int h = 1; h < tpe; h <<= 1) r += __shfl_xor(r, h, WAVE);
+    if (u < E && part == 0) rnk[u] = r;
   }
   __syncthreads();
   for (int u = tid; u < E; u += SEL_THREADS) {
@@ -225,39 +233,45 @@ void k_backfill(int B, int E, int K, int norm_topk, int flags,
   }
 }
 
-// Exclusive prefix over slots s < n of ceil(cnt[s] / unit) by one
-// wavefront (4 slots per lane); out[MAX_E] receives the total.
-__device__ __forceinline__ void wave_scan_slots(const int *cnt, int n, int unit,
-                                                int *out) {
+// Exclusive prefixes over slots s < n of cnt[s] (pairs), ceil(cnt[s] / 16)
+// (16-pair tiles) and ceil(cnt[s] / FFN_PART) (FFN parts), by one
+// wavefront in one pass (4 slots per lane); out[MAX_E] receives each total.
+__device__ __forceinline__ void wave_scan3(const int *cnt, int n, int *off, int *tb, int *pb) {
   const int lane = lane_id();
-  int local[MAX_E / WAVE];
-  int sum = 0;
+  constexpr int Q = MAX_E / WAVE;
+  int l0[Q], l1[Q], l2[Q];
+  int s0 = 0, s1 = 0, s2 = 0;
 #pragma unroll
-  for (int q = 0; q < MAX_E / WAVE; ++q) {
-    const int s = lane * (MAX_E / WAVE) + q;
-    local[q] = (s < n) ? (cnt[s] + unit - 1) / unit : 0;
-    sum += local[q];
+  for (int q = 0; q < Q; ++q) {
+    const int s = lane * Q + q;
+    const int c = (s < n) ? cnt[s] : 0;
+    l0[q] = c;
+    l1[q] = (c + 15) / 16;
+    l2[q] = (c + FFN_PART - 1) / FFN_PART;
+    s0 += l0[q]; s1 += l1[q]; s2 += l2[q];
   }
-  int incl = sum;
+  int i0 = s0, i1 = s1, i2 = s2;
 #pragma unroll
   for (int h = 1; h < WAVE; h <<= 1) {
-    const int o = __shfl_up(incl, h, WAVE);
-    if (lane >= h) incl += o;
+    const int o0 = __shfl_up(i0, h, WAVE), o1 = __shfl_up(i1, h, WAVE),
+              o2 = __shfl_up(i2, h, WAVE);
+    if (lane >= h) { i0 += o0; i1 += o1; i2 += o2; }
   }
-  int run = incl - sum;
+  int r0 = i0 - s0, r1 = i1 - s1, r2 = i2 - s2;
 #pragma unroll
-  for (int q = 0; q < MAX_E / WAVE; ++q) {
-    out[lane * (MAX_E / WAVE) + q] = run;
-    run += local[q];
+  for (int q = 0; q < Q; ++q) {
+    const int s = lane * Q + q;
+    off[s] = r0; tb[s] = r1; pb[s] = r2;
+    r0 += l0[q]; r1 += l1[q]; r2 += l2[q];
   }
-  if (lane == WAVE - 1) out[MAX_E] = incl;
+  if (lane == WAVE - 1) { off[MAX_E] = i0; tb[MAX_E] = i1; pb[MAX_E] = i2; }
 }
 
 constexpr int CP_THREADS = 1024;
 constexpr int CP_WORDS = MAX_B / 32;
 
 __global__ __launch_bounds__(CP_THREADS)
-void k_compact(int B, int K, int budget, const int32_t *__restrict__ exec_ids,
+void k_compact(int B, int K, int E, int budget, const int32_t *__restrict__ exec_ids,
                const float *__restrict__ exec_gates,
                const int32_t *__restrict__ slot_of,
                const int32_t *__restrict__ n_sel_p,
@@ -273,6 +287,7 @@ void k_compact(int B, int K, int budget, const int32_t *__restrict__ exec_ids,
   __shared__ int tb[MAX_E + 1];
   __shared__ int pb[MAX_E + 1];
   __shared__ int sel_s[MAX_E];
+  __shared__ int slot_s[MAX_E];
   const int tid = threadIdx.x, lane = lane_id();
   const int nwords = (B + 31) / 32;
   const int t = tid;
@@ -290,15 +305,16 @@ void k_compact(int B, int K, int budget, const int32_t *__restrict__ exec_ids,
     }
   }
   if (tid < budget) sel_s[tid] = sel_ids[tid];
+  if (tid < E) slot_s[tid] = slot_of[tid];
   const int n_sel = min(max(*n_sel_p, 0), budget);
   for (int i = tid; i < budget * CP_WORDS; i += CP_THREADS) bits[i] = 0u;
+  __syncthreads();
   int s_of[MAX_K];
 #pragma unroll
   for (int j = 0; j < MAX_K; ++j) {
-    const int s = (u_of[j] >= 0) ? slot_of[u_of[j]] : -1;
+    const int s = (u_of[j] >= 0 && u_of[j] < E) ? slot_s[u_of[j]] : -1;
     s_of[j] = (s >= 0 && s < n_sel) ? s : -1;
   }
-  __syncthreads();
 #pragma unroll
   for (int j = 0; j < MAX_K; ++j)
     if (s_of[j] >= 0) atomicOr(&bits[s_of[j] * CP_WORDS + (t >> 5)], 1u << (t & 31));
@@ -312,11 +328,7 @@ void k_compact(int B, int K, int budget, const int32_t *__restrict__ exec_ids,
     cnt[s] = run;
   }
   __syncthreads();
-  if (tid < WAVE) {   // exclusive scans over slots by one wavefront:
-    wave_scan_slots(cnt, n_sel, 1, off);          // pairs
-    wave_scan_slots(cnt, n_sel, 16, tb);          // 16-pair tiles
-    wave_scan_slots(cnt, n_sel, FFN_PART, pb);    // FFN token parts
-  }
+  if (tid < WAVE) wave_scan3(cnt, n_sel, off, tb, pb);
   __syncthreads();
   // the FFN's part table: every part of slot s gets the slot's entry
   for (int s = wave_id(); s < n_sel; s += CP_THREADS / WAVE) {
@@ -373,13 +385,13 @@ hipError_t launch_backfill(int B, int E, int K, int norm_topk, int flags,
   return hipGetLastError();
 }
 
-hipError_t launch_compact(int B, int K, int budget, const int32_t *exec_ids,
+hipError_t launch_compact(int B, int K, int E, int budget, const int32_t *exec_ids,
                           const float *exec_gates, const int32_t *slot_of,
                           const int32_t *n_sel, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
                           int32_t *pair_of, const int32_t *sel_ids,
                           PartRec *parts, int32_t *n_parts, hipStream_t st) {
-  launch_k(k_compact, dim3(1), dim3(CP_THREADS), 0, st, B, K, budget,
+  launch_k(k_compact, dim3(1), dim3(CP_THREADS), 0, st, B, K, E, budget,
                      exec_ids, exec_gates, slot_of, n_sel, offsets, pair_tok,
                      pair_gate, pair_of, sel_ids, parts, n_parts);
   return hipGetLastError();

@@ -17,14 +17,22 @@
 // joined by the halving tree "s[j] = s[j] + s[j + h], j < h" for h = 32 ..
 // 1.  Here lane j of a wavefront holds partial j of up to 72 dot products at
 // once; the trees run through LDS (a transpose), one dot product per lane.
+// The operands of a workgroup's 16 x 16 tile pass through LDS chunk by
+// chunk, so each is read from L2 once per workgroup.
 #include "common.hpp"
 #include "internal.hpp"
 
 namespace basek {
 
 constexpr int SC_T = 8;        // tokens per wavefront tile
-constexpr int SC_R = 8;        // matrix rows per wavefront tile
-constexpr int SC_WAVES = 4;    // wavefronts per workgroup (row direction)
+constexpr int SC_R = 4;        // matrix rows per wavefront tile
+constexpr int SC_WT = 2;       // wavefronts of a workgroup along tokens
+constexpr int SC_WR = 4;       // wavefronts of a workgroup along rows
+constexpr int SC_WAVES = SC_WT * SC_WR;
+constexpr int SC_TB = SC_T * SC_WT;           // tokens per workgroup
+constexpr int SC_RB = SC_R * SC_WR;           // rows per workgroup
+constexpr int SC_CH = 256;                    // elements per chunk
+constexpr int SC_PF = 3;                      // chunks requested ahead (register stages)
 constexpr int SC_DOTS = SC_T * SC_R + SC_T;   // + ||x||^2 of the tile's tokens
 constexpr int SC_PAD = WAVE + 1;              // LDS row of one dot's partials
 
@@ -62,32 +70,81 @@ template <> struct XChunk<float> {
   }
 };
 
+// Staging of one 256-element chunk of the workgroup's SC_TB token rows and
+// SC_RB matrix rows: 16-byte pieces, XP of them for the tokens and WP for
+// the rows per thread.
+template <typename XT>
+struct ScStage {
+  static constexpr int XB = SC_TB * SC_CH * (int)sizeof(XT) / 16;   // x pieces
+  static constexpr int WB = SC_RB * SC_CH * 4 / 16;                  // row pieces
+  static constexpr int XP = XB / (SC_WAVES * WAVE), WP = WB / (SC_WAVES * WAVE);
+  static constexpr int XS = SC_CH * (int)sizeof(XT) / 16;            // pieces per token row
+  static constexpr int WS = SC_CH * 4 / 16;                          // pieces per matrix row
+  static_assert(XB % (SC_WAVES * WAVE) == 0 && WB % (SC_WAVES * WAVE) == 0,
+                "staging pieces per thread");
+  u32x4 xv[XP], wv[WP];
+};
+
+// The workgroup's LDS: two chunk buffers while streaming, then the
+// wavefronts' partials for the trees.
+template <typename XT>
+union ScLds {
+  struct {
+    u32x4 x[2][ScStage<XT>::XB];
+    u32x4 w[2][ScStage<XT>::WB];
+  } ch;
+  float P[SC_WAVES][SC_DOTS * SC_PAD];
+};
+
 // rows r < n_router: W_r (logits, + beta); n_router <= r < n_router + n_pred:
 // the predictor matrix A (q).  With ss != nullptr the wavefronts of row
-// tile 0 also produce ||x_t||^2.  Grid (ceil(B / 8), ceil(rows / 32)).
+// tile 0 also produce ||x_t||^2.  A workgroup covers 16 tokens x 16 rows
+// (2 x 4 wavefronts of 8 x 4); each 256-element chunk of its rows is staged
+// once in LDS, the next chunk's loads in flight meanwhile.  Grid
+// (ceil(B / 16), ceil(rows / 16)).
 template <typename XT>
-__global__ __launch_bounds__(SC_WAVES * WAVE)
+__global__ __launch_bounds__(SC_WAVES * WAVE, 2)
 void k_scores(const XT *__restrict__ x, int B, int d,
               const float *__restrict__ Wr, const float *__restrict__ beta,
               int n_router, const float *__restrict__ A, int n_pred,
               float *__restrict__ logits, float *__restrict__ q,
               float *__restrict__ ss) {
-  __shared__ float P[SC_WAVES][SC_DOTS * SC_PAD];
-  const int lane = lane_id(), wv = wave_id();
+  using St = ScStage<XT>;
+  __shared__ ScLds<XT> lds;
+  const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
+  const int tw = wv % SC_WT, rw = wv / SC_WT;
   const int rows = n_router + n_pred;
-  const int t0 = blockIdx.x * SC_T;
-  const int r0 = __builtin_amdgcn_readfirstlane((blockIdx.y * SC_WAVES + wv) * SC_R);
-  const bool do_ss = ss != nullptr && r0 == 0;
+  const int tb0 = blockIdx.x * SC_TB, rb0 = blockIdx.y * SC_RB;
+  const bool do_ss = ss != nullptr && rb0 == 0 && rw == 0;
 
-  const XT *xr[SC_T];
+  // the thread's staging pieces: token row / matrix row and 16-byte column
+  const XT *xsrc[St::XP];
+  const float *wsrc[St::WP];
 #pragma unroll
-  for (int a = 0; a < SC_T; ++a) xr[a] = x + (size_t)min(t0 + a, B - 1) * d;
-  const float *wr[SC_R];
-#pragma unroll
-  for (int b = 0; b < SC_R; ++b) {
-    const int r = min(r0 + b, rows - 1);
-    wr[b] = r < n_router ? Wr + (size_t)r * d : A + (size_t)(r - n_router) * d;
+  for (int i = 0; i < St::XP; ++i) {
+    const int c = tid + i * SC_WAVES * WAVE;
+    xsrc[i] = x + (size_t)min(tb0 + c / St::XS, B - 1) * d + (c % St::XS) * (16 / sizeof(XT));
   }
+#pragma unroll
+  for (int i = 0; i < St::WP; ++i) {
+    const int c = tid + i * SC_WAVES * WAVE;
+    const int r = min(rb0 + c / St::WS, rows - 1);
+    wsrc[i] = (r < n_router ? Wr + (size_t)r * d : A + (size_t)(r - n_router) * d) +
+              (c % St::WS) * 4;
+  }
+  St st[SC_PF];
+  auto fetch = [&](St &sg, int m) {
+#pragma unroll
+    for (int i = 0; i < St::XP; ++i) sg.xv[i] = *reinterpret_cast<const u32x4 *>(xsrc[i] + m);
+#pragma unroll
+    for (int i = 0; i < St::WP; ++i) sg.wv[i] = *reinterpret_cast<const u32x4 *>(wsrc[i] + m);
+  };
+  auto put = [&](const St &sg, int b) {
+#pragma unroll
+    for (int i = 0; i < St::XP; ++i) lds.ch.x[b][tid + i * SC_WAVES * WAVE] = sg.xv[i];
+#pragma unroll
+    for (int i = 0; i < St::WP; ++i) lds.ch.w[b][tid + i * SC_WAVES * WAVE] = sg.wv[i];
+  };
 
   float acc[SC_T][SC_R], sacc[SC_T];
 #pragma unroll
@@ -96,46 +153,61 @@ void k_scores(const XT *__restrict__ x, int B, int d,
 #pragma unroll
     for (int b = 0; b < SC_R; ++b) acc[a][b] = 0.0f;
   }
-  // chunk m + 256 is requested before chunk m is consumed
-  XChunk<XT> xc[2][SC_T];
-  float4 wc[2][SC_R];
-  // row pointers are wave-uniform (scalar); the lane's elements sit at 4 lane
-  const int lo = 4 * lane;
+  const int nch = d / SC_CH;
+  // register stage q holds the chunks m = q (mod SC_PF); chunk m + 1 goes
+  // to LDS while chunk m is used, chunk m + SC_PF is requested meanwhile
 #pragma unroll
-  for (int a = 0; a < SC_T; ++a) xc[0][a].load(xr[a] + lo);
+  for (int q = 0; q < SC_PF; ++q) {
+    if (q < nch) fetch(st[q], q * SC_CH);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  put(st[0], 0);
+  lds_barrier();
+  for (int m0 = 0; m0 < nch; m0 += SC_PF) {
 #pragma unroll
-  for (int b = 0; b < SC_R; ++b) wc[0][b] = *reinterpret_cast<const float4 *>(wr[b] + lo);
-  for (int m = 0; m < d; m += 512) {
+    for (int q = 0; q < SC_PF; ++q) {
+      const int m = m0 + q;
+      if (m < nch) {
+        const int buf = m & 1;
+        // this lane's elements 4 lane .. 4 lane + 3 of the chunk
+        const XT *xl = reinterpret_cast<const XT *>(lds.ch.x[buf]) + 4 * lane;
+        const float *wl = reinterpret_cast<const float *>(lds.ch.w[buf]) + 4 * lane;
+        XChunk<XT> xc[SC_T];
+        float4 wc[SC_R];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int mn = m + 256 * (h + 1);
-      if (mn < d) {
-#pragma unroll
-        for (int a = 0; a < SC_T; ++a) xc[h ^ 1][a].load(xr[a] + mn + lo);
+        for (int a = 0; a < SC_T; ++a) xc[a].load(xl + (tw * SC_T + a) * SC_CH);
 #pragma unroll
         for (int b = 0; b < SC_R; ++b)
-          wc[h ^ 1][b] = *reinterpret_cast<const float4 *>(wr[b] + mn + lo);
-      }
-      if (m + 256 * h < d) {
+          wc[b] = *reinterpret_cast<const float4 *>(wl + (rw * SC_R + b) * SC_CH);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
 #pragma unroll
           for (int a = 0; a < SC_T; ++a) {
-            const float xv = xc[h][a].at(r);
+            const float xv = xc[a].at(r);
 #pragma unroll
             for (int b = 0; b < SC_R; ++b) {
-              const float4 w4 = wc[h][b];
+              const float4 w4 = wc[b];
               const float wv4 = r == 0 ? w4.x : r == 1 ? w4.y : r == 2 ? w4.z : w4.w;
               acc[a][b] = __builtin_fmaf(xv, wv4, acc[a][b]);
             }
             if (do_ss) sacc[a] = __builtin_fmaf(xv, xv, sacc[a]);
           }
         }
+        if (m + 1 < nch) {
+          // buffer buf ^ 1 was last read for chunk m - 1, before the
+          // previous barrier
+          put(st[(q + 1) % SC_PF], buf ^ 1);
+          lds_barrier();
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if (m + SC_PF < nch) fetch(st[q], (m + SC_PF) * SC_CH);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
   }
+  __syncthreads();          // the chunk buffers become the partials
 
-  float *Pw = P[wv];
+  float *Pw = lds.P[wv];
 #pragma unroll
   for (int a = 0; a < SC_T; ++a) {
 #pragma unroll
@@ -143,9 +215,9 @@ void k_scores(const XT *__restrict__ x, int B, int d,
     Pw[(SC_T * SC_R + a) * SC_PAD + lane] = sacc[a];
   }
   __syncthreads();
-  {
+  if (lane < SC_T * SC_R) {
     const float v = lds_tree(Pw, lane);          // dot product `lane` of the tile
-    const int t = t0 + lane / SC_R, r = r0 + lane % SC_R;
+    const int t = tb0 + tw * SC_T + lane / SC_R, r = rb0 + rw * SC_R + lane % SC_R;
     if (t < B && r < rows) {
       if (r < n_router)
         logits[(size_t)t * n_router + r] = beta ? v + beta[r] : v;
@@ -155,7 +227,8 @@ void k_scores(const XT *__restrict__ x, int B, int d,
   }
   if (do_ss && lane < SC_T) {
     const float v = lds_tree(Pw, SC_T * SC_R + lane);
-    if (t0 + lane < B) ss[t0 + lane] = v;
+    const int t = tb0 + tw * SC_T + lane;
+    if (t < B) ss[t] = v;
   }
 }
 
@@ -261,7 +334,7 @@ static void launch_scores_t(const XT *x, int B, int d, const float *Wr,
                             int n_pred, float *logits, float *q, float *ss,
                             hipStream_t st) {
   const int rows = n_router + n_pred;
-  dim3 grid((B + SC_T - 1) / SC_T, (rows + SC_R * SC_WAVES - 1) / (SC_R * SC_WAVES));
+  dim3 grid((B + SC_TB - 1) / SC_TB, (rows + SC_RB - 1) / SC_RB);
   launch_k(k_scores<XT>, grid, dim3(SC_WAVES * WAVE), 0, st, x, B, d,
                      Wr, beta, n_router, A, n_pred, logits, q, ss);
 }
