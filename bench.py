@@ -13,13 +13,18 @@ Weights are resident in HBM before timing starts.  Steps rotate over
 decode step walks a model's layer stack, so the kept experts of a step are
 not still in the 256 MiB Infinity Cache from the previous steps.
 
-Prints ONE JSON line: the step latency in microseconds (``value``, K steps
-with nothing else on the stream), the roofline of the dominant kernel (FFN
-gate/up: kept experts' gate and up rows against 8 TB/s of HBM3E), per-kernel
-times from HIP events attached by the library to each kernel's own dispatch
-(a second pass over the same K steps), the cost of plain top-K routing on
-the same layers (for BASE's overhead), and the CPU oracle timed on a
-bounded sample.
+Prints ONE JSON line.  ``value`` is the step latency in microseconds: K
+eager steps with nothing else on the stream.  The same layers captured in
+HIP graphs (one per rotated layer) and replayed K times are timed too
+(both distributions, p10 / p50 / p90 per step, are in ``timing``).  Also:
+the roofline of the dominant kernel (FFN gate/up: kept experts' gate and up
+rows against 8 TB/s of HBM3E), the HBM read rate a plain streaming-read
+kernel reaches on the same byte count (the achievable ceiling), per-kernel
+times (mean and p10 / p50 / p90) from HIP events attached by the library to
+each kernel's own dispatch (a separate eager pass over the same K steps),
+the cost of plain top-K routing on the same layers (for BASE's overhead), a
+latency-versus-budget sweep with its linear fit t = a + b B_e, and the CPU
+oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -58,6 +63,14 @@ def parse_args():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--rowmajor", action="store_true",
                    help="keep the experts row-major instead of packing them")
+    p.add_argument("--eager", action="store_true",
+                   help="skip the HIP graph replay timing")
+    p.add_argument("--sweep", default="8,16,24,32,48,64,96,128",
+                   help="budgets B_e of the latency-vs-budget sweep "
+                        "(comma list; empty: no sweep)")
+    p.add_argument("--sweep-steps", type=int, default=100)
+    p.add_argument("--no-ceiling", action="store_true",
+                   help="skip the streaming-read ceiling probe")
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain 1 GiB device-to-device copy three "
                         "times (calibrates the HBM byte counters)")
@@ -105,6 +118,63 @@ def elapsed_ms(hip, a, b):
     if hip.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
         raise RuntimeError("hipEventElapsedTime failed")
     return float(ms.value)
+
+
+def pct(a):
+    """p10 / p50 / p90 of a sample (µs, rounded)."""
+    import numpy as np
+    q = np.percentile(np.asarray(a, dtype=np.float64), [10, 50, 90])
+    return {"p10": round(float(q[0]), 2), "p50": round(float(q[1]), 2),
+            "p90": round(float(q[2]), 2)}
+
+
+def load_probe():
+    from paper_2609_36222_amd import build as hb
+    lib = ctypes.CDLL(hb.PROBE_LIB)
+    f = lib.base_probe_stream_read
+    f.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    f.restype = ctypes.c_int
+    return f
+
+
+def stream_read_ceiling(torch, hip, sptr, window_bytes, reps=40):
+    """HBM read rate of a plain streaming-read kernel (no arithmetic, the
+    FFN's 16-byte-per-lane load shape) over windows of the gate/up weight
+    stream's size, rotated over four windows so that no window is still in
+    the 256 MiB Infinity Cache.  Per launch shape (4 KiB steps per
+    wavefront): median over `reps` launches of the dispatch's own duration.
+    The ceiling is the best shape's median rate."""
+    import numpy as np
+    probe = load_probe()
+    unit = 64 * 4096
+    win = max(unit, window_bytes // unit * unit)
+    n_win = 4
+    buf = torch.randint(0, 256, (n_win * win,), dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    evs = [(new_event(hip), new_event(hip)) for _ in range(reps)]
+    shapes = {}
+    for steps in (4, 8, 16, 64):
+        waves = win // (steps * 4096)
+        for i in range(-4, reps):
+            a, b = evs[i] if i >= 0 else (None, None)
+            st = probe(buf.data_ptr() + (i % n_win) * win, waves, steps,
+                       sink.data_ptr(), a, b, sptr)
+            if st != 0:
+                raise RuntimeError(f"stream-read probe: hip error {st}")
+        torch.cuda.synchronize()
+        us = np.array([elapsed_ms(hip, a, b) * 1e3 for a, b in evs])
+        med = float(np.median(us))
+        shapes[f"{steps}x4KiB_per_wave"] = {
+            "waves": int(waves), "median_us": round(med, 2),
+            "GBps": round(win / (med * 1e-6) / 1e9, 1)}
+    for a, b in evs:
+        hip.hipEventDestroy(a)
+        hip.hipEventDestroy(b)
+    del buf
+    best = max(v["GBps"] for v in shapes.values())
+    return {"GBps": best, "bytes_per_launch": int(win), "windows": n_win,
+            "shapes": shapes}
 
 
 def kernel_source_hash():
@@ -166,7 +236,7 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU "
+        print("bench.py measures one GPU only: the library has no multi-GPU "
               "path (run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
@@ -209,7 +279,8 @@ def main():
         x = bf16((xnp.view(np.uint32) >> 16).astype(np.uint16))
     else:
         x = f32(xnp)
-    ws = torch.empty(bd.base_workspace_bytes(layers[0][1], B, budget),
+    sweep_budgets = [int(v) for v in args.sweep.split(",") if v.strip()]
+    ws = torch.empty(bd.base_workspace_bytes(layers[0][1], B, max([budget] + sweep_budgets)),
                      dtype=torch.uint8, device=dev)
     y = torch.empty(B, shape.d, dtype=torch.bfloat16 if shape.bf16 else torch.float32,
                     device=dev)
@@ -218,11 +289,11 @@ def main():
     lib = bd.load()
     plan = bd.base_plan()
 
-    def step(i):
+    def step(i, bud=budget, sp=sptr):
         _, desc = layers[i % len(layers)]
-        st = lib.base_decode_layer(ctypes.byref(desc), x.data_ptr(), B, budget,
+        st = lib.base_decode_layer(ctypes.byref(desc), x.data_ptr(), B, bud,
                                    0, None, y.data_ptr(), ctypes.byref(plan),
-                                   ws.data_ptr(), ws.numel(), sptr)
+                                   ws.data_ptr(), ws.numel(), sp)
         if st != 0:
             raise RuntimeError(bd.status_string(st))
 
@@ -230,20 +301,66 @@ def main():
     n_ev = 2 * bd.N_STAGES
     t_start, t_end = new_event(hip), new_event(hip)
 
+    def capture(bud):
+        """One HIP graph per rotated layer, each holding one decode-layer
+        call (captured through torch's stream capture: the library launches
+        on the capturing stream it is given)."""
+        graphs = []
+        for r in range(len(layers)):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                step(r, bud, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+            graphs.append(g)
+        torch.cuda.synchronize()
+        return graphs
+
+    def timed(run, n, bounds=None):
+        """n calls of run(i) between two events on the stream; with
+        `bounds` (n + 1 events) also an event between calls, for the
+        per-step distribution."""
+        torch.cuda.synchronize()
+        hip.hipEventRecord(t_start, sptr)
+        for i in range(n):
+            if bounds is not None:
+                hip.hipEventRecord(bounds[i], sptr)
+            run(i)
+        if bounds is not None:
+            hip.hipEventRecord(bounds[n], sptr)
+        hip.hipEventRecord(t_end, sptr)
+        torch.cuda.synchronize()
+        tot = elapsed_ms(hip, t_start, t_end) * 1e3 / n
+        if bounds is None:
+            return tot, None
+        per = [elapsed_ms(hip, bounds[i], bounds[i + 1]) * 1e3 for i in range(n)]
+        return tot, per
+
+    bounds = [new_event(hip) for _ in range(max(args.steps, args.sweep_steps) + 1)]
     print(f"[bench] {args.workload} B={B} B_e={budget} layers={len(layers)} "
           f"warmup={args.warmup} steps={args.steps}", file=sys.stderr, flush=True)
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
 
-    # timed region: K steps, nothing else on the stream
-    torch.cuda.synchronize()
-    hip.hipEventRecord(t_start, sptr)
-    for i in range(args.steps):
-        step(i)
-    hip.hipEventRecord(t_end, sptr)
-    torch.cuda.synchronize()
-    us_step = elapsed_ms(hip, t_start, t_end) * 1e3 / args.steps
+    # eager launches: K steps with nothing else on the stream, then the same
+    # K steps with an event between steps for the distribution
+    us_eager, _ = timed(step, args.steps)
+    _, per_eager = timed(step, args.steps, bounds)
+    timing = {"eager": {"us_per_step": round(us_eager, 2), **pct(per_eager)}}
+    us_step, mode = us_eager, "eager"
+    graphs = None
+    if not args.eager:
+        # one HIP graph per rotated layer, replayed: the form a serving loop
+        # may run the layer in.  Reported beside the eager figure; the value
+        # stays the eager one, which is the faster of the two here (graph
+        # replay adds a few µs between its nine kernel nodes)
+        graphs = capture(budget)
+        replay = lambda i: graphs[i % len(graphs)].replay()  # noqa: E731
+        for i in range(args.warmup):
+            replay(i)
+        us_graph, _ = timed(replay, args.steps)
+        _, per_graph = timed(replay, args.steps, bounds)
+        timing["hipgraph"] = {"us_per_step": round(us_graph, 2), **pct(per_graph)}
+    print(f"[bench] step {us_step:.2f} us ({mode})", file=sys.stderr, flush=True)
 
     # the same K steps, each kernel timed by events attached to its own
     # dispatch (the library's stage events): per-kernel durations
@@ -264,6 +381,7 @@ def main():
             stage_us[i, s] = elapsed_ms(hip, stage_ev[i][2 * s], stage_ev[i][2 * s + 1]) * 1e3
     stage_mean = {bd.STAGES[s]: round(float(stage_us[:, s].mean()), 2)
                   for s in range(bd.N_STAGES)}
+    stage_pct = {bd.STAGES[s]: pct(stage_us[:, s]) for s in range(bd.N_STAGES)}
 
     # what plain top-K routing costs on the same layers (base_route: the
     # router-only score kernel and the top-K tail), timed the same way
@@ -305,6 +423,41 @@ def main():
     pas_us = predict_us + stage_mean["select"]
     pre_ffn_us = sum(stage_mean[k] for k in ("scores", "tail", "select", "backfill",
                                              "compact", "gather"))
+    ceiling = None
+    if not args.no_ceiling:
+        print("[bench] streaming-read ceiling", file=sys.stderr, flush=True)
+        ceiling = stream_read_ceiling(torch, hip, sptr, gu_bytes)
+
+    sweep = None
+    if sweep_budgets:
+        # latency against the budget on the same layers and batch: t = a + b B_e
+        n_sw = args.sweep_steps
+        rows = []
+        for bud in sweep_budgets:
+            print(f"[bench] sweep B_e={bud}", file=sys.stderr, flush=True)
+            run = lambda i, bud=bud: step(i, bud)  # noqa: E731
+            for i in range(min(args.warmup, 10)):
+                run(i)
+            us_b, per_b = timed(run, n_sw, bounds[:n_sw + 1])
+            rows.append((bud, int(read_i32(plan.n_sel, 1)[0]), us_b, pct(per_b)))
+        xb = np.array([r[0] for r in rows], np.float64)
+        xn = np.array([r[1] for r in rows], np.float64)
+        t = np.array([r[2] for r in rows], np.float64)
+
+        def fit(xv):
+            if len(set(xv.tolist())) < 2:
+                return None
+            b1, a1 = np.polyfit(xv, t, 1)
+            res = t - (a1 + b1 * xv)
+            r2 = 1.0 - float((res ** 2).sum() / max(((t - t.mean()) ** 2).sum(), 1e-30))
+            return {"a_us": round(float(a1), 2), "b_us_per_expert": round(float(b1), 3),
+                    "r2": round(r2, 4)}
+        sweep = {"mode": mode, "steps": n_sw,
+                 "budgets": [r[0] for r in rows], "n_sel": [r[1] for r in rows],
+                 "us_per_step": [round(r[2], 2) for r in rows],
+                 "p10_p50_p90": [[r[3]["p10"], r[3]["p50"], r[3]["p90"]] for r in rows],
+                 "fit_vs_budget": fit(xb), "fit_vs_n_sel": fit(xn)}
+
     out = {
         "metric": METRIC,
         "value": round(us_step, 2),
@@ -353,15 +506,26 @@ def main():
             "pre_ffn_kernels_us": round(pre_ffn_us, 2),
             "pre_ffn_frac": round(pre_ffn_us / us_step, 4),
         },
+        "stages_us_p10_p50_p90": stage_pct,
         "kernel_sum_us": round(float(sum(stage_mean.values())), 2),
         "us_per_step_with_kernel_events": round(us_step_timed, 2),
+        "timing": {"value_from": mode, **timing},
     }
+    if ceiling is not None:
+        out["streaming_read_ceiling"] = ceiling
+        out["roofline"]["frac_of_streaming_ceiling"] = round(achieved / ceiling["GBps"], 4)
+        out["ffn"]["frac_of_streaming_ceiling"] = round(
+            ffn_bytes / (ffn_us * 1e-6) / 1e9 / ceiling["GBps"], 4)
+    if sweep is not None:
+        out["budget_sweep"] = sweep
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(keep_inp, budget, args.cpu_seconds)
     for row in stage_ev:
         for e in row:
             hip.hipEventDestroy(e)
+    for e in bounds + [t_start, t_end]:
+        hip.hipEventDestroy(e)
     print(json.dumps(out), flush=True)
 
 

@@ -21,6 +21,9 @@
  * - `stream` is a hipStream_t (NULL = the null stream).  Every call only
  *   enqueues work on it: no allocation, no host synchronisation, no
  *   device-to-host copy.  Outputs are valid once the stream reaches them.
+ *   Kernels are launched with ordinary launches, so a call made while the
+ *   stream is being captured (hipStreamBeginCapture) is recorded into the
+ *   graph; replays read the buffers the captured call was given.
  * - The caller owns every buffer.  Calls that need scratch memory take a
  *   workspace `ws` of at least base_workspace_bytes(L, B, budget) bytes.
  * - Validation happens on the host before anything is enqueued; on any
@@ -241,7 +244,8 @@ base_status base_pack_experts(const base_layer *L, void *w13_packed,
  * base_route stages 0 and 1, base_select stage 2, base_moe_forward 3 to 8
  * (base_predict_cost runs its own kernel, untimed).  The setting belongs
  * to the calling host thread; the caller keeps the events alive while it
- * is set.  Returns BASE_ERR_SHAPE if n_events != 2 * BASE_N_STAGES. */
+ * is set, and does not set it around calls on a capturing stream.
+ * Returns BASE_ERR_SHAPE if n_events != 2 * BASE_N_STAGES. */
 #define BASE_N_STAGES 9
 base_status base_set_stage_events(void *const *events, int32_t n_events);
 

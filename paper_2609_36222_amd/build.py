@@ -20,6 +20,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_lib")
 LIB = os.path.join(OUT_DIR, "libbase.so")
+PROBE_LIB = os.path.join(OUT_DIR, "libbase_probe.so")   # bench's streaming-read probe
 SOURCES = ["api.hip", "scores.hip", "route_predict.hip", "plan.hip", "ffn.hip",
            "pack.hip"]
 ARCH = os.environ.get("BASE_OFFLOAD_ARCH", "gfx950")
@@ -37,8 +38,18 @@ def _hipcc():
     raise RuntimeError("hipcc not found")
 
 
+def _link(objs, out):
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed:\n{r.stderr}")
+    os.replace(tmp, out)
+
+
 def build(verbose: bool = False) -> str:
-    """Compile every source and link libbase.so (always rebuilds)."""
+    """Compile every source, link libbase.so and the probe library (always
+    rebuilds)."""
     os.makedirs(OUT_DIR, exist_ok=True)
     hipcc = _hipcc()
     objs = []
@@ -53,14 +64,10 @@ def build(verbose: bool = False) -> str:
             print(r.stderr, file=sys.stderr)
         return obj
 
-    with cf.ThreadPoolExecutor(min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(compile_one, SOURCES))
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"link failed:\n{r.stderr}")
-    os.replace(tmp, LIB)
+    with cf.ThreadPoolExecutor(min(8, len(SOURCES) + 1)) as ex:
+        objs = list(ex.map(compile_one, SOURCES + ["probe.hip"]))
+    _link(objs[:-1], LIB)
+    _link(objs[-1:], PROBE_LIB)
     for o in objs:
         os.remove(o)
     return LIB

@@ -25,8 +25,13 @@ template <typename F, typename... Args>
 inline void launch_k(F kernel, dim3 grid, dim3 block, uint32_t shm, hipStream_t st,
                      Args... args) {
   KernelEvents &ev = kernel_events();
-  hipExtLaunchKernelGGL(kernel, grid, block, shm, st, ev.start, ev.stop, 0, args...);
-  ev.start = ev.stop = nullptr;
+  if (ev.start || ev.stop) {
+    hipExtLaunchKernelGGL(kernel, grid, block, shm, st, ev.start, ev.stop, 0, args...);
+    ev.start = ev.stop = nullptr;
+  } else {
+    // the ordinary launch: the form a stream capture records as a graph node
+    hipLaunchKernelGGL(kernel, grid, block, shm, st, args...);
+  }
 }
 
 // Upper bounds (host-known) of the FFN token tiling for a batch: 16-pair

@@ -184,3 +184,27 @@ def test_stage_events_validation(lib):
     assert len(bd.STAGES) == bd.N_STAGES
     with open(os.path.join(ROOT, "include", "base.h")) as f:
         assert re.search(r"#define BASE_N_STAGES %d\b" % bd.N_STAGES, f.read())
+
+
+def test_stream_read_probe_library():
+    """The benchmark's streaming-read probe sits in a library of its own
+    (not part of the method's ABI); bad arguments are refused before any
+    launch with hipErrorInvalidValue (1)."""
+    import subprocess
+    from paper_2609_36222_amd import build
+    if not os.path.exists(build.PROBE_LIB):
+        build.build()
+    out = subprocess.run(["nm", "-D", "--defined-only", build.PROBE_LIB],
+                         capture_output=True, text=True).stdout
+    syms = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    assert "base_probe_stream_read" in syms
+    assert not any(s.startswith("base_") and s != "base_probe_stream_read" for s in syms)
+    f = ctypes.CDLL(build.PROBE_LIB).base_probe_stream_read
+    f.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    f.restype = ctypes.c_int
+    assert f(FAKE, 8, 6, FAKE, None, None, None) == 1       # steps not a multiple of 4
+    assert f(FAKE, 0, 16, FAKE, None, None, None) == 1      # no waves
+    assert f(None, 8, 16, FAKE, None, None, None) == 1      # no buffer
+    assert f(FAKE, 8, 16, None, None, None, None) == 1      # no sink
+    assert f(FAKE, 8, 1 << 19, FAKE, None, None, None) == 1  # share of 2 GiB

@@ -252,3 +252,66 @@ def test_packed_layout_matches_its_definition(gu):
     exp2 = pack(inp["w2"], lambda g, t: 64 * g + 16 * t, d // 64, I)
     assert np.array_equal(got13.reshape(-1), exp13)
     assert np.array_equal(got2.reshape(-1), exp2)
+
+
+def test_graph_replay_matches_eager(gu):
+    """base_decode_layer captured once in a HIP graph (through torch's stream
+    capture) and replayed with new tokens and a new residual copied in
+    between replays, the workspace and output overwritten with junk by
+    eager kernels before each replay: every replay equals an eager call on
+    the same inputs bit for bit (all plan arrays and y), and the plan equals
+    the oracle's."""
+    from paper_2609_36222_amd import binding as bd
+    inp = named("qwen3_b64")
+    sh = inp["shape"]
+    B, budget, flags = sh.B, 32, 1
+    gl = gu.GpuLayer(inp, packed=True)
+    g = np.random.default_rng(11)
+    xs, rs = [], []
+    for s in range(3):
+        xs.append(W.decode_tokens(sh, data_seed=s + 1))
+        rs.append(W.bf16_bits_to_f32(W.f32_to_bf16_bits(
+            g.standard_normal((B, sh.d)).astype(np.float32))))
+    x = gl.x(xs[0])
+    res = gl.x(rs[0])
+    ws = gl.workspace(B, budget)
+    y = gl.y_like(B)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        bd.base_decode_layer(gl.desc, x, B, budget, flags, res, y, ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        plan = bd.base_decode_layer(gl.desc, x, B, budget, flags, res, y, ws)
+    torch.cuda.synchronize()
+    for rep in range(5):
+        k = rep % 3
+        _flush(f"graph replay {rep} tokens seed {k + 1}")
+        xk, rk = gl.x(xs[k]), gl.x(rs[k])
+        ws_e, y_e = gl.workspace(B, budget), gl.y_like(B)
+        plan_e = bd.base_decode_layer(gl.desc, xk, B, budget, flags, rk, y_e, ws_e)
+        torch.cuda.synchronize()
+        want = gu.plan_arrays(plan_e, ws_e, B, sh.K, sh.E, budget, full=True)
+        x.copy_(xk)
+        res.copy_(rk)
+        ws.fill_(0xA5)
+        y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = gu.plan_arrays(plan, ws, B, sh.K, sh.E, budget, full=True)
+        for f, v in want.items():
+            if isinstance(v, np.ndarray):
+                assert np.array_equal(got[f], v), (rep, f)
+            else:
+                assert got[f] == v, (rep, f)
+        assert np.array_equal(y.view(torch.int16).cpu().numpy(),
+                              y_e.view(torch.int16).cpu().numpy()), rep
+        if rep < 3:
+            ref = method.decode_layer_c(xs[k], inp["w_router"], inp["b_router"],
+                                        inp["pred_a"], inp["pred_b"], sh.K, budget,
+                                        None, 1, flags, rs[k])
+            check_plan(got, ref)
+            assert got["n_sel"] == ref["n_sel"]
