@@ -227,6 +227,18 @@ def decode_tokens(shape: LayerShape, layer: int = 0, data_seed: int = 0,
                          stream=_S_TOKENS, data_seed=data_seed)
 
 
+def stack_layer_input(h: np.ndarray, bf16: bool = True) -> np.ndarray:
+    """Input of a stacked layer from the residual stream h [B, d]: the
+    unit-gain RMSNorm a pre-norm decoder block applies before its MoE, in
+    fp32, rounded to bf16 for bf16 layers.  The layer then adds its MoE
+    output to h itself (the residual), so the stream grows slowly with depth
+    instead of compounding the experts' gain."""
+    z = _rmsnorm_rows(h)
+    if bf16:
+        z = bf16_bits_to_f32(f32_to_bf16_bits(z))
+    return np.ascontiguousarray(z, dtype=np.float32)
+
+
 def layer_inputs(name: str, layer: int = 0, data_seed: int = 0,
                  with_experts: bool = True, B=None):
     """Everything one decode layer consumes, as numpy arrays."""
