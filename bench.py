@@ -55,7 +55,9 @@ def parse_args():
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", default="qwen3_b256")
-    p.add_argument("--budget", type=int, default=32)
+    p.add_argument("--budget", type=int, default=None,
+                   help="expert budget B_e (default: the workload's first, 32 "
+                        "for the batch-256 layer)")
     p.add_argument("--layers", type=int, default=4,
                    help="distinct layers the steps rotate over")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -200,16 +202,21 @@ def stored_traffic(workload, budget):
     return float(m_b.group(1))
 
 
+def blas_threads():
+    try:
+        import numpy  # noqa: F401  (loads the BLAS threadpoolctl reports)
+        from threadpoolctl import threadpool_info
+        return int(max([i.get("num_threads", 1) for i in threadpool_info()] + [1]))
+    except Exception:
+        return os.cpu_count() or 1
+
+
 def cpu_baseline(inp, budget, seconds):
     """The CPU oracle, as it stands, on whole decode layers of the same
     workload until the time budget is spent."""
     import numpy as np  # noqa: F401
     from oracle import method, carith
-    try:
-        from threadpoolctl import threadpool_info
-        blas = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:
-        blas = os.cpu_count() or 1
+    blas = blas_threads()
     carith.build()
     sh = inp["shape"]
     ex = method.Experts(inp["w13"], inp["w2"], sh.bf16)
@@ -227,6 +234,164 @@ def cpu_baseline(inp, budget, seconds):
                 sample=f"{n} full decode layers of the timed workload "
                        f"({sh.name}, B={sh.B}, B_e={budget}): canonical fp32 "
                        "scoring in C (1 thread) + fp64 NumPy/BLAS expert FFN")
+
+
+def bench_stack(args, shape, np, torch, W, bd):
+    """One step = the whole stack of MoE layers (48 Qwen3-shaped layers at
+    batch 128, B_e = 24 each), every layer's experts resident and distinct.
+
+    Inputs are those of the pre-norm residual stream: an untimed pass runs
+    the stack once (layer l takes RMSNorm(h_l), adds its MoE output to h_l;
+    the norm between layers is the decoder block's, done on the host) and
+    keeps every layer's x_l and h_l on the device; each timed step then runs
+    the 48 base_decode_layer calls on those inputs, nothing else."""
+    dev = torch.device("cuda", 0)
+    budget = args.budget
+    L, B, K = shape.layers, shape.B, shape.K
+
+    def f32(a):
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+
+    def bf16v(v):
+        u = (np.ascontiguousarray(v, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+        return torch.from_numpy(u.view(np.int16)).to(dev).view(torch.bfloat16)
+
+    def bits(b):
+        return torch.from_numpy(np.ascontiguousarray(b).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    def host(t):
+        u = t.view(torch.int16).cpu().numpy().view(np.uint16)
+        return (u.astype(np.uint32) << 16).view(np.float32)
+
+    lib = bd.load()
+    sptr = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    plan = bd.base_plan()
+    print(f"[bench] {shape.name}: building {L} layers", file=sys.stderr, flush=True)
+    layers, xs, hs, samples = [], [], [], []
+    h_np = W.layer_inputs(shape.name, layer=0, with_experts=False)["x"]
+    ws = None
+    y = torch.empty(B, shape.d, dtype=torch.bfloat16, device=dev)
+    for layer in range(L):
+        inp = W.layer_inputs(shape.name, layer=layer)
+        lay = bd.Layer(f32(inp["w_router"]), f32(inp["b_router"]), f32(inp["pred_a"]),
+                       f32(inp["pred_b"]), bits(inp["w13"]), bits(inp["w2"]))
+        lay = bd.packed_layer(lay, K)
+        desc = lay.desc(K)
+        if ws is None:
+            ws = torch.empty(bd.base_workspace_bytes(desc, B, budget), dtype=torch.uint8,
+                             device=dev)
+        x_np = h_np if layer == 0 else W.stack_layer_input(h_np)
+        x, h = bf16v(x_np), bf16v(h_np)
+        st = lib.base_decode_layer(ctypes.byref(desc), x.data_ptr(), B, budget, 0,
+                                   h.data_ptr(), y.data_ptr(), ctypes.byref(plan),
+                                   ws.data_ptr(), ws.numel(), sptr)
+        if st != 0:
+            raise RuntimeError(bd.status_string(st))
+        torch.cuda.synchronize()
+        if layer in (0, L // 2, L - 1):
+            samples.append(dict(inp, x=x_np, residual=h_np))
+        layers.append((lay, desc))
+        xs.append(x)
+        hs.append(h)
+        h_np = host(y)
+        del inp
+        if layer % 8 == 7:
+            print(f"[bench] built layer {layer}", file=sys.stderr, flush=True)
+
+    def step(_i, sp=sptr):
+        for layer in range(L):
+            st = lib.base_decode_layer(ctypes.byref(layers[layer][1]), xs[layer].data_ptr(),
+                                       B, budget, 0, hs[layer].data_ptr(), y.data_ptr(),
+                                       ctypes.byref(plan), ws.data_ptr(), ws.numel(), sp)
+            if st != 0:
+                raise RuntimeError(bd.status_string(st))
+
+    hip = hip_runtime()
+    t0, t1 = new_event(hip), new_event(hip)
+    bounds = [new_event(hip) for _ in range(args.steps + 1)]
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    hip.hipEventRecord(t0, sptr)
+    for i in range(args.steps):
+        step(i)
+    hip.hipEventRecord(t1, sptr)
+    torch.cuda.synchronize()
+    us_step = elapsed_ms(hip, t0, t1) * 1e3 / args.steps
+    for i in range(args.steps):
+        hip.hipEventRecord(bounds[i], sptr)
+        step(i)
+    hip.hipEventRecord(bounds[args.steps], sptr)
+    torch.cuda.synchronize()
+    per = [elapsed_ms(hip, bounds[i], bounds[i + 1]) * 1e3 for i in range(args.steps)]
+
+    # per-kernel durations: one more step with every layer's stage events
+    n_ev = 2 * bd.N_STAGES
+    evs = [[new_event(hip) for _ in range(n_ev)] for _ in range(L)]
+    keep = [(ctypes.c_void_p * n_ev)(*row) for row in evs]
+    for layer in range(L):
+        lib.base_set_stage_events(keep[layer], n_ev)
+        st = lib.base_decode_layer(ctypes.byref(layers[layer][1]), xs[layer].data_ptr(), B,
+                                   budget, 0, hs[layer].data_ptr(), y.data_ptr(),
+                                   ctypes.byref(plan), ws.data_ptr(), ws.numel(), sptr)
+        if st != 0:
+            raise RuntimeError(bd.status_string(st))
+    lib.base_set_stage_events(None, 0)
+    torch.cuda.synchronize()
+    stage_us = np.array([[elapsed_ms(hip, evs[layer][2 * s], evs[layer][2 * s + 1]) * 1e3
+                          for s in range(bd.N_STAGES)] for layer in range(L)])
+    stage_sum = {bd.STAGES[s]: round(float(stage_us[:, s].sum()), 1)
+                 for s in range(bd.N_STAGES)}
+    gu_bytes = budget * 2 * shape.I * shape.d * 2
+    gu_us = float(stage_us[:, bd.STAGES.index("ffn_gateup")].mean())
+    ffn_us = float(stage_us[:, bd.STAGES.index("ffn_gateup")].sum()
+                   + stage_us[:, bd.STAGES.index("ffn_down")].sum())
+    achieved = gu_bytes / (gu_us * 1e-6) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(us_step, 1),
+        "unit": "us",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(us_step / 1e3, 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {
+            "workload": f"{shape.name}: {L} Qwen3-30B-A3B-shaped MoE layers d={shape.d} "
+                        f"E={shape.E} top-{K} I={shape.I}, batch {B}, B_e={budget} per "
+                        "layer, pre-norm residual stream carried, bf16 experts "
+                        f"({L * shape.E * 3 * shape.I * shape.d * 2 / 1e9:.1f} GB resident)",
+            "batch": B, "budget": budget, "layers": L, "expert_layout": "packed"},
+        "us_per_layer": round(us_step / L, 2),
+        "timing": {"eager": {"us_per_step": round(us_step, 1), **pct(per)}},
+        "roofline": {
+            "bound": "hbm", "kernel": "k_gateup_bf16 (FFN gate/up)",
+            "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "algorithmic_bytes_per_launch": gu_bytes, "avg_launch_us": round(gu_us, 2)},
+        "ffn": {"retained_weight_bytes": L * budget * 3 * shape.I * shape.d * 2,
+                "us": round(ffn_us, 1)},
+        "stages_us_summed_over_layers": stage_sum,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        from oracle import method, carith
+        carith.build()
+        n, t_start = 0, time.perf_counter()
+        while True:
+            smp = samples[n % len(samples)]
+            ex = method.Experts(smp["w13"], smp["w2"], True)
+            method.decode_layer_c(smp["x"], smp["w_router"], smp["b_router"], smp["pred_a"],
+                                  smp["pred_b"], K, budget, ex, 1, 0, smp["residual"])
+            n += 1
+            if time.perf_counter() - t_start >= args.cpu_seconds and n >= len(samples):
+                break
+        per_layer = (time.perf_counter() - t_start) / n
+        out["cpu_baseline"] = dict(
+            value=round(per_layer * L * 1e6, 0), unit="us per 48-layer step (extrapolated)",
+            cores=blas_threads(), kind="oracle",
+            sample=f"{n} layer calls over layers 0, {L // 2} and {L - 1} of the stack "
+                   f"(B={B}, B_e={budget}, residual carried), mean x {L}")
+    print(json.dumps(out), flush=True)
 
 
 def main():
@@ -251,7 +416,11 @@ def main():
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
     shape = W.WORKLOADS[args.workload]
-    assert shape.layers == 1, "stacked workloads are not a bench step"
+    if args.budget is None:
+        args.budget = shape.budgets[0]
+    if shape.layers > 1:
+        bench_stack(args, shape, np, torch, W, bd)
+        return
     budget = args.budget
 
     def f32(a):
