@@ -73,6 +73,8 @@ def parse_args():
     p.add_argument("--sweep-steps", type=int, default=100)
     p.add_argument("--no-ceiling", action="store_true",
                    help="skip the streaming-read ceiling probe")
+    p.add_argument("--working-set-probe", action="store_true",
+                   help="only measure the streaming-read rate by working-set size")
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain 1 GiB device-to-device copy three "
                         "times (calibrates the HBM byte counters)")
@@ -134,8 +136,8 @@ def load_probe():
     from paper_2609_36222_amd import build as hb
     lib = ctypes.CDLL(hb.PROBE_LIB)
     f = lib.base_probe_stream_read
-    f.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p,
-                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    f.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     f.restype = ctypes.c_int
     return f
 
@@ -160,7 +162,7 @@ def stream_read_ceiling(torch, hip, sptr, window_bytes, reps=40):
         waves = win // (steps * 4096)
         for i in range(-4, reps):
             a, b = evs[i] if i >= 0 else (None, None)
-            st = probe(buf.data_ptr() + (i % n_win) * win, waves, steps,
+            st = probe(buf.data_ptr() + (i % n_win) * win, waves, steps, 0,
                        sink.data_ptr(), a, b, sptr)
             if st != 0:
                 raise RuntimeError(f"stream-read probe: hip error {st}")
@@ -177,6 +179,42 @@ def stream_read_ceiling(torch, hip, sptr, window_bytes, reps=40):
     best = max(v["GBps"] for v in shapes.values())
     return {"GBps": best, "bytes_per_launch": int(win), "windows": n_win,
             "shapes": shapes}
+
+
+def working_set_probe(reps=20):
+    """Read rate of the streaming-read probe by working-set size: every
+    launch reads 201 MB (the gate/up weight bytes of the batch-256 layer at
+    B_e = 32) in the FFN's load shape, from a working set of 2 MB to 201 MB
+    that the launch's wavefronts share (each byte read 201 MB / working set
+    times).  Shows where the L2s, the Infinity Cache and HBM each serve it."""
+    import numpy as np
+    import torch
+    torch.cuda.set_device(0)
+    hip = hip_runtime()
+    probe = load_probe()
+    sptr = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    launch = 201326592
+    buf = torch.randint(0, 256, (launch,), dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    evs = [(new_event(hip), new_event(hip)) for _ in range(reps)]
+    rows = []
+    for steps in (4, 16):
+        waves = launch // (steps * 4096)
+        for ws in (1 << 21, 1 << 23, 1 << 25, 1 << 26, 1 << 27, launch):
+            shares = ws // (steps * 4096)
+            for i in range(-3, reps):
+                a, b = evs[i] if i >= 0 else (None, None)
+                st = probe(buf.data_ptr(), waves, steps, shares, sink.data_ptr(), a, b, sptr)
+                if st != 0:
+                    raise RuntimeError(f"stream-read probe: hip error {st}")
+            torch.cuda.synchronize()
+            med = float(np.median([elapsed_ms(hip, a, b) * 1e3 for a, b in evs]))
+            rows.append({"steps_per_wave": steps, "waves": waves, "working_set_bytes": ws,
+                         "median_us": round(med, 2),
+                         "GBps": round(launch / (med * 1e-6) / 1e9, 1)})
+            print(f"[bench] working set {ws:>10d} B, {steps:2d} steps per wave: "
+                  f"{rows[-1]['GBps']} GB/s", file=sys.stderr, flush=True)
+    print(json.dumps({"working_set_probe": rows, "bytes_per_launch": launch}), flush=True)
 
 
 def kernel_source_hash():
@@ -398,6 +436,9 @@ def main():
     args = parse_args()
     if args.copy_probe:
         copy_probe()
+        return
+    if args.working_set_probe:
+        working_set_probe()
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:

@@ -200,11 +200,11 @@ def test_stream_read_probe_library():
     assert "base_probe_stream_read" in syms
     assert not any(s.startswith("base_") and s != "base_probe_stream_read" for s in syms)
     f = ctypes.CDLL(build.PROBE_LIB).base_probe_stream_read
-    f.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p,
-                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    f.argtypes = [ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     f.restype = ctypes.c_int
-    assert f(FAKE, 8, 6, FAKE, None, None, None) == 1       # steps not a multiple of 4
-    assert f(FAKE, 0, 16, FAKE, None, None, None) == 1      # no waves
-    assert f(None, 8, 16, FAKE, None, None, None) == 1      # no buffer
-    assert f(FAKE, 8, 16, None, None, None, None) == 1      # no sink
-    assert f(FAKE, 8, 1 << 19, FAKE, None, None, None) == 1  # share of 2 GiB
+    assert f(FAKE, 8, 6, 0, FAKE, None, None, None) == 1       # steps not a multiple of 4
+    assert f(FAKE, 0, 16, 0, FAKE, None, None, None) == 1      # no waves
+    assert f(None, 8, 16, 0, FAKE, None, None, None) == 1      # no buffer
+    assert f(FAKE, 8, 16, 0, None, None, None, None) == 1      # no sink
+    assert f(FAKE, 8, 1 << 19, 0, FAKE, None, None, None) == 1  # share of 2 GiB
