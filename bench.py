@@ -63,6 +63,9 @@ def parse_args():
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="wall time budget of the CPU oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--score-rule", type=int, default=0,
+                   help="selection rule of the layers (0 BASE, 1 top-1 union, "
+                        "2 weight sum, 3 squared weight sum, 4 static energy)")
     p.add_argument("--rowmajor", action="store_true",
                    help="keep the experts row-major instead of packing them")
     p.add_argument("--eager", action="store_true",
@@ -475,7 +478,8 @@ def main():
         inp = W.layer_inputs(args.workload, layer=r)
         wdev = (bf16(inp["w13"]), bf16(inp["w2"])) if shape.bf16 else (f32(inp["w13"]), f32(inp["w2"]))
         lay = bd.Layer(f32(inp["w_router"]), f32(inp["b_router"]),
-                       f32(inp["pred_a"]), f32(inp["pred_b"]), *wdev)
+                       f32(inp["pred_a"]), f32(inp["pred_b"]), *wdev,
+                       score_rule=args.score_rule)
         if shape.bf16 and not args.rowmajor:   # one-time, outside timing
             lay = bd.packed_layer(lay, shape.K)
             del wdev
@@ -687,6 +691,7 @@ def main():
                         f"B_e={budget}, bf16 experts, fp32 router+predictor",
             "batch": B, "budget": budget, "n_sel": n_sel, "pairs": pairs,
             "expert_layout": "row-major" if (args.rowmajor or not shape.bf16) else "packed",
+            "score_rule": args.score_rule,
             "layers_rotated": len(layers),
         },
         "roofline": {

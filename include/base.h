@@ -66,7 +66,7 @@ typedef enum {
     BASE_ERR_ALIGN = -5,      /* misaligned pointer (see base_layer) */
     BASE_ERR_WORKSPACE = -6,  /* workspace smaller than base_workspace_bytes */
     BASE_ERR_HIP = -7,        /* a HIP launch failed */
-    BASE_ERR_FLAGS = -8       /* unknown bits in flags */
+    BASE_ERR_FLAGS = -8       /* unknown bits in flags, or unknown score_rule */
 } base_status;
 
 /* Element type of x, y, residual and the expert weights w13, w2.  Router
@@ -89,6 +89,30 @@ enum {
     BASE_FILL_DROP = 2
 };
 
+/* Selection rule of a layer (base_layer.score_rule): the per-pair score
+ * whose sum over the batch, D_u = sum_{t: u in R_t} score(t, u), ranks the
+ * experts (App. "Selection-rule ablation", Table selection_score_ablation).
+ * Every rule keeps min(budget, |union|) experts of the batch union, ties to
+ * the lower index, and feeds the same backfill. */
+enum {
+    /* predicted removal error w^2 exp(a_u . x/||x|| + b_u) (Sec. 3.4,
+     * eq. log_energy_predictor).  The method; default. */
+    BASE_SCORE_BASE = 0,
+    /* top-1 union: 1 for the token's first route, 0 for its others; the
+     * experts are ranked by membership (D_u > 0), then index, so a budget
+     * equal to the union's size keeps exactly the union. */
+    BASE_SCORE_TOP1 = 1,
+    /* router-weight sum: w */
+    BASE_SCORE_WEIGHT = 2,
+    /* squared router-weight sum: w^2 (one fp32 product) */
+    BASE_SCORE_WEIGHT_SQ = 3,
+    /* static expert energy: w^2 mu_u with mu_u the expert's mean
+     * calibration energy, given as pred_b = log mu_u; computed as the
+     * predictor's sequence with a_u . x/||x|| = 0, (w * w) * exp(b_u).
+     * pred_a is not read. */
+    BASE_SCORE_STATIC = 4
+};
+
 /* Layout of the expert weights w13 and w2 (see base_pack_experts). */
 enum {
     /* w13 [E][2I][d], w2 [E][d][I], row-major */
@@ -108,11 +132,15 @@ typedef struct base_layer {
     int32_t dtype;      /* base_dtype of x, y, residual, w13, w2 */
     int32_t norm_topk;  /* 1: w = p / sum_{top-K} p ; 0: w = softmax p */
     int32_t w_layout;   /* BASE_W_ROWMAJOR or BASE_W_PACKED */
+    int32_t score_rule; /* BASE_SCORE_* (0: the method's predicted error) */
     const float *w_router;  /* [E][d] fp32, 16-B aligned */
     const float *b_router;  /* [E] fp32 router bias, or NULL */
-    const float *pred_a;    /* [E][d] fp32 predictor slopes a_u, 16-B aligned */
+    const float *pred_a;    /* [E][d] fp32 predictor slopes a_u, 16-B
+                               aligned; read by BASE_SCORE_BASE only */
     const float *pred_b;    /* [E] fp32 predictor intercepts b_u (bias
-                               correction folded in, App. A) */
+                               correction folded in, App. A), or log mu_u
+                               for BASE_SCORE_STATIC; not read by the
+                               router-only rules */
     const void *w13;        /* [E][2I][d]: rows 0..I-1 gate, I..2I-1 up;
                                16-B aligned */
     const void *w2;         /* [E][d][I] down projection; 16-B aligned */
@@ -161,7 +189,9 @@ base_status base_route(const base_layer *L, const void *x, int32_t B,
 
 /* Predicted removal cost of every routed pair (Sec. 3.4, eq.
  * log_energy_predictor): z_bar = x / ||x|| (0 if x = 0),
- * s_hat = a_u . z_bar + b_u, cost = w^2 exp(s_hat).
+ * s_hat = a_u . z_bar + b_u, cost = w^2 exp(s_hat).  For a layer with
+ * another score_rule, that rule's per-pair score (see BASE_SCORE_*; x is
+ * then not read).
  *   topk_ids, topk_w  [B][K] as produced by base_route
  *   cost              [B][K] fp32 out */
 base_status base_predict_cost(const base_layer *L, const void *x, int32_t B,
@@ -173,8 +203,9 @@ base_status base_predict_cost(const base_layer *L, const void *x, int32_t B,
  *   scores          [E] fp32 out: D_hat_u = sum of cost over tokens routing u
  *   counts          [E] int32 out: number of tokens routing u
  *   sel_ids         [budget] int32 out: the kept experts in rank order
- *                   (D_hat desc, index asc) among experts with count > 0;
- *                   -1 beyond n_sel
+ *                   (D_hat desc, index asc; for BASE_SCORE_TOP1 layers
+ *                   (D_hat > 0) desc, index asc) among experts with
+ *                   count > 0; -1 beyond n_sel
  *   n_sel           [1] int32 out: min(budget, |batch union|)
  *   slot_of_expert  [E] int32 out: rank of u in sel_ids, or -1 */
 base_status base_select(const base_layer *L, int32_t B,

@@ -34,6 +34,11 @@ from . import carith
 GATE_PAPER, GATE_RENORM = 0, 1      # flags bit 0
 FILL_BACKFILL, FILL_DROP = 0, 2     # flags bit 1
 
+# Selection rules (App. selection-rule ablation): the per-pair score whose
+# batch sum D_u ranks the experts.  SCORE_BASE is the method.
+SCORE_BASE, SCORE_TOP1, SCORE_WEIGHT, SCORE_WEIGHT_SQ, SCORE_STATIC = 0, 1, 2, 3, 4
+SCORE_RULES = (SCORE_BASE, SCORE_TOP1, SCORE_WEIGHT, SCORE_WEIGHT_SQ, SCORE_STATIC)
+
 
 # ------------------------------------------------------------ bf16 helpers --
 def bf16_round(a):
@@ -182,6 +187,50 @@ def predict64(x, pred_a, pred_b, ids, w):
     return np.asarray(w, np.float64) ** 2 * np.exp(s)
 
 
+def pair_scores64(rule, x, pred_a, pred_b, ids, w):
+    """Per routed pair score of each selection rule, fp64 (App.
+    selection-rule ablation): BASE w^2 exp(a_u . z_bar + b_u); TOP1 1 for
+    the token's first-ranked route and 0 for the others (so that D_u > 0
+    exactly when u is some token's top-1); WEIGHT w; WEIGHT_SQ w^2; STATIC
+    w^2 mu_u, the expert's mean calibration energy, with mu_u = exp(b_u)
+    (pred_b holds log mu_u)."""
+    w = np.asarray(w, np.float64)
+    if rule == SCORE_BASE:
+        return predict64(x, pred_a, pred_b, ids, w)
+    if rule == SCORE_TOP1:
+        c = np.zeros(w.shape)
+        c[:, 0] = 1.0
+        return c
+    if rule == SCORE_WEIGHT:
+        return w.copy()
+    if rule == SCORE_WEIGHT_SQ:
+        return w ** 2
+    if rule == SCORE_STATIC:
+        return w ** 2 * np.exp(np.asarray(pred_b, np.float64)[ids])
+    raise ValueError(rule)
+
+
+def pair_scores_c(rule, x, pred_a, pred_b, ids, w):
+    """The same scores at the canonical fp32 level: BASE is carith.predict;
+    WEIGHT_SQ is one fp32 product w * w; STATIC is (w * w) * cexp(b_u), the
+    predictor's sequence with a_u . z_bar = 0; TOP1 and WEIGHT are exact."""
+    w = np.asarray(w, np.float32)
+    if rule == SCORE_BASE:
+        return carith.predict(x, pred_a, pred_b, ids, w)
+    if rule == SCORE_TOP1:
+        c = np.zeros(w.shape, np.float32)
+        c[:, 0] = np.float32(1.0)
+        return c
+    if rule == SCORE_WEIGHT:
+        return w.copy()
+    if rule == SCORE_WEIGHT_SQ:
+        return (w * w).astype(np.float32)
+    if rule == SCORE_STATIC:
+        e = carith.cexp(np.asarray(pred_b, np.float32)[ids])
+        return ((w * w) * e).astype(np.float32)
+    raise ValueError(rule)
+
+
 def aggregate64(ids, cost, E):
     """D_hat_u = sum_{t: u in R_t} cost(t,u); counts of routing tokens."""
     D = np.zeros(E)
@@ -191,14 +240,19 @@ def aggregate64(ids, cost, E):
 
 
 # -------------------------------------------------------------- selection ---
-def select(scores, counts, budget):
+def select(scores, counts, budget, binary=False):
     """Sec. 3.4/3.5: keep the n_sel = min(budget, |U|) experts of the batch
     union U = {u : count_u > 0} that come first in the order (score desc,
-    index asc).  Returns sel_ids [budget] (rank order, -1 padded), n_sel,
+    index asc).  With `binary` (the top-1-union rule) the order uses only
+    whether the score is positive (union membership), then the index.
+    Returns sel_ids [budget] (rank order, -1 padded), n_sel,
     slot_of_expert [E] (rank, or -1 when not retained)."""
     E = len(scores)
     U = [u for u in range(E) if counts[u] > 0]
-    U.sort(key=lambda u: (-scores[u], u))
+    if binary:
+        U.sort(key=lambda u: (-(1.0 if scores[u] > 0 else 0.0), u))
+    else:
+        U.sort(key=lambda u: (-scores[u], u))
     n_sel = min(budget, len(U))
     sel = np.full(budget, -1, np.int32)
     slot = np.full(E, -1, np.int32)
@@ -312,15 +366,17 @@ def moe_restricted64(x, exec_ids, n_exec, gates, experts, residual=None,
 
 # ------------------------------------------------ canonical fp32 pipeline --
 def decode_layer_c(x, w_router, b_router, pred_a, pred_b, K, budget,
-                   experts=None, norm_topk=1, flags=0, residual=None):
+                   experts=None, norm_topk=1, flags=0, residual=None,
+                   score_rule=SCORE_BASE):
     """The whole hot path at the canonical fp32 level (ids, gates and plan)
     with the expert FFN in fp64 on the same plan."""
     logits, ids, w = carith.route(x, w_router, b_router, K, norm_topk)
-    cost = carith.predict(x, pred_a, pred_b, ids, w)
+    cost = pair_scores_c(score_rule, x, pred_a, pred_b, ids, w)
     E = logits.shape[1]
     scores, counts = carith.aggregate(ids, cost, E)
     budget_c = min(budget, E)
-    sel, n_sel, slot = select(scores, counts, budget_c)
+    sel, n_sel, slot = select(scores, counts, budget_c,
+                              binary=score_rule == SCORE_TOP1)
     ex, n_ex = backfill(logits, ids, slot, n_sel, K, flags)
     g = gates_c(logits, ids, ex, n_ex, norm_topk, flags)
     offsets, pair_tok, pair_gate, pair_of = compact(ex, n_ex, slot, g,

@@ -18,6 +18,7 @@ BASE_F32, BASE_BF16 = 0, 1
 W_ROWMAJOR, W_PACKED = 0, 1
 GATE_PAPER, GATE_RENORM = 0, 1
 FILL_BACKFILL, FILL_DROP = 0, 2
+SCORE_BASE, SCORE_TOP1, SCORE_WEIGHT, SCORE_WEIGHT_SQ, SCORE_STATIC = 0, 1, 2, 3, 4
 
 EXPORTS = ("base_workspace_bytes", "base_route", "base_predict_cost",
            "base_select", "base_moe_forward", "base_decode_layer",
@@ -33,7 +34,7 @@ _i32 = ctypes.c_int32
 class base_layer(ctypes.Structure):
     _fields_ = [("d", _i32), ("E", _i32), ("K", _i32), ("I", _i32),
                 ("dtype", _i32), ("norm_topk", _i32), ("w_layout", _i32),
-                ("w_router", _vp), ("b_router", _vp), ("pred_a", _vp),
+                ("score_rule", _i32), ("w_router", _vp), ("b_router", _vp), ("pred_a", _vp),
                 ("pred_b", _vp), ("w13", _vp), ("w2", _vp)]
 
 
@@ -129,7 +130,7 @@ class Layer:
     fp32 or bf16 (the layer dtype, also the dtype of x and y)."""
 
     def __init__(self, w_router, b_router, pred_a, pred_b, w13, w2,
-                 norm_topk: int = 1, w_layout: int = 0):
+                 norm_topk: int = 1, w_layout: int = 0, score_rule: int = 0):
         import torch
         E, d = w_router.shape
         I = w2.shape[2]
@@ -140,12 +141,14 @@ class Layer:
         self.d, self.E, self.I, self.K = d, E, I, K
         self.norm_topk = norm_topk
         self.w_layout = w_layout
+        self.score_rule = score_rule
         self._desc = None
 
     def desc(self, K: int) -> base_layer:
         w_router, b_router, pred_a, pred_b, w13, w2 = self.tensors
         return base_layer(self.d, self.E, K, self.I, self.dtype,
-                          self.norm_topk, self.w_layout, _ptr(w_router), _ptr(b_router),
+                          self.norm_topk, self.w_layout, self.score_rule,
+                          _ptr(w_router), _ptr(b_router),
                           _ptr(pred_a), _ptr(pred_b), _ptr(w13), _ptr(w2))
 
 
@@ -209,7 +212,7 @@ def packed_layer(layer: "Layer", K: int, stream=None) -> "Layer":
     w13p, w2p = torch.empty_like(w13), torch.empty_like(w2)
     base_pack_experts(layer.desc(K), w13p, w2p, stream)
     return Layer(w_router, b_router, pred_a, pred_b, w13p, w2p,
-                 layer.norm_topk, W_PACKED)
+                 layer.norm_topk, W_PACKED, layer.score_rule)
 
 
 def base_set_stage_events(events):

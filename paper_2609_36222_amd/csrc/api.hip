@@ -12,12 +12,19 @@ namespace {
 
 using namespace basek;
 
+static_assert(SCORE_BASE == BASE_SCORE_BASE && SCORE_TOP1 == BASE_SCORE_TOP1 &&
+                  SCORE_WEIGHT == BASE_SCORE_WEIGHT && SCORE_WEIGHT_SQ == BASE_SCORE_WEIGHT_SQ &&
+                  SCORE_STATIC == BASE_SCORE_STATIC,
+              "selection rule values");
+
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 size_t elem_bytes(int32_t dtype) { return dtype == BASE_BF16 ? 2 : 4; }
 
 base_status check_layer(const base_layer *L, int32_t B, bool need_router,
                         bool need_pred, bool need_experts) {
+  if (L && (L->score_rule < BASE_SCORE_BASE || L->score_rule > BASE_SCORE_STATIC))
+    return BASE_ERR_FLAGS;
   if (!L) return BASE_ERR_NULL;
   if (L->dtype != BASE_F32 && L->dtype != BASE_BF16) return BASE_ERR_DTYPE;
   if (B < 1 || B > MAX_B) return BASE_ERR_SHAPE;
@@ -32,9 +39,14 @@ base_status check_layer(const base_layer *L, int32_t B, bool need_router,
     if (!aligned(L->w_router, 16)) return BASE_ERR_ALIGN;
     if (L->b_router && !aligned(L->b_router, 4)) return BASE_ERR_ALIGN;
   }
-  if (need_pred) {
-    if (!L->pred_a || !L->pred_b) return BASE_ERR_NULL;
-    if (!aligned(L->pred_a, 16) || !aligned(L->pred_b, 4)) return BASE_ERR_ALIGN;
+  // the predictor parameters each selection rule reads
+  if (need_pred && L->score_rule == BASE_SCORE_BASE) {
+    if (!L->pred_a) return BASE_ERR_NULL;
+    if (!aligned(L->pred_a, 16)) return BASE_ERR_ALIGN;
+  }
+  if (need_pred && (L->score_rule == BASE_SCORE_BASE || L->score_rule == BASE_SCORE_STATIC)) {
+    if (!L->pred_b) return BASE_ERR_NULL;
+    if (!aligned(L->pred_b, 4)) return BASE_ERR_ALIGN;
   }
   if (need_experts) {
     if (!L->w13 || !L->w2) return BASE_ERR_NULL;
@@ -238,7 +250,7 @@ base_status base_route(const base_layer *L, const void *x, int32_t B,
   stage_end(st);
   stage(1);
   HIP_TRY(launch_tail(B, L->E, L->K, L->norm_topk, logits, nullptr, nullptr,
-                      nullptr, topk_ids, topk_w, nullptr, 1, st));
+                      nullptr, topk_ids, topk_w, nullptr, 1, BASE_SCORE_BASE, st));
   stage_end(st);
   return BASE_OK;
 }
@@ -251,9 +263,15 @@ base_status base_predict_cost(const base_layer *L, const void *x, int32_t B,
   BASE_TRY(check_ptr(topk_ids, 4));
   BASE_TRY(check_ptr(topk_w, 4));
   BASE_TRY(check_ptr(cost, 4));
-  HIP_TRY(launch_predict(L->dtype == BASE_BF16, x, B, L->d, L->E, L->K,
-                         topk_ids, topk_w, L->pred_a, L->pred_b, cost,
-                         (hipStream_t)stream));
+  if (L->score_rule == BASE_SCORE_BASE)
+    HIP_TRY(launch_predict(L->dtype == BASE_BF16, x, B, L->d, L->E, L->K,
+                           topk_ids, topk_w, L->pred_a, L->pred_b, cost,
+                           (hipStream_t)stream));
+  else   // the other rules' scores need only the routes (and pred_b)
+    HIP_TRY(launch_tail(B, L->E, L->K, L->norm_topk, nullptr, nullptr, nullptr,
+                        L->pred_b, const_cast<int32_t *>(topk_ids),
+                        const_cast<float *>(topk_w), cost, 2, L->score_rule,
+                        (hipStream_t)stream));
   return BASE_OK;
 }
 
@@ -272,8 +290,9 @@ base_status base_select(const base_layer *L, int32_t B, const int32_t *topk_ids,
   BASE_TRY(check_ptr(slot_of_expert, 4));
   const int32_t bc = budget < L->E ? budget : L->E;
   stage(2);
-  HIP_TRY(launch_select(B, L->K, L->E, topk_ids, cost, bc, scores, counts,
-                        sel_ids, n_sel, slot_of_expert, (hipStream_t)stream));
+  HIP_TRY(launch_select(B, L->K, L->E, topk_ids, cost, bc,
+                        L->score_rule == BASE_SCORE_TOP1, scores, counts, sel_ids,
+                        n_sel, slot_of_expert, (hipStream_t)stream));
   stage_end((hipStream_t)stream);
   return BASE_OK;
 }
@@ -331,17 +350,21 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
   int32_t *slot = at<int32_t>(ws, o.slot_of);
   float *q = at<float>(ws, o.q);
   float *ss = at<float>(ws, o.ss);
+  // the predictor's dot products and norms only for the method's own rule
+  const bool pred = L->score_rule == BASE_SCORE_BASE;
   stage(0);
   HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
-                        L->pred_a, L->E, logits, q, ss, st));
+                        pred ? L->pred_a : nullptr, pred ? L->E : 0, logits,
+                        pred ? q : nullptr, pred ? ss : nullptr, st));
   stage_end(st);
   stage(1);
   HIP_TRY(launch_tail(B, L->E, L->K, L->norm_topk, logits, q, ss, L->pred_b,
-                      ids, w, cost, 3, st));
+                      ids, w, cost, 3, L->score_rule, st));
   stage_end(st);
   stage(2);
-  HIP_TRY(launch_select(B, L->K, L->E, ids, cost, bc, at<float>(ws, o.scores),
-                        at<int32_t>(ws, o.counts), sel, nsel, slot, st));
+  HIP_TRY(launch_select(B, L->K, L->E, ids, cost, bc, L->score_rule == BASE_SCORE_TOP1,
+                        at<float>(ws, o.scores), at<int32_t>(ws, o.counts), sel,
+                        nsel, slot, st));
   stage_end(st);
   BASE_TRY(run_forward(L, x, B, logits, ids, sel, nsel, slot, bc, flags,
                        residual, y, ws, o, st));
@@ -384,7 +407,7 @@ const char *base_status_string(int32_t status) {
     case BASE_ERR_ALIGN: return "misaligned pointer";
     case BASE_ERR_WORKSPACE: return "workspace too small";
     case BASE_ERR_HIP: return "HIP launch failed";
-    case BASE_ERR_FLAGS: return "unknown flag bits";
+    case BASE_ERR_FLAGS: return "unknown flag bits or score rule";
     default: return "unknown status";
   }
 }

@@ -61,16 +61,22 @@ hipError_t launch_scores(bool bf16, const void *x, int B, int d, const float *Wr
                          const float *beta, int n_router, const float *A,
                          int n_pred, float *logits, float *q, float *ss,
                          hipStream_t st);
-// mode bit 0: top-K + weights from logits; bit 1: costs from q / ss
+// Selection rules (the values of BASE_SCORE_* in base.h): the per-pair
+// score k_tail writes as the cost
+constexpr int SCORE_BASE = 0, SCORE_TOP1 = 1, SCORE_WEIGHT = 2, SCORE_WEIGHT_SQ = 3,
+              SCORE_STATIC = 4;
+// mode bit 0: top-K + weights from logits; bit 1: per-pair scores of `rule`
+// (SCORE_BASE: from q / ss)
 hipError_t launch_tail(int B, int E, int K, int norm_topk, const float *logits,
                        const float *q, const float *ss, const float *bp,
-                       int32_t *ids, float *w, float *cost, int mode,
+                       int32_t *ids, float *w, float *cost, int mode, int rule,
                        hipStream_t st);
 hipError_t launch_predict(bool bf16, const void *x, int B, int d, int E, int K,
                           const int32_t *ids, const float *w, const float *A,
                           const float *bp, float *cost, hipStream_t st);
+// binary: rank by (score > 0) instead of the score (the top-1-union rule)
 hipError_t launch_select(int B, int K, int E, const int32_t *ids,
-                         const float *cost, int budget, float *scores,
+                         const float *cost, int budget, bool binary, float *scores,
                          int32_t *counts, int32_t *sel_ids, int32_t *n_sel,
                          int32_t *slot_of, hipStream_t st);
 hipError_t launch_backfill(int B, int E, int K, int norm_topk, int flags,

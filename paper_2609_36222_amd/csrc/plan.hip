@@ -6,7 +6,8 @@
 //            ascending order; then the kept set: the min(budget, |union|)
 //            experts of the batch union first in the order (D_hat desc,
 //            index asc) (Sec. 3.4; App. "Custom GPU Kernels": one kernel
-//            selects the highest-scoring experts for the whole batch).
+//            selects the highest-scoring experts for the whole batch); for
+//            the top-1-union rule the order (D_hat > 0 desc, index asc).
 // k_backfill one wavefront per token: the experts it executes -- its K
 //            highest-ranked experts inside the kept set, or only its kept
 //            routes under the drop rule -- and their gates (Sec. 3.5).
@@ -29,7 +30,7 @@ constexpr int SEL_V = 2 * 128 * SEL_PAD;          // chunk-matrix capacity (floa
 // asc).
 __global__ __launch_bounds__(SEL_THREADS)
 void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
-              const float *__restrict__ cost, int budget,
+              const float *__restrict__ cost, int budget, int binary,
               float *__restrict__ scores, int32_t *__restrict__ counts,
               int32_t *__restrict__ sel_ids, int32_t *__restrict__ n_sel_out,
               int32_t *__restrict__ slot_of) {
@@ -96,7 +97,10 @@ void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
 
   for (int u = tid; u < ((E + WAVE - 1) & ~(WAVE - 1)); u += SEL_THREADS) {
     const bool in = u < E && cnt[u] > 0;
-    if (u < E) key[u] = in ? rank_key(D[u], u) : 0;   // 0: ranks after every expert
+    if (u < E) {
+      const float kv = binary ? (D[u] > 0.0f ? 1.0f : 0.0f) : D[u];
+      key[u] = in ? rank_key(kv, u) : 0;   // 0: ranks after every expert
+    }
     const uint64_t m = __ballot(in);
     if (lane == 0 && m) atomicAdd(&n_union, (int)__popcll(m));
   }
@@ -366,11 +370,11 @@ void k_compact(int B, int K, int E, int budget, const int32_t *__restrict__ exec
 }
 
 hipError_t launch_select(int B, int K, int E, const int32_t *ids,
-                         const float *cost, int budget, float *scores,
+                         const float *cost, int budget, bool binary, float *scores,
                          int32_t *counts, int32_t *sel_ids, int32_t *n_sel,
                          int32_t *slot_of, hipStream_t st) {
   launch_k(k_select, dim3(1), dim3(SEL_THREADS), 0, st, B, K, E, ids,
-                     cost, budget, scores, counts, sel_ids, n_sel, slot_of);
+                     cost, budget, (int)binary, scores, counts, sel_ids, n_sel, slot_of);
   return hipGetLastError();
 }
 

@@ -9,7 +9,8 @@
 //           ||x_t||^2.
 // k_tail    one wavefront per token: top-K by exact ranks, router weights,
 //           then the cost of each routed pair, cost = w^2 exp(q[t][u] /
-//           ||x_t|| + b_u), one lane per pair.
+//           ||x_t|| + b_u), one lane per pair (or another selection rule's
+//           per-pair score: App. selection-rule ablation).
 //
 // Fixed fp32 order of every dot product of length d: partial j (0..63) owns
 // the elements 256m + 4j + r (r = 0..3) and accumulates them in ascending
@@ -236,13 +237,16 @@ constexpr int TL_WAVES = 4;    // tokens (wavefronts) per workgroup
 
 
 // mode bit 0: route (top-K and weights from the logits into ids / w)
-// mode bit 1: costs from q, ss and the routed pairs (ids / w, read back when
-//             bit 0 is off)
+// mode bit 1: per-pair scores of the routed pairs (ids / w, read back when
+//             bit 0 is off) under `rule`: SCORE_BASE w^2 exp(q / ||x|| + b_u)
+//             from q and ss; SCORE_TOP1 1 for the first route, else 0;
+//             SCORE_WEIGHT w; SCORE_WEIGHT_SQ w * w; SCORE_STATIC
+//             (w * w) * exp(b_u)
 __global__ __launch_bounds__(TL_WAVES * WAVE)
 void k_tail(int B, int E, int K, int norm_topk, const float *__restrict__ logits,
             const float *__restrict__ q, const float *__restrict__ ss,
             const float *__restrict__ bp, int32_t *__restrict__ ids_io,
-            float *__restrict__ w_io, float *__restrict__ cost, int mode) {
+            float *__restrict__ w_io, float *__restrict__ cost, int mode, int rule) {
   __shared__ __attribute__((aligned(16))) uint64_t keys[TL_WAVES][MAX_E];
   __shared__ float lrow[TL_WAVES][MAX_E];
   __shared__ int top[TL_WAVES][MAX_K];
@@ -315,16 +319,29 @@ void k_tail(int B, int E, int K, int norm_topk, const float *__restrict__ logits
 
   if ((mode & 2) && live && lane < K) {
     const int u = (my_id >= 0 && my_id < E) ? my_id : 0;   // out-of-range ids read row 0
-    const float s2 = ss[t];
-    float inv = 0.0f;
-    if (s2 > 0.0f) {
-      const float rt = sqrtf(s2);
-      inv = 1.0f / rt;
+    float c;
+    if (rule == SCORE_BASE) {
+      const float s2 = ss[t];
+      float inv = 0.0f;
+      if (s2 > 0.0f) {
+        const float rt = sqrtf(s2);
+        inv = 1.0f / rt;
+      }
+      float s = q[(size_t)t * E + u] * inv;
+      s = s + bp[u];
+      const float w2 = my_w * my_w;
+      c = w2 * base_exp(s);
+    } else if (rule == SCORE_TOP1) {
+      c = lane == 0 ? 1.0f : 0.0f;
+    } else if (rule == SCORE_WEIGHT) {
+      c = my_w;
+    } else if (rule == SCORE_WEIGHT_SQ) {
+      c = my_w * my_w;
+    } else {   // SCORE_STATIC
+      const float w2 = my_w * my_w;
+      c = w2 * base_exp(bp[u]);
     }
-    float s = q[(size_t)t * E + u] * inv;
-    s = s + bp[u];
-    const float w2 = my_w * my_w;
-    cost[(size_t)t * K + lane] = w2 * base_exp(s);
+    cost[(size_t)t * K + lane] = c;
   }
 }
 
@@ -354,11 +371,11 @@ hipError_t launch_scores(bool bf16, const void *x, int B, int d, const float *Wr
 
 hipError_t launch_tail(int B, int E, int K, int norm_topk, const float *logits,
                        const float *q, const float *ss, const float *bp,
-                       int32_t *ids, float *w, float *cost, int mode,
+                       int32_t *ids, float *w, float *cost, int mode, int rule,
                        hipStream_t st) {
   launch_k(k_tail, dim3((B + TL_WAVES - 1) / TL_WAVES),
                      dim3(TL_WAVES * WAVE), 0, st, B, E, K, norm_topk, logits,
-                     q, ss, bp, ids, w, cost, mode);
+                     q, ss, bp, ids, w, cost, mode, rule);
   return hipGetLastError();
 }
 

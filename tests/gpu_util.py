@@ -33,7 +33,7 @@ def to_np_f32(t):
 
 class GpuLayer:
     def __init__(self, inp, pred_a=None, pred_b=None, norm_topk=1,
-                 packed=False):
+                 packed=False, score_rule=0):
         sh = inp["shape"]
         self.shape = sh
         self.bf16 = sh.bf16
@@ -47,7 +47,7 @@ class GpuLayer:
         else:
             self.w13, self.w2 = dev_f32(inp["w13"]), dev_f32(inp["w2"])
         self.layer = bd.Layer(self.wr, self.br, self.pa, self.pb, self.w13,
-                              self.w2, norm_topk)
+                              self.w2, norm_topk, score_rule=score_rule)
         if packed:
             self.layer = bd.packed_layer(self.layer, sh.K)
         self.desc = self.layer.desc(sh.K)

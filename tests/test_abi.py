@@ -48,11 +48,11 @@ def test_exported_symbols_in_dynamic_table(lib):
 
 def layer(**kw):
     v = dict(d=2048, E=128, K=8, I=768, dtype=1, norm_topk=1, w_layout=0,
-             w_router=FAKE, b_router=FAKE, pred_a=FAKE, pred_b=FAKE, w13=FAKE,
-             w2=FAKE)
+             score_rule=0, w_router=FAKE, b_router=FAKE, pred_a=FAKE, pred_b=FAKE,
+             w13=FAKE, w2=FAKE)
     v.update(kw)
     return bd.base_layer(v["d"], v["E"], v["K"], v["I"], v["dtype"],
-                         v["norm_topk"], v["w_layout"], v["w_router"],
+                         v["norm_topk"], v["w_layout"], v["score_rule"], v["w_router"],
                          v["b_router"], v["pred_a"], v["pred_b"], v["w13"],
                          v["w2"])
 
@@ -82,7 +82,8 @@ def test_status_strings(lib):
     (dict(dtype=7), DTYPE), (dict(norm_topk=2), SHAPE),
     (dict(w_layout=2), SHAPE), (dict(w_layout=1, dtype=0), DTYPE),
     (dict(w_router=0), NULL), (dict(w_router=FAKE + 4), ALIGN),
-    (dict(b_router=FAKE + 2), ALIGN)])
+    (dict(b_router=FAKE + 2), ALIGN), (dict(score_rule=5), FLAGS),
+    (dict(score_rule=-1), FLAGS)])
 def test_route_layer_validation(lib, kw, expect):
     assert route(lib, layer(**kw)) == expect
 
@@ -150,6 +151,20 @@ def test_decode_layer_validation(lib):
     assert decode(lib, L, nbytes=100) == WS
     assert decode(lib, layer(pred_b=0)) == NULL
     assert decode(lib, layer(w2=0)) == NULL
+
+
+def test_score_rules_read_only_their_parameters(lib):
+    """BASE needs pred_a and pred_b, STATIC pred_b only, the router-only
+    rules neither (their calls pass validation up to the workspace check)."""
+    for rule in (bd.SCORE_TOP1, bd.SCORE_WEIGHT, bd.SCORE_WEIGHT_SQ):
+        assert decode(lib, layer(score_rule=rule, pred_a=0, pred_b=0), nbytes=100) == WS
+    assert decode(lib, layer(score_rule=bd.SCORE_STATIC, pred_a=0), nbytes=100) == WS
+    assert decode(lib, layer(score_rule=bd.SCORE_STATIC, pred_b=0)) == NULL
+    assert decode(lib, layer(score_rule=bd.SCORE_BASE, pred_a=0)) == NULL
+    L = layer(score_rule=bd.SCORE_STATIC, pred_a=0)
+    assert lib.base_predict_cost(ctypes.byref(L), FAKE, 4, FAKE, FAKE, 0, None) == NULL
+    assert lib.base_predict_cost(ctypes.byref(layer(score_rule=9)), FAKE, 4, FAKE, FAKE,
+                                 FAKE, None) == FLAGS
 
 
 def test_workspace_grows_with_shape_and_clamps_budget(lib):

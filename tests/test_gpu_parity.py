@@ -51,15 +51,15 @@ def named(name, data_seed=0, with_experts=True):
 
 
 def oracle_layer(inp, budget, flags=0, norm_topk=1, residual=None,
-                 with_y=True):
+                 with_y=True, score_rule=0):
     sh = inp["shape"]
     ex = method.Experts(inp["w13"], inp["w2"], sh.bf16) if with_y else None
     return method.decode_layer_c(inp["x"], inp["w_router"], inp["b_router"],
                                  inp["pred_a"], inp["pred_b"], sh.K, budget,
-                                 ex, norm_topk, flags, residual)
+                                 ex, norm_topk, flags, residual, score_rule)
 
 
-def check_scoring(gl, inp, ref, B, budget):
+def check_scoring(gl, inp, ref, B, budget, score_rule=0):
     """Staged route / predict / select against the oracle, bit for bit."""
     x = gl.x(inp["x"])
     logits, ids, w = gl.route(x, B)
@@ -69,9 +69,9 @@ def check_scoring(gl, inp, ref, B, budget):
     cost = gl.predict(x, B, ids, w)
     c = cost.cpu().numpy()
     assert np.array_equal(c, ref["cost"])
-    c64 = method.predict64(inp["x"], inp["pred_a"], inp["pred_b"],
-                           ref["topk_ids"], ref["topk_w"].astype(np.float64))
-    assert np.max(np.abs(c - c64) / c64) < 1e-4
+    c64 = method.pair_scores64(score_rule, inp["x"], inp["pred_a"], inp["pred_b"],
+                               ref["topk_ids"], ref["topk_w"].astype(np.float64))
+    assert np.max(np.abs(c - c64) / np.where(c64 > 0, c64, 1.0)) < 1e-4
     scores, counts, sel, nsel, slot = gl.select(B, ids, cost, budget)
     assert np.array_equal(scores.cpu().numpy(), ref["scores"])
     assert np.array_equal(counts.cpu().numpy(), ref["counts"])
@@ -91,21 +91,21 @@ def check_plan(got, ref):
 
 
 def run_case(gu, inp, budget, flags=0, norm_topk=1, with_residual=False,
-             check_y=True):
+             check_y=True, score_rule=0):
     sh = inp["shape"]
     B = inp["x"].shape[0]
     _flush(f"case {sh.name} B={B} budget={budget} flags={flags} "
-           f"norm_topk={norm_topk} residual={with_residual}")
+           f"norm_topk={norm_topk} residual={with_residual} rule={score_rule}")
     residual = None
     if with_residual:
         g = np.random.default_rng(7)
         residual = g.standard_normal((B, sh.d)).astype(np.float32)
         if sh.bf16:
             residual = W.bf16_bits_to_f32(W.f32_to_bf16_bits(residual))
-    ref = oracle_layer(inp, budget, flags, norm_topk, residual, check_y)
-    gl = gu.GpuLayer(inp, norm_topk=norm_topk)
+    ref = oracle_layer(inp, budget, flags, norm_topk, residual, check_y, score_rule)
+    gl = gu.GpuLayer(inp, norm_topk=norm_topk, score_rule=score_rule)
     x, logits, ids, w, cost, sel, nsel, slot = check_scoring(gl, inp, ref, B,
-                                                              budget)
+                                                              budget, score_rule)
     res_d = None if residual is None else gl.x(residual)
     # staged forward
     ws = gl.workspace(B, budget)
@@ -134,7 +134,7 @@ def run_case(gu, inp, budget, flags=0, norm_topk=1, with_residual=False,
     assert np.array_equal(gu.to_np_f32(y2), y_staged)
     if sh.bf16:
         # packed expert layout: same values, same arithmetic, same bits
-        glp = gu.GpuLayer(inp, norm_topk=norm_topk, packed=True)
+        glp = gu.GpuLayer(inp, norm_topk=norm_topk, packed=True, score_rule=score_rule)
         ws3 = glp.workspace(B, budget)
         y3 = glp.y_like(B)
         bd.base_decode_layer(glp.desc, x, B, budget, flags, res_d, y3, ws3)
@@ -168,6 +168,20 @@ def test_qwen3_b256_full_size(gu, qwen3_b256, budget):
     ref, _ = run_case(gu, qwen3_b256, budget)
     if budget == 128:   # covers the whole union: dense top-K
         assert np.array_equal(ref["exec_ids"], ref["topk_ids"])
+
+
+@pytest.mark.parametrize("rule", [1, 2, 3, 4], ids=["top1", "weight", "weight_sq", "static"])
+@pytest.mark.parametrize("name,budget", [("tiny", 3), ("olmoe", 16), ("qwen3_b64", 16)])
+def test_selection_rules(gu, name, budget, rule):
+    """The selection-rule variants (App. selection-rule ablation): per-pair
+    scores, ranking, kept set and everything after it bit for bit with the
+    oracle, fused == staged, packed == row-major."""
+    run_case(gu, named(name), budget, score_rule=rule)
+
+
+@pytest.mark.parametrize("rule", [1, 4], ids=["top1", "static"])
+def test_selection_rules_full_size(gu, qwen3_b256, rule):
+    run_case(gu, qwen3_b256, 32, score_rule=rule)
 
 
 def test_qwen3_b256_flags(gu, qwen3_b256):

@@ -253,6 +253,34 @@ def layer_inputs(name: str, layer: int = 0, data_seed: int = 0,
     return out
 
 
+def rules_layer(seed=0, d=256, E=32, K=4, I=128, B=16, n_calib=4096):
+    """A small fp32 layer for comparing selection rules, whose experts
+    differ in output energy in two ways the rules can see or miss: a
+    per-expert output scale (log-normal, sigma 0.5) and a preferred input
+    direction (the gate rows of expert u lean along a unit vector v_u, so
+    its energy grows with z . v_u).  Returns the router, the row-major fp32
+    experts, calibration tokens and decode batches (RMS-normalised N(0, I)
+    rows); the seeds are this function's own."""
+    g = np.random.default_rng(np.random.SeedSequence([SEED_ROOT, 77, seed]))
+    wr = (g.standard_normal((E, d)) * 0.08).astype(np.float32)
+    br = (g.standard_normal(E) * 0.3).astype(np.float32)
+    w13 = (g.standard_normal((E, 2 * I, d)) / np.sqrt(d)).astype(np.float32)
+    scale = np.exp(g.standard_normal(E) * 0.5)
+    w2 = (g.standard_normal((E, d, I)) / np.sqrt(I) * scale[:, None, None]).astype(np.float32)
+    v = g.standard_normal((E, d))
+    v /= np.linalg.norm(v, axis=1, keepdims=True)
+    w13[:, :I, :] += (8.0 * v[:, None, :] * g.standard_normal((E, I, 1)) / np.sqrt(d)).astype(np.float32)
+
+    def rows(n):
+        z = g.standard_normal((n, d))
+        return _rmsnorm_rows(z)
+
+    calib = rows(n_calib)
+    batches = [rows(B) for _ in range(24)]
+    return dict(w_router=wr, b_router=br, w13=w13, w2=w2, calib=calib,
+                batches=batches, K=K)
+
+
 def custom_layer(d, E, K, I, B, bf16=True, seed=0, router_std=0.075,
                  zipf_bias=True, rmsnorm=True, identical_tokens=False,
                  zero_token=False):
