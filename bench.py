@@ -617,6 +617,30 @@ def main():
             route_us[i, s] = elapsed_ms(hip, stage_ev[i][2 * s], stage_ev[i][2 * s + 1]) * 1e3
     route_scores_us, route_tail_us = (float(v) for v in route_us.mean(axis=0))
 
+    # the fused layer makes the selection and the backfill in one kernel;
+    # aggregation + selection alone is timed through base_select (its own
+    # kernel) on the same routes and costs
+    bc = min(budget, shape.E)
+    sc_s = torch.empty(shape.E, dtype=torch.float32, device=dev)
+    cn_s = torch.empty(shape.E, dtype=torch.int32, device=dev)
+    sel_s = torch.empty(bc, dtype=torch.int32, device=dev)
+    ns_s = torch.empty(1, dtype=torch.int32, device=dev)
+    sl_s = torch.empty(shape.E, dtype=torch.int32, device=dev)
+    select_us = np.zeros(args.steps)
+    for i in range(args.steps):
+        _, desc = layers[i % len(layers)]
+        lib.base_set_stage_events(ev_keep[i], n_ev)
+        st = lib.base_select(ctypes.byref(desc), B, plan.topk_ids, plan.cost, budget,
+                             sc_s.data_ptr(), cn_s.data_ptr(), sel_s.data_ptr(),
+                             ns_s.data_ptr(), sl_s.data_ptr(), sptr)
+        if st != 0:
+            raise RuntimeError(bd.status_string(st))
+    lib.base_set_stage_events(None, 0)
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        select_us[i] = elapsed_ms(hip, stage_ev[i][4], stage_ev[i][5]) * 1e3
+    select_only_us = float(select_us.mean())
+
     # plan of the last step (for the algorithmic byte count)
     def read_i32(ptr, n):
         off = ptr - ws.data_ptr()
@@ -634,7 +658,7 @@ def main():
     # the score and tail kernels beyond plain routing) and aggregation +
     # selection
     predict_us = (stage_mean["scores"] - route_scores_us) + (stage_mean["tail"] - route_tail_us)
-    pas_us = predict_us + stage_mean["select"]
+    pas_us = predict_us + select_only_us
     pre_ffn_us = sum(stage_mean[k] for k in ("scores", "tail", "select", "backfill",
                                              "compact", "gather"))
     ceiling = None
@@ -714,7 +738,8 @@ def main():
         "stages_us": stage_mean,
         "overhead": {
             "predict_us": round(predict_us, 2),
-            "aggregate_select_us": stage_mean["select"],
+            "aggregate_select_us": round(select_only_us, 2),
+            "select_stage_includes_backfill": True,
             "predict_aggregate_select_us": round(pas_us, 2),
             "predict_aggregate_select_frac": round(pas_us / us_step, 4),
             "plain_routing_us": round(route_scores_us + route_tail_us, 2),

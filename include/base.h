@@ -271,9 +271,11 @@ base_status base_pack_experts(const base_layer *L, void *w13_packed,
  * kernel each: 0 scores (router logits, predictor dot products, norms),
  * 1 tail (top-K, router weights, predicted costs), 2 aggregation +
  * selection, 3 backfill + gates, 4 compaction, 5 token gather, 6 FFN
- * gate/up, 7 FFN down, 8 combine.  base_decode_layer runs all of them;
- * base_route stages 0 and 1, base_select stage 2, base_moe_forward 3 to 8
- * (base_predict_cost runs its own kernel, untimed).  The setting belongs
+ * gate/up, 7 FFN down, 8 combine.  base_route runs stages 0 and 1,
+ * base_select stage 2, base_moe_forward 3 to 8 (base_predict_cost runs its
+ * own kernel, untimed); base_decode_layer runs all of them except that one
+ * kernel makes the selection and the backfill: stage 2 times it and stage 3
+ * records its pair back to back.  The setting belongs
  * to the calling host thread; the caller keeps the events alive while it
  * is set, and does not set it around calls on a capturing stream.
  * Returns BASE_ERR_SHAPE if n_events != 2 * BASE_N_STAGES. */

@@ -146,13 +146,14 @@ T *at(void *ws, size_t off) {
   return reinterpret_cast<T *>(static_cast<char *>(ws) + off);
 }
 
-// backfill + compaction + FFN + combine, on plan arrays already in place
+// backfill (unless done with the selection) + compaction + FFN + combine,
+// on plan arrays already in place
 base_status run_forward(const base_layer *L, const void *x, int32_t B,
                         const float *logits, const int32_t *ids,
                         const int32_t *sel_ids, const int32_t *n_sel,
                         const int32_t *slot_of, int32_t bc, int32_t flags,
                         const void *residual, void *y, void *ws,
-                        const Layout &o, hipStream_t st) {
+                        const Layout &o, hipStream_t st, bool backfilled = false) {
   const bool bf16 = L->dtype == BASE_BF16;
   int32_t *exec_ids = at<int32_t>(ws, o.exec_ids);
   float *exec_gates = at<float>(ws, o.exec_gates);
@@ -161,8 +162,9 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
   float *pair_gate = at<float>(ws, o.pair_gate);
   int32_t *pair_of = at<int32_t>(ws, o.pair_of);
   stage(3);
-  HIP_TRY(launch_backfill(B, L->E, L->K, L->norm_topk, flags, logits, ids,
-                          slot_of, n_sel, exec_ids, exec_gates, st));
+  if (!backfilled)
+    HIP_TRY(launch_backfill(B, L->E, L->K, L->norm_topk, flags, logits, ids,
+                            slot_of, n_sel, exec_ids, exec_gates, st));
   stage_end(st);
   stage(4);
   PartRec *parts = at<PartRec>(ws, o.parts);
@@ -361,13 +363,15 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
   HIP_TRY(launch_tail(B, L->E, L->K, L->norm_topk, logits, q, ss, L->pred_b,
                       ids, w, cost, 3, L->score_rule, st));
   stage_end(st);
-  stage(2);
-  HIP_TRY(launch_select(B, L->K, L->E, ids, cost, bc, L->score_rule == BASE_SCORE_TOP1,
-                        at<float>(ws, o.scores), at<int32_t>(ws, o.counts), sel,
-                        nsel, slot, st));
+  stage(2);   // selection and backfill in one launch
+  HIP_TRY(launch_select_backfill(B, L->K, L->E, ids, cost, bc,
+                                 L->score_rule == BASE_SCORE_TOP1, L->norm_topk, flags,
+                                 logits, at<float>(ws, o.scores), at<int32_t>(ws, o.counts),
+                                 sel, nsel, slot, at<int32_t>(ws, o.exec_ids),
+                                 at<float>(ws, o.exec_gates), st));
   stage_end(st);
   BASE_TRY(run_forward(L, x, B, logits, ids, sel, nsel, slot, bc, flags,
-                       residual, y, ws, o, st));
+                       residual, y, ws, o, st, true));
   fill_plan(plan_out, ws, o, true);
   return BASE_OK;
 }

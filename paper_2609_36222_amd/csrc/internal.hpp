@@ -79,6 +79,12 @@ hipError_t launch_select(int B, int K, int E, const int32_t *ids,
                          const float *cost, int budget, bool binary, float *scores,
                          int32_t *counts, int32_t *sel_ids, int32_t *n_sel,
                          int32_t *slot_of, hipStream_t st);
+// selection and backfill in one launch (same results as the two launches)
+hipError_t launch_select_backfill(int B, int K, int E, const int32_t *ids, const float *cost,
+                                  int budget, bool binary, int norm_topk, int flags,
+                                  const float *logits, float *scores, int32_t *counts,
+                                  int32_t *sel_ids, int32_t *n_sel, int32_t *slot_of,
+                                  int32_t *exec_ids, float *exec_gates, hipStream_t st);
 hipError_t launch_backfill(int B, int E, int K, int norm_topk, int flags,
                            const float *logits, const int32_t *ids,
                            const int32_t *slot_of, const int32_t *n_sel,

@@ -13,6 +13,8 @@
 //            routes under the drop rule -- and their gates (Sec. 3.5).
 // k_compact  one workgroup: counting sort of the executed (token, rank)
 //            pairs by (kept slot, token), the token lists of the grouped FFN.
+// k_select_backfill  the first two in one launch (the fused layer): every
+//            workgroup repeats the selection and backfills its own tokens.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -22,30 +24,125 @@ constexpr int SEL_THREADS = 1024;
 constexpr int SEL_PAD = WAVE + 1;                 // LDS row of one chunk tree
 constexpr int SEL_V = 2 * 128 * SEL_PAD;          // chunk-matrix capacity (floats)
 
-// One workgroup.  Chunk c (tokens 64c .. 64c + 63) of expert u is the row
-// V[c][u][0..63] (position j: the cost of token 64c + j if it routes u, else
-// +0); one thread per (chunk, expert) adds its row by the halving tree, and
-// the chunk sums are added to D_hat_u in ascending chunk order.  The kept
-// set is ranked with 64-bit keys whose unsigned order is (D_hat desc, index
-// asc).
-__global__ __launch_bounds__(SEL_THREADS)
-void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
-              const float *__restrict__ cost, int budget, int binary,
-              float *__restrict__ scores, int32_t *__restrict__ counts,
-              int32_t *__restrict__ sel_ids, int32_t *__restrict__ n_sel_out,
-              int32_t *__restrict__ slot_of) {
-  __shared__ __attribute__((aligned(16))) float V[SEL_V];
-  __shared__ float CS[SEL_THREADS];
-  __shared__ float D[MAX_E];
-  __shared__ int cnt[MAX_E];
-  __shared__ uint64_t key[MAX_E];
-  __shared__ int rnk[MAX_E];
-  __shared__ int n_union;
-  const int tid = threadIdx.x, lane = lane_id();
+// LDS of the selection (one workgroup of SEL_THREADS threads)
+struct SelLds {
+  float V[SEL_V];
+  float CS[SEL_THREADS];
+  float D[MAX_E];
+  int cnt[MAX_E];
+  uint64_t key[MAX_E];
+  int rnk[MAX_E];
+  int n_union;
+};
 
-  // thread t holds the routes of token t (B <= SEL_THREADS), loaded once
-  int uk[MAX_K];
-  float ck[MAX_K];
+// Aggregation and selection by one workgroup of SEL_THREADS threads; thread
+// t < B brings token t's routes (uk) and costs (ck).  Chunk c (tokens 64c ..
+// 64c + 63) of expert u is the row V[c][u][0..63] (position j: the cost of
+// token 64c + j if it routes u, else +0); one thread per (chunk, expert)
+// adds its row by the halving tree, and the chunk sums are added to D_hat_u
+// in ascending chunk order.  The kept set is ranked with 64-bit keys whose
+// unsigned order is (D_hat desc, index asc) -- (D_hat > 0 desc, index asc)
+// with `binary`.  Writes scores, counts, sel_ids, n_sel and slot_of when
+// `out` is set, and slot_of into slot_lds when that is given; returns n_sel
+// (every thread).
+__device__ __forceinline__ int select_body(SelLds &S, int B, int K, int E, int budget,
+                                           int binary, const int (&uk)[MAX_K],
+                                           const float (&ck)[MAX_K], bool out,
+                                           float *__restrict__ scores,
+                                           int32_t *__restrict__ counts,
+                                           int32_t *__restrict__ sel_ids,
+                                           int32_t *__restrict__ n_sel_out,
+                                           int32_t *__restrict__ slot_of, int *slot_lds) {
+  const int tid = threadIdx.x, lane = lane_id();
+  for (int u = tid; u < E; u += SEL_THREADS) { S.cnt[u] = 0; S.D[u] = 0.0f; }
+  if (tid == 0) S.n_union = 0;
+  const int nchunks = (B + WAVE - 1) / WAVE;
+  // chunks per batch: bounded by V and by one thread per (chunk, expert)
+  const int cb = max(1, min(min(nchunks, SEL_V / (E * SEL_PAD)), SEL_THREADS / E));
+  for (int c0 = 0; c0 < nchunks; c0 += cb) {
+    const int nb = min(cb, nchunks - c0);
+    const int nv = min(SEL_V, (nb * E * SEL_PAD + 3) & ~3) / 4;
+    for (int i = tid; i < nv; i += SEL_THREADS)
+      reinterpret_cast<float4 *>(S.V)[i] = float4{0.0f, 0.0f, 0.0f, 0.0f};
+    __syncthreads();
+    // the routes in rank order (a repeated expert keeps its last cost, and
+    // counts every time)
+    const int cl = tid / WAVE - c0;
+    if (tid < B && cl >= 0 && cl < nb) {
+#pragma unroll
+      for (int k = 0; k < MAX_K; ++k)
+        if (k < K && uk[k] >= 0 && uk[k] < E) {
+          S.V[(cl * E + uk[k]) * SEL_PAD + lane] = ck[k];
+          atomicAdd(&S.cnt[uk[k]], 1);
+        }
+    }
+    __syncthreads();
+    if (tid < nb * E) {
+      float v[WAVE];
+#pragma unroll
+      for (int q = 0; q < WAVE; ++q) v[q] = S.V[tid * SEL_PAD + q];
+#pragma unroll
+      for (int h = WAVE / 2; h >= 1; h >>= 1)
+#pragma unroll
+        for (int q = 0; q < h; ++q) v[q] = v[q] + v[q + h];
+      S.CS[tid] = v[0];
+    }
+    __syncthreads();
+    for (int u = tid; u < E; u += SEL_THREADS)
+      for (int c = 0; c < nb; ++c)
+        S.D[u] = (c0 + c == 0) ? S.CS[c * E + u] : S.D[u] + S.CS[c * E + u];
+    __syncthreads();
+  }
+
+  for (int u = tid; u < ((E + WAVE - 1) & ~(WAVE - 1)); u += SEL_THREADS) {
+    const bool in = u < E && S.cnt[u] > 0;
+    if (u < E) {
+      const float kv = binary ? (S.D[u] > 0.0f ? 1.0f : 0.0f) : S.D[u];
+      S.key[u] = in ? rank_key(kv, u) : 0;   // 0: ranks after every expert
+    }
+    const uint64_t m = __ballot(in);
+    if (lane == 0 && m) atomicAdd(&S.n_union, (int)__popcll(m));
+  }
+  __syncthreads();
+  const int n_sel = min(budget, S.n_union);
+  {
+    // tpe consecutive threads per expert, each over a share of the keys
+    const int tpe = E <= 64 ? 16 : E <= 128 ? 8 : 4;
+    const int u = tid / tpe, part = tid % tpe;
+    int r = 0;
+    if (u < E && S.cnt[u] > 0) {
+      const uint64_t ku = S.key[u];
+      for (int v = part; v < E; v += tpe) r += S.key[v] > ku;
+    }
+    for (int h = 1; h < tpe; h <<= 1) r += __shfl_xor(r, h, WAVE);
+    if (u < E && part == 0) S.rnk[u] = r;
+  }
+  __syncthreads();
+  for (int u = tid; u < E; u += SEL_THREADS) {
+    int slot = -1;
+    if (S.cnt[u] > 0 && S.rnk[u] < n_sel) {
+      slot = S.rnk[u];
+      if (out) sel_ids[slot] = u;
+    }
+    if (slot_lds) slot_lds[u] = slot;
+    if (out) {
+      slot_of[u] = slot;
+      scores[u] = S.D[u];
+      counts[u] = S.cnt[u];
+    }
+  }
+  if (out) {
+    for (int r = n_sel + tid; r < budget; r += SEL_THREADS) sel_ids[r] = -1;
+    if (tid == 0) *n_sel_out = n_sel;
+  }
+  return n_sel;
+}
+
+// Thread t < B: token t's routes and costs.
+__device__ __forceinline__ void load_routes(int B, int K, const int32_t *__restrict__ ids,
+                                            const float *__restrict__ cost, int (&uk)[MAX_K],
+                                            float (&ck)[MAX_K]) {
+  const int tid = threadIdx.x;
 #pragma unroll
   for (int k = 0; k < MAX_K; ++k) {
     uk[k] = -1;
@@ -55,125 +152,73 @@ void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
       ck[k] = cost[(size_t)tid * K + k];
     }
   }
-  for (int u = tid; u < E; u += SEL_THREADS) { cnt[u] = 0; D[u] = 0.0f; }
-  if (tid == 0) n_union = 0;
-  const int nchunks = (B + WAVE - 1) / WAVE;
-  // chunks per batch: bounded by V and by one thread per (chunk, expert)
-  const int cb = max(1, min(min(nchunks, SEL_V / (E * SEL_PAD)), SEL_THREADS / E));
-  for (int c0 = 0; c0 < nchunks; c0 += cb) {
-    const int nb = min(cb, nchunks - c0);
-    const int nv = min(SEL_V, (nb * E * SEL_PAD + 3) & ~3) / 4;
-    for (int i = tid; i < nv; i += SEL_THREADS)
-      reinterpret_cast<float4 *>(V)[i] = float4{0.0f, 0.0f, 0.0f, 0.0f};
-    __syncthreads();
-    // the routes in rank order (a repeated expert keeps its last cost, and
-    // counts every time)
-    const int cl = tid / WAVE - c0;
-    if (tid < B && cl >= 0 && cl < nb) {
-#pragma unroll
-      for (int k = 0; k < MAX_K; ++k)
-        if (k < K && uk[k] >= 0 && uk[k] < E) {
-          V[(cl * E + uk[k]) * SEL_PAD + lane] = ck[k];
-          atomicAdd(&cnt[uk[k]], 1);
-        }
-    }
-    __syncthreads();
-    if (tid < nb * E) {
-      float v[WAVE];
-#pragma unroll
-      for (int q = 0; q < WAVE; ++q) v[q] = V[tid * SEL_PAD + q];
-#pragma unroll
-      for (int h = WAVE / 2; h >= 1; h >>= 1)
-#pragma unroll
-        for (int q = 0; q < h; ++q) v[q] = v[q] + v[q + h];
-      CS[tid] = v[0];
-    }
-    __syncthreads();
-    for (int u = tid; u < E; u += SEL_THREADS)
-      for (int c = 0; c < nb; ++c)
-        D[u] = (c0 + c == 0) ? CS[c * E + u] : D[u] + CS[c * E + u];
-    __syncthreads();
-  }
+}
 
-  for (int u = tid; u < ((E + WAVE - 1) & ~(WAVE - 1)); u += SEL_THREADS) {
-    const bool in = u < E && cnt[u] > 0;
-    if (u < E) {
-      const float kv = binary ? (D[u] > 0.0f ? 1.0f : 0.0f) : D[u];
-      key[u] = in ? rank_key(kv, u) : 0;   // 0: ranks after every expert
-    }
-    const uint64_t m = __ballot(in);
-    if (lane == 0 && m) atomicAdd(&n_union, (int)__popcll(m));
-  }
-  __syncthreads();
-  const int n_sel = min(budget, n_union);
-  {
-    // tpe consecutive threads per expert, each over a share of the keys
-    const int tpe = E <= 64 ? 16 : E <= 128 ? 8 : 4;
-    const int u = tid / tpe, part = tid % tpe;
-    int r = 0;
-    if (u < E && cnt[u] > 0) {
-      const uint64_t ku = key[u];
-      for (int v = part; v < E; v += tpe) r += key[v] > ku;
-    }
-    for (int h = 1; h < tpe; h <<= 1) r += __shfl_xor(r, h, WAVE);
-    if (u < E && part == 0) rnk[u] = r;
-  }
-  __syncthreads();
-  for (int u = tid; u < E; u += SEL_THREADS) {
-    int slot = -1;
-    if (cnt[u] > 0 && rnk[u] < n_sel) {
-      slot = rnk[u];
-      sel_ids[slot] = u;
-    }
-    slot_of[u] = slot;
-    scores[u] = D[u];
-    counts[u] = cnt[u];
-  }
-  for (int r = n_sel + tid; r < budget; r += SEL_THREADS) sel_ids[r] = -1;
-  if (tid == 0) *n_sel_out = n_sel;
+// One workgroup: the batch's aggregation and selection.
+__global__ __launch_bounds__(SEL_THREADS)
+void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
+              const float *__restrict__ cost, int budget, int binary,
+              float *__restrict__ scores, int32_t *__restrict__ counts,
+              int32_t *__restrict__ sel_ids, int32_t *__restrict__ n_sel_out,
+              int32_t *__restrict__ slot_of) {
+  __shared__ SelLds S;
+  int uk[MAX_K];
+  float ck[MAX_K];
+  load_routes(B, K, ids, cost, uk, ck);
+  select_body(S, B, K, E, budget, binary, uk, ck, true, scores, counts, sel_ids, n_sel_out,
+              slot_of, nullptr);
 }
 
 constexpr int BF_WAVES = 4;
+constexpr int SB_WAVES = SEL_THREADS / WAVE;   // tokens per workgroup of k_select_backfill
 
-// One wavefront per token.  The kept experts (slot_of >= 0) are packed into
-// an LDS list with their keys (logit, index) for this token; each is ranked
-// among them, and the first min(K, n_sel) by rank are executed in rank
-// order.  Under the drop rule the token executes its routed experts that
-// were kept, in routing order.  Gates: exp(l_v - l_max) over the original
-// denominator (its top-K, or all E for a plain softmax router) or, with
-// renormalisation, over the executed experts.
-__global__ __launch_bounds__(BF_WAVES * WAVE)
-void k_backfill(int B, int E, int K, int norm_topk, int flags,
-                const float *__restrict__ logits, const int32_t *__restrict__ ids,
-                const int32_t *__restrict__ slot_of,
-                const int32_t *__restrict__ n_sel_p,
-                int32_t *__restrict__ exec_ids, float *__restrict__ exec_gates) {
-  __shared__ __attribute__((aligned(16))) uint64_t kk[BF_WAVES][MAX_E];
-  __shared__ int ke[BF_WAVES][MAX_E];
-  __shared__ int xs[BF_WAVES][MAX_K];
-  __shared__ float num_s[BF_WAVES][MAX_K];
-  __shared__ float den_s[BF_WAVES][MAX_K];
-  __shared__ int nx_s[BF_WAVES];
-  const int lane = lane_id(), wv = wave_id();
-  const int t = blockIdx.x * BF_WAVES + wv;
-  const int tc = min(t, B - 1);          // every wavefront takes part in the barriers
-  const int n_sel = *n_sel_p;
-  const float *lt = logits + (size_t)tc * E;
+// Per-wavefront LDS of the backfill
+template <int W>
+struct BfLds {
+  uint64_t kk[W][MAX_E];
+  int ke[W][MAX_E];
+  int xs[W][MAX_K];
+  float num_s[W][MAX_K];
+  float den_s[W][MAX_K];
+  int nx_s[W];
+};
 
-  // lane k < K: routed expert k (out-of-range ids read expert 0)
+// One wavefront per token t (wavefront wv of a workgroup of W; every
+// wavefront takes part in the barriers).  The kept experts (slot_of >= 0)
+// are packed into an LDS list with their keys (logit, index) for this
+// token; each is ranked among them, and the first min(K, n_sel) by rank are
+// executed in rank order.  Under the drop rule the token executes its
+// routed experts that were kept, in routing order.  Gates: exp(l_v - l_max)
+// over the original denominator (its top-K, or all E for a plain softmax
+// router) or, with renormalisation, over the executed experts.
+// lt: the token's logits row (global memory or an LDS copy); r_k: lane k <
+// K's routed expert (0 for an out-of-range id).
+// Lane k < K: routed expert k of token t (out-of-range ids read expert 0).
+__device__ __forceinline__ int route_of(const int32_t *__restrict__ ids, int t, int K, int E) {
+  const int lane = lane_id();
   int r_k = 0;
   if (lane < K) {
-    const int u = ids[(size_t)tc * K + lane];
+    const int u = ids[(size_t)t * K + lane];
     r_k = (u >= 0 && u < E) ? u : 0;
   }
+  return r_k;
+}
+
+template <int W>
+__device__ __forceinline__ void backfill_body(BfLds<W> &S, int t, int B, int E, int K,
+                                              int norm_topk, int flags, const float *lt,
+                                              int r_k, const int32_t *slot_of, int n_sel,
+                                              int32_t *__restrict__ exec_ids,
+                                              float *__restrict__ exec_gates) {
+  const int lane = lane_id(), wv = wave_id();
   const int r0 = __shfl(r_k, 0, WAVE);
   const float lmax = lt[r0];
 
   if (flags & 2) {   // drop: the routed experts that were kept, routing order
     const bool kept = lane < K && slot_of[r_k] >= 0;
     const uint64_t m = __ballot(kept);
-    if (kept) xs[wv][__popcll(m & ((1ull << lane) - 1))] = r_k;
-    if (lane == 0) nx_s[wv] = __popcll(m);
+    if (kept) S.xs[wv][__popcll(m & ((1ull << lane) - 1))] = r_k;
+    if (lane == 0) S.nx_s[wv] = __popcll(m);
   } else {           // backfill: first min(K, n_sel) kept experts by rank
     int base = 0;
 #pragma unroll
@@ -183,45 +228,45 @@ void k_backfill(int B, int E, int K, int norm_topk, int flags,
       const uint64_t m = __ballot(kept);
       if (kept) {
         const int pos = base + __popcll(m & ((1ull << lane) - 1));
-        kk[wv][pos] = rank_key(lt[e], e);
-        ke[wv][pos] = e;
+        S.kk[wv][pos] = rank_key(lt[e], e);
+        S.ke[wv][pos] = e;
       }
       base += __popcll(m);
     }
     const int n_kept = base;
-    if (lane == 0) nx_s[wv] = min(min(K, n_sel), n_kept);
-    if (n_kept & 1) { if (lane == 0) kk[wv][n_kept] = 0; }
+    if (lane == 0) S.nx_s[wv] = min(min(K, n_sel), n_kept);
+    if (n_kept & 1) { if (lane == 0) S.kk[wv][n_kept] = 0; }
     __syncthreads();
     const int kp = min(K, n_sel);
     for (int s = lane; s < n_kept; s += WAVE) {
-      const uint64_t ks = kk[wv][s];
+      const uint64_t ks = S.kk[wv][s];
       int r = 0;
       for (int f = 0; f < n_kept; f += 2) {
-        const u32x4 o = *reinterpret_cast<const u32x4 *>(&kk[wv][f]);
+        const u32x4 o = *reinterpret_cast<const u32x4 *>(&S.kk[wv][f]);
         r += (((uint64_t)o.y << 32 | o.x) > ks);
         r += (((uint64_t)o.w << 32 | o.z) > ks);
       }
-      if (r < kp) xs[wv][r] = ke[wv][s];
+      if (r < kp) S.xs[wv][r] = S.ke[wv][s];
     }
   }
   __syncthreads();
-  const int nx = nx_s[wv];
+  const int nx = S.nx_s[wv];
 
   // gates: numerators exp(l_v - l_max); denominator per flags
   float num = 0.0f;
   if (lane < nx) {
-    num = base_exp(lt[xs[wv][lane]] - lmax);
-    num_s[wv][lane] = num;
+    num = base_exp(lt[S.xs[wv][lane]] - lmax);
+    S.num_s[wv][lane] = num;
   }
-  if (lane < K) den_s[wv][lane] = base_exp(lt[r_k] - lmax);
+  if (lane < K) S.den_s[wv][lane] = base_exp(lt[r_k] - lmax);
   __syncthreads();
-  float S;
+  float Ssum;
   if (flags & 1) {          // renormalised over the executed experts
-    S = 0.0f;
-    for (int j = 0; j < nx; ++j) S = S + num_s[wv][j];
+    Ssum = 0.0f;
+    for (int j = 0; j < nx; ++j) Ssum = Ssum + S.num_s[wv][j];
   } else if (norm_topk) {   // the router's top-K denominator
-    S = 0.0f;
-    for (int k = 0; k < K; ++k) S = S + den_s[wv][k];
+    Ssum = 0.0f;
+    for (int k = 0; k < K; ++k) Ssum = Ssum + S.den_s[wv][k];
   } else {                  // the router's full softmax denominator
     float part = 0.0f;
 #pragma unroll
@@ -229,12 +274,68 @@ void k_backfill(int B, int E, int K, int norm_topk, int flags,
       const int e = lane + WAVE * i;
       if (e < E) part = part + base_exp(lt[e] - lmax);
     }
-    S = wave_tree_sum(part);
+    Ssum = wave_tree_sum(part);
   }
   if (t < B && lane < K) {
-    exec_ids[(size_t)t * K + lane] = (lane < nx) ? xs[wv][lane] : -1;
-    exec_gates[(size_t)t * K + lane] = (lane < nx) ? num / S : 0.0f;
+    exec_ids[(size_t)t * K + lane] = (lane < nx) ? S.xs[wv][lane] : -1;
+    exec_gates[(size_t)t * K + lane] = (lane < nx) ? num / Ssum : 0.0f;
   }
+}
+
+__global__ __launch_bounds__(BF_WAVES * WAVE)
+void k_backfill(int B, int E, int K, int norm_topk, int flags,
+                const float *__restrict__ logits, const int32_t *__restrict__ ids,
+                const int32_t *__restrict__ slot_of,
+                const int32_t *__restrict__ n_sel_p,
+                int32_t *__restrict__ exec_ids, float *__restrict__ exec_gates) {
+  __shared__ BfLds<BF_WAVES> S;
+  const int t = blockIdx.x * BF_WAVES + wave_id(), tc = min(t, B - 1);
+  backfill_body<BF_WAVES>(S, t, B, E, K, norm_topk, flags, logits + (size_t)tc * E,
+                          route_of(ids, tc, K, E), slot_of, *n_sel_p, exec_ids, exec_gates);
+}
+
+// Selection and backfill in one launch: every workgroup makes the batch's
+// selection itself (the same fixed-order arithmetic, so the same result
+// everywhere; workgroup 0 writes it out) and then backfills its own
+// SB_WAVES tokens, one per wavefront, against the kept set in its LDS.
+__global__ __launch_bounds__(SEL_THREADS)
+void k_select_backfill(int B, int K, int E, const int32_t *__restrict__ ids,
+                       const float *__restrict__ cost, int budget, int binary,
+                       int norm_topk, int flags, const float *__restrict__ logits,
+                       float *__restrict__ scores, int32_t *__restrict__ counts,
+                       int32_t *__restrict__ sel_ids, int32_t *__restrict__ n_sel_out,
+                       int32_t *__restrict__ slot_of, int32_t *__restrict__ exec_ids,
+                       float *__restrict__ exec_gates) {
+  __shared__ union {
+    SelLds sel;
+    BfLds<SB_WAVES> bf;
+  } U;
+  __shared__ int slot_s[MAX_E];
+  __shared__ float lrow[SB_WAVES][MAX_E];
+  // the backfill's own loads first (its token's logits row and routes), so
+  // that they are in flight while the selection runs
+  const int lane = lane_id(), wv = wave_id();
+  const int t = blockIdx.x * SB_WAVES + wv, tc = min(t, B - 1);
+  float lv[MAX_E / WAVE];
+#pragma unroll
+  for (int i = 0; i < MAX_E / WAVE; ++i) {
+    const int e = lane + WAVE * i;
+    lv[i] = e < E ? logits[(size_t)tc * E + e] : 0.0f;
+  }
+  const int r_k = route_of(ids, tc, K, E);
+  int uk[MAX_K];
+  float ck[MAX_K];
+  load_routes(B, K, ids, cost, uk, ck);
+  const int n_sel = select_body(U.sel, B, K, E, budget, binary, uk, ck, blockIdx.x == 0,
+                                scores, counts, sel_ids, n_sel_out, slot_of, slot_s);
+#pragma unroll
+  for (int i = 0; i < MAX_E / WAVE; ++i) {
+    const int e = lane + WAVE * i;
+    if (e < E) lrow[wv][e] = lv[i];
+  }
+  __syncthreads();   // slot_s and lrow complete; the selection's LDS is free
+  backfill_body<SB_WAVES>(U.bf, t, B, E, K, norm_topk, flags, lrow[wv], r_k, slot_s, n_sel,
+                          exec_ids, exec_gates);
 }
 
 // Exclusive prefixes over slots s < n of cnt[s] (pairs), ceil(cnt[s] / 16)
@@ -375,6 +476,17 @@ hipError_t launch_select(int B, int K, int E, const int32_t *ids,
                          int32_t *slot_of, hipStream_t st) {
   launch_k(k_select, dim3(1), dim3(SEL_THREADS), 0, st, B, K, E, ids,
                      cost, budget, (int)binary, scores, counts, sel_ids, n_sel, slot_of);
+  return hipGetLastError();
+}
+
+hipError_t launch_select_backfill(int B, int K, int E, const int32_t *ids, const float *cost,
+                                  int budget, bool binary, int norm_topk, int flags,
+                                  const float *logits, float *scores, int32_t *counts,
+                                  int32_t *sel_ids, int32_t *n_sel, int32_t *slot_of,
+                                  int32_t *exec_ids, float *exec_gates, hipStream_t st) {
+  launch_k(k_select_backfill, dim3((B + SB_WAVES - 1) / SB_WAVES), dim3(SEL_THREADS), 0, st,
+           B, K, E, ids, cost, budget, (int)binary, norm_topk, flags, logits, scores, counts,
+           sel_ids, n_sel, slot_of, exec_ids, exec_gates);
   return hipGetLastError();
 }
 
