@@ -87,14 +87,34 @@ __device__ __forceinline__ uint64_t rank_key(float v, int e) {
   return ((uint64_t)o << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)e);
 }
 
-// Wave-wide first-ranked (value, index) pair; every lane gets the winner.
-__device__ __forceinline__ void wave_argbest(float &v, int &i) {
-#pragma unroll
-  for (int h = 32; h >= 1; h >>= 1) {
-    float ov = __shfl_xor(v, h, WAVE);
-    int oi = __shfl_xor(i, h, WAVE);
-    if (ranks_before(ov, oi, v, i)) { v = ov; i = oi; }
-  }
+// Wave-wide maximum of a 64-bit key (rank_key order); every lane gets it.
+// Within each row of 16 lanes by DPP moves (quad permutations, then the
+// half-row and row mirrors: after each step every lane holds the maximum of
+// its group), then over the four rows' values read out as uniform values.
+template <int CTRL>
+__device__ __forceinline__ uint64_t max_dpp(uint64_t k) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)k, CTRL, 0xF, 0xF, false);
+  const uint32_t hi =
+      (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(k >> 32), CTRL, 0xF, 0xF, false);
+  const uint64_t o = ((uint64_t)hi << 32) | lo;
+  return o > k ? o : k;
+}
+
+__device__ __forceinline__ uint64_t lane_key(uint64_t k, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)k, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(k >> 32), l);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
+  k = max_dpp<0xB1>(k);    // quad_perm [1, 0, 3, 2]: pairs
+  k = max_dpp<0x4E>(k);    // quad_perm [2, 3, 0, 1]: quads
+  k = max_dpp<0x141>(k);   // row_half_mirror: 8 lanes
+  k = max_dpp<0x140>(k);   // row_mirror: 16 lanes
+  const uint64_t a = lane_key(k, 0), b = lane_key(k, 16), c = lane_key(k, 32),
+                 d = lane_key(k, 48);
+  const uint64_t ab = a > b ? a : b, cd = c > d ? c : d;
+  return ab > cd ? ab : cd;
 }
 
 // ------------------------------------------------------------ base_exp ---

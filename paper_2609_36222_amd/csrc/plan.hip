@@ -170,7 +170,8 @@ void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
 }
 
 constexpr int BF_WAVES = 4;
-constexpr int SB_WAVES = SEL_THREADS / WAVE;   // tokens per workgroup of k_select_backfill
+constexpr int SB_WAVES = SEL_THREADS / WAVE;   // wavefronts of k_select_backfill
+constexpr int SB_TOK = 4;                      // its tokens per workgroup (wavefronts 0 ..)
 
 // Per-wavefront LDS of the backfill
 template <int W>
@@ -187,12 +188,12 @@ struct BfLds {
 // wavefront takes part in the barriers).  The kept experts (slot_of >= 0)
 // are packed into an LDS list with their keys (logit, index) for this
 // token; each is ranked among them, and the first min(K, n_sel) by rank are
-// executed in rank order.  Under the drop rule the token executes its
+// executed in rank order.  (Ranking by counting in LDS takes fewer vector
+// instructions than K successive wave maxima, which matters when 16
+// wavefronts share a CU.)  Under the drop rule the token executes its
 // routed experts that were kept, in routing order.  Gates: exp(l_v - l_max)
 // over the original denominator (its top-K, or all E for a plain softmax
 // router) or, with renormalisation, over the executed experts.
-// lt: the token's logits row (global memory or an LDS copy); r_k: lane k <
-// K's routed expert (0 for an out-of-range id).
 // Lane k < K: routed expert k of token t (out-of-range ids read expert 0).
 __device__ __forceinline__ int route_of(const int32_t *__restrict__ ids, int t, int K, int E) {
   const int lane = lane_id();
@@ -204,38 +205,44 @@ __device__ __forceinline__ int route_of(const int32_t *__restrict__ ids, int t, 
   return r_k;
 }
 
+// lt: the token's logits row (global memory or an LDS copy); r_k: lane k <
+// K's routed expert (0 for an out-of-range id).  An inactive wavefront
+// only takes part in the workgroup's barriers.
 template <int W>
-__device__ __forceinline__ void backfill_body(BfLds<W> &S, int t, int B, int E, int K,
-                                              int norm_topk, int flags, const float *lt,
+__device__ __forceinline__ void backfill_body(BfLds<W> &S, bool active, int t, int B, int E,
+                                              int K, int norm_topk, int flags, const float *lt,
                                               int r_k, const int32_t *slot_of, int n_sel,
                                               int32_t *__restrict__ exec_ids,
                                               float *__restrict__ exec_gates) {
   const int lane = lane_id(), wv = wave_id();
   const int r0 = __shfl(r_k, 0, WAVE);
-  const float lmax = lt[r0];
+  const float lmax = active ? lt[r0] : 0.0f;
 
   if (flags & 2) {   // drop: the routed experts that were kept, routing order
-    const bool kept = lane < K && slot_of[r_k] >= 0;
-    const uint64_t m = __ballot(kept);
-    if (kept) S.xs[wv][__popcll(m & ((1ull << lane) - 1))] = r_k;
-    if (lane == 0) S.nx_s[wv] = __popcll(m);
-  } else {           // backfill: first min(K, n_sel) kept experts by rank
-    int base = 0;
-#pragma unroll
-    for (int i = 0; i < MAX_E / WAVE; ++i) {
-      const int e = lane + WAVE * i;
-      const bool kept = e < E && slot_of[e] >= 0;
+    if (active) {
+      const bool kept = lane < K && slot_of[r_k] >= 0;
       const uint64_t m = __ballot(kept);
-      if (kept) {
-        const int pos = base + __popcll(m & ((1ull << lane) - 1));
-        S.kk[wv][pos] = rank_key(lt[e], e);
-        S.ke[wv][pos] = e;
-      }
-      base += __popcll(m);
+      if (kept) S.xs[wv][__popcll(m & ((1ull << lane) - 1))] = r_k;
+      if (lane == 0) S.nx_s[wv] = __popcll(m);
     }
-    const int n_kept = base;
-    if (lane == 0) S.nx_s[wv] = min(min(K, n_sel), n_kept);
-    if (n_kept & 1) { if (lane == 0) S.kk[wv][n_kept] = 0; }
+  } else {           // backfill: first min(K, n_sel) kept experts by rank
+    int n_kept = 0;
+    if (active) {
+#pragma unroll
+      for (int i = 0; i < MAX_E / WAVE; ++i) {
+        const int e = lane + WAVE * i;
+        const bool kept = e < E && slot_of[e] >= 0;
+        const uint64_t m = __ballot(kept);
+        if (kept) {
+          const int pos = n_kept + __popcll(m & ((1ull << lane) - 1));
+          S.kk[wv][pos] = rank_key(lt[e], e);
+          S.ke[wv][pos] = e;
+        }
+        n_kept += __popcll(m);
+      }
+      if (lane == 0) S.nx_s[wv] = min(min(K, n_sel), n_kept);
+      if (n_kept & 1) { if (lane == 0) S.kk[wv][n_kept] = 0; }
+    }
     __syncthreads();
     const int kp = min(K, n_sel);
     for (int s = lane; s < n_kept; s += WAVE) {
@@ -250,7 +257,7 @@ __device__ __forceinline__ void backfill_body(BfLds<W> &S, int t, int B, int E, 
     }
   }
   __syncthreads();
-  const int nx = S.nx_s[wv];
+  const int nx = active ? S.nx_s[wv] : 0;
 
   // gates: numerators exp(l_v - l_max); denominator per flags
   float num = 0.0f;
@@ -258,8 +265,9 @@ __device__ __forceinline__ void backfill_body(BfLds<W> &S, int t, int B, int E, 
     num = base_exp(lt[S.xs[wv][lane]] - lmax);
     S.num_s[wv][lane] = num;
   }
-  if (lane < K) S.den_s[wv][lane] = base_exp(lt[r_k] - lmax);
+  if (active && lane < K) S.den_s[wv][lane] = base_exp(lt[r_k] - lmax);
   __syncthreads();
+  if (!active) return;
   float Ssum;
   if (flags & 1) {          // renormalised over the executed experts
     Ssum = 0.0f;
@@ -290,14 +298,16 @@ void k_backfill(int B, int E, int K, int norm_topk, int flags,
                 int32_t *__restrict__ exec_ids, float *__restrict__ exec_gates) {
   __shared__ BfLds<BF_WAVES> S;
   const int t = blockIdx.x * BF_WAVES + wave_id(), tc = min(t, B - 1);
-  backfill_body<BF_WAVES>(S, t, B, E, K, norm_topk, flags, logits + (size_t)tc * E,
+  backfill_body<BF_WAVES>(S, true, t, B, E, K, norm_topk, flags, logits + (size_t)tc * E,
                           route_of(ids, tc, K, E), slot_of, *n_sel_p, exec_ids, exec_gates);
 }
 
 // Selection and backfill in one launch: every workgroup makes the batch's
 // selection itself (the same fixed-order arithmetic, so the same result
 // everywhere; workgroup 0 writes it out) and then backfills its own
-// SB_WAVES tokens, one per wavefront, against the kept set in its LDS.
+// SB_TOK tokens, one per wavefront, against the kept set in its LDS (more
+// workgroups with fewer tokens each: the backfill's vector work spreads
+// over more CUs).
 __global__ __launch_bounds__(SEL_THREADS)
 void k_select_backfill(int B, int K, int E, const int32_t *__restrict__ ids,
                        const float *__restrict__ cost, int budget, int binary,
@@ -311,31 +321,34 @@ void k_select_backfill(int B, int K, int E, const int32_t *__restrict__ ids,
     BfLds<SB_WAVES> bf;
   } U;
   __shared__ int slot_s[MAX_E];
-  __shared__ float lrow[SB_WAVES][MAX_E];
+  __shared__ float lrow[SB_TOK][MAX_E];
   // the backfill's own loads first (its token's logits row and routes), so
   // that they are in flight while the selection runs
   const int lane = lane_id(), wv = wave_id();
-  const int t = blockIdx.x * SB_WAVES + wv, tc = min(t, B - 1);
+  const bool active = wv < SB_TOK;
+  const int t = blockIdx.x * SB_TOK + wv, tc = min(t, B - 1);
   float lv[MAX_E / WAVE];
 #pragma unroll
   for (int i = 0; i < MAX_E / WAVE; ++i) {
     const int e = lane + WAVE * i;
-    lv[i] = e < E ? logits[(size_t)tc * E + e] : 0.0f;
+    lv[i] = (active && e < E) ? logits[(size_t)tc * E + e] : 0.0f;
   }
-  const int r_k = route_of(ids, tc, K, E);
+  const int r_k = active ? route_of(ids, tc, K, E) : 0;
   int uk[MAX_K];
   float ck[MAX_K];
   load_routes(B, K, ids, cost, uk, ck);
   const int n_sel = select_body(U.sel, B, K, E, budget, binary, uk, ck, blockIdx.x == 0,
                                 scores, counts, sel_ids, n_sel_out, slot_of, slot_s);
+  if (active) {
 #pragma unroll
-  for (int i = 0; i < MAX_E / WAVE; ++i) {
-    const int e = lane + WAVE * i;
-    if (e < E) lrow[wv][e] = lv[i];
+    for (int i = 0; i < MAX_E / WAVE; ++i) {
+      const int e = lane + WAVE * i;
+      if (e < E) lrow[wv][e] = lv[i];
+    }
   }
   __syncthreads();   // slot_s and lrow complete; the selection's LDS is free
-  backfill_body<SB_WAVES>(U.bf, t, B, E, K, norm_topk, flags, lrow[wv], r_k, slot_s, n_sel,
-                          exec_ids, exec_gates);
+  backfill_body<SB_WAVES>(U.bf, active, t, B, E, K, norm_topk, flags,
+                          lrow[active ? wv : 0], r_k, slot_s, n_sel, exec_ids, exec_gates);
 }
 
 // Exclusive prefixes over slots s < n of cnt[s] (pairs), ceil(cnt[s] / 16)
@@ -484,7 +497,7 @@ hipError_t launch_select_backfill(int B, int K, int E, const int32_t *ids, const
                                   const float *logits, float *scores, int32_t *counts,
                                   int32_t *sel_ids, int32_t *n_sel, int32_t *slot_of,
                                   int32_t *exec_ids, float *exec_gates, hipStream_t st) {
-  launch_k(k_select_backfill, dim3((B + SB_WAVES - 1) / SB_WAVES), dim3(SEL_THREADS), 0, st,
+  launch_k(k_select_backfill, dim3((B + SB_TOK - 1) / SB_TOK), dim3(SEL_THREADS), 0, st,
            B, K, E, ids, cost, budget, (int)binary, norm_topk, flags, logits, scores, counts,
            sel_ids, n_sel, slot_of, exec_ids, exec_gates);
   return hipGetLastError();

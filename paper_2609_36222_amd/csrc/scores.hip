@@ -247,9 +247,7 @@ void k_tail(int B, int E, int K, int norm_topk, const float *__restrict__ logits
             const float *__restrict__ q, const float *__restrict__ ss,
             const float *__restrict__ bp, int32_t *__restrict__ ids_io,
             float *__restrict__ w_io, float *__restrict__ cost, int mode, int rule) {
-  __shared__ __attribute__((aligned(16))) uint64_t keys[TL_WAVES][MAX_E];
   __shared__ float lrow[TL_WAVES][MAX_E];
-  __shared__ int top[TL_WAVES][MAX_K];
   __shared__ float eps_s[TL_WAVES][MAX_K];
   const int lane = lane_id(), wv = wave_id();
   const int t = blockIdx.x * TL_WAVES + wv;
@@ -266,31 +264,28 @@ void k_tail(int B, int E, int K, int norm_topk, const float *__restrict__ logits
     for (int i = 0; i < MAX_E / WAVE; ++i) {
       const int e = lane + WAVE * i;
       lv[i] = (e < E) ? lt[e] : 0.0f;
-      kv[i] = rank_key(lv[i], e);
+      kv[i] = (e < E) ? rank_key(lv[i], e) : 0;    // 0 ranks after every expert
       if (e < E) lrow[wv][e] = lv[i];
-      if (e < ((E + 1) & ~1)) keys[wv][e] = (e < E) ? kv[i] : 0;   // 0 ranks last
     }
-    __syncthreads();
-    // rank of (l_e, e) in the order (logit desc, index asc) among all E
+    // the top K in the order (logit desc, index asc): K successive wave
+    // maxima of the keys, each winner removed by the lane holding it (keys
+    // are distinct); lane k keeps route k
+    int top0 = 0;
+    for (int k = 0; k < K; ++k) {
+      uint64_t best = 0;
 #pragma unroll
-    for (int i = 0; i < MAX_E / WAVE; ++i) {
-      const int e = lane + WAVE * i;
-      if (i * WAVE < E) {
-        int rank = 0;
-        for (int f = 0; f < E; f += 2) {
-          const u32x4 o = *reinterpret_cast<const u32x4 *>(&keys[wv][f]);
-          rank += (((uint64_t)o.y << 32 | o.x) > kv[i]);
-          rank += (((uint64_t)o.w << 32 | o.z) > kv[i]);
-        }
-        if (e < E && rank < K) top[wv][rank] = e;
-      }
+      for (int i = 0; i < MAX_E / WAVE; ++i) best = kv[i] > best ? kv[i] : best;
+      const uint64_t win = wave_max_key(best);
+      const int e = (int)(0xFFFFFFFFu - (uint32_t)win);
+      if (k == 0) top0 = e;
+      if (lane == k) my_id = e;
+#pragma unroll
+      for (int i = 0; i < MAX_E / WAVE; ++i)
+        if (kv[i] == win) kv[i] = 0;
     }
     __syncthreads();
-    const float lmax = lrow[wv][top[wv][0]];
-    if (lane < K) {
-      my_id = top[wv][lane];
-      eps_s[wv][lane] = base_exp(lrow[wv][my_id] - lmax);
-    }
+    const float lmax = lrow[wv][top0];
+    if (lane < K) eps_s[wv][lane] = base_exp(lrow[wv][my_id] - lmax);
     __syncthreads();
     float S;
     if (norm_topk) {
