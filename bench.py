@@ -47,6 +47,10 @@ METRIC = ("MoE decode-step latency (µs) + HBM GB/s vs peak at batch "
           "64/256, budget B_e")
 DOMINANT = "ffn_gateup"
 PROFILE_DIR = os.path.join(ROOT, "profiles")
+SHAPE_LABEL = {"tiny": "tiny fp32", "olmoe": "OLMoE-shaped", "qwen3_b64": "Qwen3-30B-A3B-shaped",
+               "qwen3_b256": "Qwen3-30B-A3B-shaped", "mixtral": "Mixtral-shaped",
+               "deepseek_v2_lite": "DeepSeek-V2-Lite-shaped",
+               "qwen15_moe": "Qwen1.5-MoE-A2.7B-shaped"}
 
 
 def parse_args():
@@ -70,7 +74,7 @@ def parse_args():
                    help="keep the experts row-major instead of packing them")
     p.add_argument("--eager", action="store_true",
                    help="skip the HIP graph replay timing")
-    p.add_argument("--sweep", default="8,16,24,32,48,64,96,128",
+    p.add_argument("--sweep", default="4,8,16,24,32,48,64,96,128",
                    help="budgets B_e of the latency-vs-budget sweep "
                         "(comma list; empty: no sweep)")
     p.add_argument("--sweep-steps", type=int, default=100)
@@ -477,9 +481,15 @@ def main():
     for r in range(args.layers):
         inp = W.layer_inputs(args.workload, layer=r)
         wdev = (bf16(inp["w13"]), bf16(inp["w2"])) if shape.bf16 else (f32(inp["w13"]), f32(inp["w2"]))
+        shared = None
+        if shape.n_shared:
+            g = inp.get("shared_gate")
+            shared = (bf16(inp["w13_shared"]), bf16(inp["w2_shared"]),
+                      None if g is None else f32(g))
         lay = bd.Layer(f32(inp["w_router"]), f32(inp["b_router"]),
                        f32(inp["pred_a"]), f32(inp["pred_b"]), *wdev,
-                       score_rule=args.score_rule)
+                       norm_topk=shape.norm_topk, score_rule=args.score_rule,
+                       shared=shared)
         if shape.bf16 and not args.rowmajor:   # one-time, outside timing
             lay = bd.packed_layer(lay, shape.K)
             del wdev
@@ -710,9 +720,12 @@ def main():
         "dtype": "bf16" if shape.bf16 else "f32",
         "data": "synthetic",
         "config": {
-            "workload": f"{args.workload}: Qwen3-30B-A3B-shaped MoE layer d={shape.d} "
-                        f"E={shape.E} top-{shape.K} I={shape.I}, batch {B}, "
-                        f"B_e={budget}, bf16 experts, fp32 router+predictor",
+            "workload": f"{args.workload}: {SHAPE_LABEL.get(args.workload, '')} MoE layer d={shape.d} "
+                        f"E={shape.E} top-{shape.K} I={shape.I}"
+                        + (f" + {shape.n_shared} shared experts" if shape.n_shared else "")
+                        + f", batch {B}, B_e={budget}, "
+                        + ("bf16 experts" if shape.bf16 else "fp32 experts")
+                        + ", fp32 router+predictor",
             "batch": B, "budget": budget, "n_sel": n_sel, "pairs": pairs,
             "expert_layout": "row-major" if (args.rowmajor or not shape.bf16) else "packed",
             "score_rule": args.score_rule,

@@ -144,7 +144,22 @@ typedef struct base_layer {
     const void *w13;        /* [E][2I][d]: rows 0..I-1 gate, I..2I-1 up;
                                16-B aligned */
     const void *w2;         /* [E][d][I] down projection; 16-B aligned */
+    /* Shared experts: always active for every token, outside the budget
+     * and the selection (the paper leaves them out of its notation, Sec.
+     * 3.1; its DeepSeek-V2-Lite and Qwen1.5-MoE models have them).  bf16
+     * layers only (else BASE_ERR_DTYPE).  Each has the routed experts'
+     * shape; a wider shared expert (intermediate size m I) is given as m of
+     * them: its gate rows, up rows and down columns cut into m consecutive
+     * blocks of I. */
+    int32_t n_shared;          /* 0 .. BASE_MAX_SHARED */
+    const void *w13_shared;    /* [n_shared][2I][d], layout w_layout; 16-B aligned */
+    const void *w2_shared;     /* [n_shared][d][I], layout w_layout; 16-B aligned */
+    const float *shared_gate;  /* [d] fp32: the shared experts' outputs are
+                                  scaled by sigmoid(x_t . shared_gate), or NULL:
+                                  by 1 */
 } base_layer;
+
+#define BASE_MAX_SHARED 8
 
 /* Device pointers into the caller's workspace, filled by base_moe_forward
  * and base_decode_layer when plan_out != NULL.  Arrays not produced by the
@@ -163,12 +178,16 @@ typedef struct base_plan {
     /* produced by both */
     int32_t *exec_ids;        /* [B][K] expert executed at rank j, -1 padded */
     float   *exec_gates;      /* [B][K] its gate, 0 padded */
-    int32_t *offsets;         /* [budget+1] first pair of each slot; the
-                                 entries from n_sel on equal the pair count */
-    int32_t *pair_tok;        /* [B*K] token of pair p (pairs sorted by
-                                 (slot, token)) */
-    float   *pair_gate;       /* [B*K] gate of pair p */
-    int32_t *pair_of;         /* [B][K] pair index of (t, j), -1 if none */
+    int32_t *offsets;         /* [budget+n_shared+1] first pair of each
+                                 slot: kept slots 0 .. n_sel-1, then the
+                                 routed pair count up to index budget, then
+                                 shared expert i at budget+i (B pairs each,
+                                 after every routed pair) */
+    int32_t *pair_tok;        /* [B*K + n_shared*B] token of pair p (pairs
+                                 sorted by (slot, token)) */
+    float   *pair_gate;       /* [B*K + n_shared*B] gate of pair p */
+    int32_t *pair_of;         /* [B][K+n_shared] pair index of (t, j), -1 if
+                                 none; j >= K: shared expert j-K */
 } base_plan;
 
 /* Bytes of workspace base_moe_forward / base_decode_layer need for this
@@ -218,7 +237,10 @@ base_status base_select(const base_layer *L, int32_t B,
  * backfill (or drop) per token, gates per `flags`, compaction of the
  * executed (token, expert) pairs by kept slot, grouped SwiGLU FFN over the
  * kept experts only -- each kept expert's weights are read once -- and
- *   y_t = residual_t + sum_j gate_{t,j} E_{X_t[j]}(x_t)   (j ascending).
+ *   y_t = residual_t + sum_j gate_{t,j} E_{X_t[j]}(x_t)   (j ascending)
+ *         + sum_i g_t S_i(x_t)   (shared experts, i ascending; g_t =
+ *         sigmoid(x_t . shared_gate) with the dot product in the fixed
+ *         order above and 1 / (1 + exp(-s)) in fp32, or 1).
  *   logits, topk_ids          from base_route
  *   sel_ids, n_sel, slot_of_expert   from base_select (same budget)
  *   residual  [B][d] (L->dtype) or NULL
@@ -243,7 +265,9 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
                               void *stream);
 
 /* Packed expert weights (BASE_W_PACKED).  A one-time permutation, done when
- * a model is loaded; the values are unchanged.  With 16-row tiles and
+ * a model is loaded; the values are unchanged.  The shared experts of a
+ * packed layer are packed the same way, by a call whose L has E = n_shared
+ * and w13, w2 = w13_shared, w2_shared (K and n_shared are not read).  With 16-row tiles and
  * 32-element k-steps, a "fragment" is 16 rows x 32 elements of one matrix,
  * stored as 64 lanes x 8 consecutive elements (lane l: row l % 16,
  * elements 8 (l / 16) .. +7 of the k-step).  Rows are grouped four tiles at

@@ -319,10 +319,14 @@ def gates64(logits, ids, exec_ids, n_exec, norm_topk=1, flags=0):
     return g
 
 
-def compact(exec_ids, n_exec, slot_of, gates, budget):
+def compact(exec_ids, n_exec, slot_of, gates, budget, n_shared=0, shared_gates=None):
     """Token-to-expert compaction: the executed pairs (t, j) sorted by
     (slot, token).  offsets[s] = first pair of slot s (offsets[budget] = P),
-    pair_tok/pair_gate per pair, pair_of[t, j] = pair index (or -1)."""
+    pair_tok/pair_gate per pair, pair_of[t, j] = pair index (or -1).  With
+    n_shared shared experts, shared expert i follows as B more pairs (every
+    token in order, gate shared_gates[t] or 1): offsets[budget + i] is its
+    first pair, offsets[budget + n_shared] the total, and pair_of gets
+    columns K + i."""
     B, K = exec_ids.shape
     pairs = []
     for t in range(B):
@@ -346,7 +350,30 @@ def compact(exec_ids, n_exec, slot_of, gates, budget):
     for s in range(budget - 1, -1, -1):
         if s not in seen:
             offsets[s] = offsets[s + 1]
+    if n_shared:
+        g = np.ones(B, np.float32) if shared_gates is None else np.asarray(shared_gates, np.float32)
+        offsets = np.concatenate([offsets, P + B * np.arange(1, n_shared + 1)]).astype(np.int32)
+        pair_tok = np.concatenate([pair_tok] + [np.arange(B, dtype=np.int32)] * n_shared)
+        pair_gate = np.concatenate([pair_gate] + [g] * n_shared).astype(np.float32)
+        pair_of = np.concatenate(
+            [pair_of] + [(P + i * B + np.arange(B, dtype=np.int32))[:, None]
+                         for i in range(n_shared)], axis=1).astype(np.int32)
     return offsets, pair_tok, pair_gate, pair_of
+
+
+def shared_gate_c(x, gate):
+    """The shared experts' gate at the canonical fp32 level: s = x . gate in
+    the fixed dot-product order, g = 1 / (1 + exp(-s)) (one fp32 operation at
+    a time, exp as cexp)."""
+    s = carith.cdot_matrix(np.asarray(x, np.float32), np.asarray(gate, np.float32)[None, :])[:, 0]
+    e = carith.cexp((-s).astype(np.float32))
+    den = (np.float32(1.0) + e).astype(np.float32)
+    return (np.float32(1.0) / den).astype(np.float32)
+
+
+def shared_gate64(x, gate):
+    s = np.asarray(x, np.float64) @ np.asarray(gate, np.float64)
+    return 1.0 / (1.0 + np.exp(-s))
 
 
 def moe_restricted64(x, exec_ids, n_exec, gates, experts, residual=None,
@@ -367,9 +394,12 @@ def moe_restricted64(x, exec_ids, n_exec, gates, experts, residual=None,
 # ------------------------------------------------ canonical fp32 pipeline --
 def decode_layer_c(x, w_router, b_router, pred_a, pred_b, K, budget,
                    experts=None, norm_topk=1, flags=0, residual=None,
-                   score_rule=SCORE_BASE):
+                   score_rule=SCORE_BASE, shared=None):
     """The whole hot path at the canonical fp32 level (ids, gates and plan)
-    with the expert FFN in fp64 on the same plan."""
+    with the expert FFN in fp64 on the same plan.  shared: None or a dict
+    with the always-active shared experts ("experts": Experts, "gate": [d]
+    or None): they run on every token, outside the budget, and add
+    g_t S_i(x_t) to y (g_t = sigmoid(x_t . gate) or 1)."""
     logits, ids, w = carith.route(x, w_router, b_router, K, norm_topk)
     cost = pair_scores_c(score_rule, x, pred_a, pred_b, ids, w)
     E = logits.shape[1]
@@ -379,15 +409,25 @@ def decode_layer_c(x, w_router, b_router, pred_a, pred_b, K, budget,
                               binary=score_rule == SCORE_TOP1)
     ex, n_ex = backfill(logits, ids, slot, n_sel, K, flags)
     g = gates_c(logits, ids, ex, n_ex, norm_topk, flags)
+    ns = 0 if shared is None else shared["experts"].E
+    sg = None
+    if ns and shared.get("gate") is not None:
+        sg = shared_gate_c(x, shared["gate"])
     offsets, pair_tok, pair_gate, pair_of = compact(ex, n_ex, slot, g,
-                                                    budget_c)
+                                                    budget_c, ns, sg)
     out = dict(logits=logits, topk_ids=ids, topk_w=w, cost=cost,
                scores=scores, counts=counts, sel_ids=sel, n_sel=n_sel,
                slot_of_expert=slot, exec_ids=ex, n_exec=n_ex, exec_gates=g,
                offsets=offsets, pair_tok=pair_tok, pair_gate=pair_gate,
                pair_of=pair_of)
+    if ns:
+        out["shared_gate"] = np.ones(x.shape[0], np.float32) if sg is None else sg
     if experts is not None:
-        out["y"] = moe_restricted64(x, ex, n_ex, g, experts, residual)
+        y = moe_restricted64(x, ex, n_ex, g, experts, residual)
+        for i in range(ns):
+            y += (np.asarray(out["shared_gate"], np.float64)[:, None]
+                  * shared["experts"].forward(i, np.asarray(x)))
+        out["y"] = y
     return out
 
 

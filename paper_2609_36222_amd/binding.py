@@ -35,7 +35,9 @@ class base_layer(ctypes.Structure):
     _fields_ = [("d", _i32), ("E", _i32), ("K", _i32), ("I", _i32),
                 ("dtype", _i32), ("norm_topk", _i32), ("w_layout", _i32),
                 ("score_rule", _i32), ("w_router", _vp), ("b_router", _vp), ("pred_a", _vp),
-                ("pred_b", _vp), ("w13", _vp), ("w2", _vp)]
+                ("pred_b", _vp), ("w13", _vp), ("w2", _vp),
+                ("n_shared", _i32), ("w13_shared", _vp), ("w2_shared", _vp),
+                ("shared_gate", _vp)]
 
 
 _PLAN_FIELDS = ["logits", "topk_ids", "topk_w", "cost", "scores", "counts",
@@ -127,10 +129,13 @@ class Layer:
     """One MoE layer: torch tensors plus the C descriptor pointing at them.
 
     w_router, b_router, pred_a, pred_b: fp32; w13 [E,2I,d], w2 [E,d,I]:
-    fp32 or bf16 (the layer dtype, also the dtype of x and y)."""
+    fp32 or bf16 (the layer dtype, also the dtype of x and y).  shared:
+    None or (w13_shared [S,2I,d], w2_shared [S,d,I], gate [d] fp32 or
+    None), the always-active shared experts."""
 
     def __init__(self, w_router, b_router, pred_a, pred_b, w13, w2,
-                 norm_topk: int = 1, w_layout: int = 0, score_rule: int = 0):
+                 norm_topk: int = 1, w_layout: int = 0, score_rule: int = 0,
+                 shared=None):
         import torch
         E, d = w_router.shape
         I = w2.shape[2]
@@ -142,6 +147,7 @@ class Layer:
         self.norm_topk = norm_topk
         self.w_layout = w_layout
         self.score_rule = score_rule
+        self.shared = shared
         self._desc = None
 
     def desc(self, K: int) -> base_layer:
@@ -149,7 +155,14 @@ class Layer:
         return base_layer(self.d, self.E, K, self.I, self.dtype,
                           self.norm_topk, self.w_layout, self.score_rule,
                           _ptr(w_router), _ptr(b_router),
-                          _ptr(pred_a), _ptr(pred_b), _ptr(w13), _ptr(w2))
+                          _ptr(pred_a), _ptr(pred_b), _ptr(w13), _ptr(w2),
+                          *self._shared_fields())
+
+    def _shared_fields(self):
+        if self.shared is None:
+            return (0, None, None, None)
+        w13s, w2s, gate = self.shared
+        return (int(w13s.shape[0]), _ptr(w13s), _ptr(w2s), _ptr(gate))
 
 
 def base_workspace_bytes(desc: base_layer, B: int, budget: int) -> int:
@@ -211,8 +224,17 @@ def packed_layer(layer: "Layer", K: int, stream=None) -> "Layer":
     w_router, b_router, pred_a, pred_b, w13, w2 = layer.tensors
     w13p, w2p = torch.empty_like(w13), torch.empty_like(w2)
     base_pack_experts(layer.desc(K), w13p, w2p, stream)
+    shared = None
+    if layer.shared is not None:
+        w13s, w2s, gate = layer.shared
+        d = base_layer(layer.d, int(w13s.shape[0]), 1, layer.I, layer.dtype, layer.norm_topk,
+                       W_ROWMAJOR, 0, None, None, None, None, _ptr(w13s), _ptr(w2s),
+                       0, None, None, None)
+        w13sp, w2sp = torch.empty_like(w13s), torch.empty_like(w2s)
+        base_pack_experts(d, w13sp, w2sp, stream)
+        shared = (w13sp, w2sp, gate)
     return Layer(w_router, b_router, pred_a, pred_b, w13p, w2p,
-                 layer.norm_topk, W_PACKED, layer.score_rule)
+                 layer.norm_topk, W_PACKED, layer.score_rule, shared)
 
 
 def base_set_stage_events(events):

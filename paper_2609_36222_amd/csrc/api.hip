@@ -48,11 +48,23 @@ base_status check_layer(const base_layer *L, int32_t B, bool need_router,
     if (!L->pred_b) return BASE_ERR_NULL;
     if (!aligned(L->pred_b, 4)) return BASE_ERR_ALIGN;
   }
+  if (L->n_shared < 0 || L->n_shared > BASE_MAX_SHARED) return BASE_ERR_SHAPE;
+  if (L->n_shared > 0 && L->dtype != BASE_BF16) return BASE_ERR_DTYPE;
+  if (L->shared_gate && !aligned(L->shared_gate, 16)) return BASE_ERR_ALIGN;
   if (need_experts) {
     if (!L->w13 || !L->w2) return BASE_ERR_NULL;
     if (!aligned(L->w13, 16) || !aligned(L->w2, 16)) return BASE_ERR_ALIGN;
+    if (L->n_shared > 0) {
+      if (!L->w13_shared || !L->w2_shared) return BASE_ERR_NULL;
+      if (!aligned(L->w13_shared, 16) || !aligned(L->w2_shared, 16)) return BASE_ERR_ALIGN;
+    }
   }
   return BASE_OK;
+}
+
+// the shared-expert gate vector (only with shared experts)
+const float *shared_gate(const base_layer *L) {
+  return L->n_shared > 0 ? L->shared_gate : nullptr;
 }
 
 base_status check_ptr(const void *p, size_t a) {
@@ -73,7 +85,7 @@ base_status check_ptr(const void *p, size_t a) {
 
 // Workspace layout: every array starts on a 256-byte boundary.
 struct Layout {
-  size_t logits, q, ss, topk_ids, topk_w, cost, scores, counts, sel_ids, n_sel,
+  size_t logits, q, ss, gdot, topk_ids, topk_w, cost, scores, counts, sel_ids, n_sel,
       slot_of, exec_ids, exec_gates, offsets, pair_tok, pair_gate, pair_of,
       parts, n_parts, xp, H, pairbuf, total;
 };
@@ -89,9 +101,12 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
     return here;
   };
   const size_t BK = (size_t)B * L->K;
+  const int ns = L->n_shared;
+  const size_t P = BK + (size_t)ns * B;   // routed pairs + shared pairs
   o.logits = take((size_t)B * L->E * 4);
   o.q = take((size_t)B * L->E * 4);
   o.ss = take((size_t)B * 4);
+  o.gdot = take((size_t)B * 4);
   o.topk_ids = take(BK * 4);
   o.topk_w = take(BK * 4);
   o.cost = take(BK * 4);
@@ -102,22 +117,22 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
   o.slot_of = take((size_t)L->E * 4);
   o.exec_ids = take(BK * 4);
   o.exec_gates = take(BK * 4);
-  o.offsets = take(((size_t)bc + 1) * 4);
-  o.pair_tok = take(BK * 4);
-  o.pair_gate = take(BK * 4);
-  o.pair_of = take(BK * 4);
-  o.parts = take((size_t)ffn_max_parts(B, L->K, bc) * sizeof(PartRec));
+  o.offsets = take(((size_t)bc + ns + 1) * 4);
+  o.pair_tok = take(P * 4);
+  o.pair_gate = take(P * 4);
+  o.pair_of = take((size_t)B * (L->K + ns) * 4);
+  o.parts = take((size_t)ffn_max_parts(B, L->K, bc, ns) * sizeof(PartRec));
   o.n_parts = take(4);
   if (L->dtype == BASE_BF16) {
     // fragment-ordered tokens and SwiGLU activations (16-pair tiles)
-    const size_t tiles = (size_t)ffn_max_tiles(B, L->K, bc);
+    const size_t tiles = (size_t)ffn_max_tiles(B, L->K, bc, ns);
     o.xp = take(tiles * 16 * (size_t)L->d * 2);
     o.H = take(tiles * 16 * (size_t)L->I * 2);
   } else {
     o.xp = 0;
     o.H = take(BK * L->I * 4);
   }
-  o.pairbuf = take(BK * L->d * 4);
+  o.pairbuf = take(P * L->d * 4);
   o.total = at;
   return o;
 }
@@ -169,28 +184,29 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
   stage(4);
   PartRec *parts = at<PartRec>(ws, o.parts);
   int32_t *n_parts = at<int32_t>(ws, o.n_parts);
-  HIP_TRY(launch_compact(B, L->K, L->E, bc, exec_ids, exec_gates, slot_of, n_sel,
-                         offsets, pair_tok, pair_gate, pair_of, sel_ids, parts,
-                         n_parts, st));
+  const int ns = L->n_shared;
+  HIP_TRY(launch_compact(B, L->K, L->E, bc, ns, exec_ids, exec_gates, slot_of, n_sel,
+                         shared_gate(L) ? at<float>(ws, o.gdot) : nullptr, offsets,
+                         pair_tok, pair_gate, pair_of, sel_ids, parts, n_parts, st));
   stage_end(st);
   stage(5);
   if (bf16)
-    HIP_TRY(launch_gather(x, B, L->d, L->K, bc, parts, n_parts, pair_tok,
-                          at<void>(ws, o.xp), st));
+    HIP_TRY(launch_gather(x, B, L->d, ffn_max_parts(B, L->K, bc, ns), parts, n_parts,
+                          pair_tok, at<void>(ws, o.xp), st));
   stage_end(st);
   stage(6);
   const bool packed = L->w_layout == BASE_W_PACKED;
-  HIP_TRY(launch_gateup(bf16, packed, x, B, L->d, L->I, L->E, L->K, bc, L->w13,
-                        sel_ids, n_sel, offsets, pair_tok, parts, n_parts,
+  HIP_TRY(launch_gateup(bf16, packed, x, B, L->d, L->I, L->E, L->K, bc, ns, L->w13,
+                        L->w13_shared, sel_ids, n_sel, offsets, pair_tok, parts, n_parts,
                         at<void>(ws, o.xp), at<void>(ws, o.H), st));
   stage_end(st);
   stage(7);
-  HIP_TRY(launch_down(bf16, packed, B, L->d, L->I, L->E, L->K, bc, L->w2,
-                      sel_ids, n_sel, offsets, parts, n_parts, pair_gate,
+  HIP_TRY(launch_down(bf16, packed, B, L->d, L->I, L->E, L->K, bc, ns, L->w2,
+                      L->w2_shared, sel_ids, n_sel, offsets, parts, n_parts, pair_gate,
                       at<void>(ws, o.H), at<float>(ws, o.pairbuf), st));
   stage_end(st);
   stage(8);
-  HIP_TRY(launch_combine(bf16, B, L->d, L->K, pair_of, at<float>(ws, o.pairbuf),
+  HIP_TRY(launch_combine(bf16, B, L->d, L->K + ns, pair_of, at<float>(ws, o.pairbuf),
                          residual, y, st));
   stage_end(st);
   return BASE_OK;
@@ -248,7 +264,7 @@ base_status base_route(const base_layer *L, const void *x, int32_t B,
   const bool bf16 = L->dtype == BASE_BF16;
   stage(0);
   HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
-                        nullptr, 0, logits, nullptr, nullptr, st));
+                        nullptr, 0, nullptr, logits, nullptr, nullptr, nullptr, st));
   stage_end(st);
   stage(1);
   HIP_TRY(launch_tail(B, L->E, L->K, L->norm_topk, logits, nullptr, nullptr,
@@ -320,6 +336,10 @@ base_status base_moe_forward(const base_layer *L, const void *x, int32_t B,
   const int32_t bc = budget < L->E ? budget : L->E;
   BASE_TRY(check_ws(L, B, bc, ws, ws_bytes));
   const Layout o = layout(L, B, bc);
+  if (shared_gate(L))   // the shared experts' gate: its own dot-product launch
+    HIP_TRY(launch_scores(L->dtype == BASE_BF16, x, B, L->d, nullptr, nullptr, 0, nullptr, 0,
+                          shared_gate(L), nullptr, nullptr, at<float>(ws, o.gdot), nullptr,
+                          (hipStream_t)stream));
   BASE_TRY(run_forward(L, x, B, logits, topk_ids, sel_ids, n_sel,
                        slot_of_expert, bc, flags, residual, y, ws, o,
                        (hipStream_t)stream));
@@ -356,8 +376,8 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
   const bool pred = L->score_rule == BASE_SCORE_BASE;
   stage(0);
   HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
-                        pred ? L->pred_a : nullptr, pred ? L->E : 0, logits,
-                        pred ? q : nullptr, pred ? ss : nullptr, st));
+                        pred ? L->pred_a : nullptr, pred ? L->E : 0, shared_gate(L), logits,
+                        pred ? q : nullptr, at<float>(ws, o.gdot), pred ? ss : nullptr, st));
   stage_end(st);
   stage(1);
   HIP_TRY(launch_tail(B, L->E, L->K, L->norm_topk, logits, q, ss, L->pred_b,
@@ -381,7 +401,12 @@ base_status base_pack_experts(const base_layer *L, void *w13_packed,
   if (!L) return BASE_ERR_NULL;
   if (L->dtype != BASE_BF16) return BASE_ERR_DTYPE;
   if (L->w_layout != BASE_W_ROWMAJOR) return BASE_ERR_SHAPE;
-  BASE_TRY(check_layer(L, 1, false, false, true));
+  // only the expert matrices' shape matters here (E experts of [2I][d] and
+  // [d][I]; the shared experts are packed by a call with E = n_shared)
+  base_layer C = *L;
+  C.K = 1;
+  C.n_shared = 0;
+  BASE_TRY(check_layer(&C, 1, false, false, true));
   BASE_TRY(check_ptr(w13_packed, 16));
   BASE_TRY(check_ptr(w2_packed, 16));
   HIP_TRY(launch_pack(L->w13, L->w2, w13_packed, w2_packed, L->E, L->d, L->I,

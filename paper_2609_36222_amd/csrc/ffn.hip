@@ -9,7 +9,8 @@
 //   tokens padded to 16).  Each workgroup streams its 64 gate rows and 64
 //   up rows of the expert once.
 // k_down (slot s, 64-row tile of d): pairbuf[p][c] = gate_p * (H[p] . W_d[c]).
-// k_combine: y_t = residual_t + sum_j pairbuf[pair_of[t][j]] in j order.
+// k_combine: y_t = residual_t + sum_j pairbuf[pair_of[t][j]] in j order
+//   (the K routed ranks, then the shared experts).
 //
 // MFMA operand layout used here (v_mfma_f32_16x16x32_bf16): lane l supplies
 // row (l % 16) of A and column (l % 16) of B with the 8 contraction
@@ -277,7 +278,8 @@ __device__ __forceinline__ f32x4 sum_partials(const Partials<S> &sh, int t, int 
 // t = w, w + GU_SPLIT, .. < 2, each with its up tile t + 2.
 template <bool PACKED>
 __global__ __launch_bounds__(GU_SPLIT * WAVE, 2)
-void k_gateup_bf16(int d, int I, int E, const uint16_t *__restrict__ w13,
+void k_gateup_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w13r,
+                   const uint16_t *__restrict__ w13s,
                    const PartRec *__restrict__ parts,
                    const int32_t *__restrict__ n_parts,
                    const uint16_t *__restrict__ xp, uint16_t *__restrict__ hp) {
@@ -285,8 +287,10 @@ void k_gateup_bf16(int d, int I, int E, const uint16_t *__restrict__ w13,
   const int groups = I / 32;
   Unit un;
   if (!find_unit(groups, parts, n_parts, un)) return;
-  const int u = un.u, n = un.n, tile0 = un.tile0;
-  if (u < 0 || u >= E) return;   // only for a plan not made by base_select
+  if (un.u < 0 || un.u >= E + ns) return;   // only for a plan not made by base_select
+  // experts E .. E + ns - 1 are the shared ones
+  const uint16_t *w13 = un.u < E ? w13r : w13s;
+  const int u = un.u < E ? un.u : un.u - E, n = un.n, tile0 = un.tile0;
   const int nt = (n + 15) / 16;
   const int lane = lane_id(), row = lane & 15, g = un.g;
   WeightSrc ws;
@@ -330,7 +334,8 @@ void k_gateup_bf16(int d, int I, int E, const uint16_t *__restrict__ w13,
 // row tiles t = w, w + DN_SPLIT, ...
 template <bool PACKED>
 __global__ __launch_bounds__(DN_SPLIT * WAVE, 2)
-void k_down_bf16(int d, int I, int E, const uint16_t *__restrict__ w2,
+void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
+                 const uint16_t *__restrict__ w2s,
                  const PartRec *__restrict__ parts,
                  const int32_t *__restrict__ n_parts,
                  const float *__restrict__ pair_gate,
@@ -339,8 +344,9 @@ void k_down_bf16(int d, int I, int E, const uint16_t *__restrict__ w2,
   const int groups = d / 64;
   Unit un;
   if (!find_unit(groups, parts, n_parts, un)) return;
-  const int u = un.u, n = un.n, tile0 = un.tile0, p0 = un.p0;
-  if (u < 0 || u >= E) return;   // only for a plan not made by base_select
+  if (un.u < 0 || un.u >= E + ns) return;   // only for a plan not made by base_select
+  const uint16_t *w2 = un.u < E ? w2r : w2s;
+  const int u = un.u < E ? un.u : un.u - E, n = un.n, tile0 = un.tile0, p0 = un.p0;
   const int nt = (n + 15) / 16;
   const int lane = lane_id(), row = lane & 15, g = un.g;
   WeightSrc ws;
@@ -437,7 +443,7 @@ constexpr int CB_THREADS = 256;
 
 template <bool BF16>
 __global__ __launch_bounds__(CB_THREADS)
-void k_combine(int B, int d, int K, const int32_t *__restrict__ pair_of,
+void k_combine(int B, int d, int kc, const int32_t *__restrict__ pair_of,
                const float *__restrict__ pairbuf, const void *__restrict__ res,
                void *__restrict__ y) {
   const int t = blockIdx.x;
@@ -448,9 +454,9 @@ void k_combine(int B, int d, int K, const int32_t *__restrict__ pair_of,
     if (BF16) load4((const uint16_t *)res + (size_t)t * d + c, acc);
     else load4((const float *)res + (size_t)t * d + c, acc);
   }
-  for (int j = 0; j < K; ++j) {
-    const int p = pair_of[(size_t)t * K + j];
-    if (p < 0) break;
+  for (int j = 0; j < kc; ++j) {
+    const int p = pair_of[(size_t)t * kc + j];
+    if (p < 0) continue;   // a routed rank the token does not execute
     const float4 v = *reinterpret_cast<const float4 *>(pairbuf + (size_t)p * d + c);
     acc[0] = acc[0] + v.x; acc[1] = acc[1] + v.y;
     acc[2] = acc[2] + v.z; acc[3] = acc[3] + v.w;
@@ -465,27 +471,27 @@ void k_combine(int B, int d, int K, const int32_t *__restrict__ pair_of,
   }
 }
 
-hipError_t launch_gather(const void *x, int B, int d, int K, int budget,
+hipError_t launch_gather(const void *x, int B, int d, int max_parts,
                          const PartRec *parts, const int32_t *n_parts,
                          const int32_t *pair_tok, void *xp, hipStream_t st) {
-  const long long waves = (long long)ffn_max_parts(B, K, budget) * (d / 32);
+  const long long waves = (long long)max_parts * (d / 32);
   launch_k(k_gather, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, st,
                      (const uint16_t *)x, d, parts, n_parts, pair_tok, (uint16_t *)xp);
   return hipGetLastError();
 }
 
 hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
-                         int I, int E, int K, int budget, const void *w13,
-                         const int32_t *sel_ids, const int32_t *n_sel,
+                         int I, int E, int K, int budget, int ns, const void *w13,
+                         const void *w13s, const int32_t *sel_ids, const int32_t *n_sel,
                          const int32_t *offsets, const int32_t *pair_tok,
                          const PartRec *parts, const int32_t *n_parts,
                          const void *xp, void *H, hipStream_t st) {
   if (bf16) {
-    const long long units = (long long)ffn_max_parts(B, K, budget) * (I / 32);
+    const long long units = (long long)ffn_max_parts(B, K, budget, ns) * (I / 32);
     launch_k(packed ? k_gateup_bf16<true> : k_gateup_bf16<false>,
-                       dim3(ffn_grid(units)), dim3(GU_SPLIT * WAVE), 0, st, d, I, E,
-                       (const uint16_t *)w13, parts, n_parts, (const uint16_t *)xp,
-                       (uint16_t *)H);
+                       dim3(ffn_grid(units)), dim3(GU_SPLIT * WAVE), 0, st, d, I, E, ns,
+                       (const uint16_t *)w13, (const uint16_t *)w13s, parts, n_parts,
+                       (const uint16_t *)xp, (uint16_t *)H);
   } else {
     launch_k(k_gateup_f32, dim3(budget, (I + F32_ROWS - 1) / F32_ROWS),
                        dim3(F32_ROWS * F32_TG), 0, st, (const float *)x, d, I,
@@ -496,17 +502,18 @@ hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
 }
 
 hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K,
-                       int budget, const void *w2, const int32_t *sel_ids,
+                       int budget, int ns, const void *w2, const void *w2s,
+                       const int32_t *sel_ids,
                        const int32_t *n_sel, const int32_t *offsets,
                        const PartRec *parts, const int32_t *n_parts,
                        const float *pair_gate, const void *H, float *pairbuf,
                        hipStream_t st) {
   if (bf16) {
-    const long long units = (long long)ffn_max_parts(B, K, budget) * (d / 64);
+    const long long units = (long long)ffn_max_parts(B, K, budget, ns) * (d / 64);
     launch_k(packed ? k_down_bf16<true> : k_down_bf16<false>,
-                       dim3(ffn_grid(units)), dim3(DN_SPLIT * WAVE), 0, st, d, I, E,
-                       (const uint16_t *)w2, parts, n_parts, pair_gate,
-                       (const uint16_t *)H, pairbuf);
+                       dim3(ffn_grid(units)), dim3(DN_SPLIT * WAVE), 0, st, d, I, E, ns,
+                       (const uint16_t *)w2, (const uint16_t *)w2s, parts, n_parts,
+                       pair_gate, (const uint16_t *)H, pairbuf);
   } else {
     launch_k(k_down_f32, dim3(budget, (d + F32_ROWS - 1) / F32_ROWS),
                        dim3(F32_ROWS * F32_TG), 0, st, d, I, E,
@@ -516,15 +523,15 @@ hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K
   return hipGetLastError();
 }
 
-hipError_t launch_combine(bool bf16, int B, int d, int K,
+hipError_t launch_combine(bool bf16, int B, int d, int kc,
                           const int32_t *pair_of, const float *pairbuf,
                           const void *residual, void *y, hipStream_t st) {
   dim3 grid(B, (d + CB_THREADS * 4 - 1) / (CB_THREADS * 4));
   if (bf16)
-    launch_k(k_combine<true>, grid, dim3(CB_THREADS), 0, st, B, d, K,
+    launch_k(k_combine<true>, grid, dim3(CB_THREADS), 0, st, B, d, kc,
                        pair_of, pairbuf, residual, y);
   else
-    launch_k(k_combine<false>, grid, dim3(CB_THREADS), 0, st, B, d, K,
+    launch_k(k_combine<false>, grid, dim3(CB_THREADS), 0, st, B, d, kc,
                        pair_of, pairbuf, residual, y);
   return hipGetLastError();
 }

@@ -34,11 +34,17 @@ inline void launch_k(F kernel, dim3 grid, dim3 block, uint32_t shm, hipStream_t 
   }
 }
 
+constexpr int MAX_SHARED = 8;               // shared experts per layer
+constexpr int MAX_SLOTS = MAX_E + MAX_SHARED;  // kept slots + shared slots
+
 // Upper bounds (host-known) of the FFN token tiling for a batch: 16-pair
-// tiles and 64-token parts over all kept slots.
-inline int ffn_max_tiles(int B, int K, int budget) { return (B * K + 15) / 16 + budget; }
-inline int ffn_max_parts(int B, int K, int budget) {
-  return (B * K + FFN_PART - 1) / FFN_PART + budget;
+// tiles and FFN_PART-token parts over all kept slots and the ns shared
+// slots (B pairs each).
+inline int ffn_max_tiles(int B, int K, int budget, int ns) {
+  return (B * K + 15) / 16 + budget + ns * ((B + 15) / 16);
+}
+inline int ffn_max_parts(int B, int K, int budget, int ns) {
+  return (B * K + FFN_PART - 1) / FFN_PART + budget + ns * ((B + FFN_PART - 1) / FFN_PART);
 }
 
 // The FFN's part table: entry q (one per 64-token part) describes the kept
@@ -57,10 +63,12 @@ struct alignas(32) PartRec {
 
 // rows: n_router of W_r (-> logits [B][n_router], + beta) then n_pred of A
 // (-> q [B][n_pred]); ss [B] = ||x||^2 when non-null
+// rows: n_router of Wr (logits, + beta), n_pred of A (q), then the vector G
+// when given (gdot); ss: ||x||^2 when given
 hipError_t launch_scores(bool bf16, const void *x, int B, int d, const float *Wr,
                          const float *beta, int n_router, const float *A,
-                         int n_pred, float *logits, float *q, float *ss,
-                         hipStream_t st);
+                         int n_pred, const float *G, float *logits, float *q,
+                         float *gdot, float *ss, hipStream_t st);
 // Selection rules (the values of BASE_SCORE_* in base.h): the per-pair
 // score k_tail writes as the cost
 constexpr int SCORE_BASE = 0, SCORE_TOP1 = 1, SCORE_WEIGHT = 2, SCORE_WEIGHT_SQ = 3,
@@ -90,30 +98,36 @@ hipError_t launch_backfill(int B, int E, int K, int norm_topk, int flags,
                            const int32_t *slot_of, const int32_t *n_sel,
                            int32_t *exec_ids, float *exec_gates,
                            hipStream_t st);
-hipError_t launch_compact(int B, int K, int E, int budget, const int32_t *exec_ids,
+// ns shared slots follow the kept ones (expert E + i, every token, gate
+// sigmoid(gdot[t]) or 1 when gdot is null)
+hipError_t launch_compact(int B, int K, int E, int budget, int ns, const int32_t *exec_ids,
                           const float *exec_gates, const int32_t *slot_of,
-                          const int32_t *n_sel, int32_t *offsets,
+                          const int32_t *n_sel, const float *gdot, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
                           int32_t *pair_of, const int32_t *sel_ids,
                           PartRec *parts, int32_t *n_parts, hipStream_t st);
-hipError_t launch_gather(const void *x, int B, int d, int K, int budget,
+hipError_t launch_gather(const void *x, int B, int d, int max_parts,
                          const PartRec *parts, const int32_t *n_parts,
                          const int32_t *pair_tok, void *xp, hipStream_t st);
 hipError_t launch_pack(const void *w13, const void *w2, void *w13p, void *w2p,
                        int E, int d, int I, hipStream_t st);
+// parts of expert u >= E read the shared experts' weights (w13s / w2s, u - E)
 hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
-                         int I, int E, int K, int budget, const void *w13,
+                         int I, int E, int K, int budget, int ns, const void *w13,
+                         const void *w13s,
                          const int32_t *sel_ids, const int32_t *n_sel,
                          const int32_t *offsets, const int32_t *pair_tok,
                          const PartRec *parts, const int32_t *n_parts,
                          const void *xp, void *H, hipStream_t st);
 hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K,
-                       int budget, const void *w2, const int32_t *sel_ids,
+                       int budget, int ns, const void *w2, const void *w2s,
+                       const int32_t *sel_ids,
                        const int32_t *n_sel, const int32_t *offsets,
                        const PartRec *parts, const int32_t *n_parts,
                        const float *pair_gate, const void *H, float *pairbuf,
                        hipStream_t st);
-hipError_t launch_combine(bool bf16, int B, int d, int K,
+// kc: columns of pair_of (K routed + the shared experts)
+hipError_t launch_combine(bool bf16, int B, int d, int kc,
                           const int32_t *pair_of, const float *pairbuf,
                           const void *residual, void *y, hipStream_t st);
 

@@ -353,10 +353,13 @@ void k_select_backfill(int B, int K, int E, const int32_t *__restrict__ ids,
 
 // Exclusive prefixes over slots s < n of cnt[s] (pairs), ceil(cnt[s] / 16)
 // (16-pair tiles) and ceil(cnt[s] / FFN_PART) (FFN parts), by one
-// wavefront in one pass (4 slots per lane); out[MAX_E] receives each total.
+// wavefront in one pass (SCAN_Q slots per lane); index SCAN_N receives each
+// total.
+constexpr int SCAN_Q = (MAX_SLOTS + WAVE - 1) / WAVE;
+constexpr int SCAN_N = SCAN_Q * WAVE;
 __device__ __forceinline__ void wave_scan3(const int *cnt, int n, int *off, int *tb, int *pb) {
   const int lane = lane_id();
-  constexpr int Q = MAX_E / WAVE;
+  constexpr int Q = SCAN_Q;
   int l0[Q], l1[Q], l2[Q];
   int s0 = 0, s1 = 0, s2 = 0;
 #pragma unroll
@@ -382,17 +385,22 @@ __device__ __forceinline__ void wave_scan3(const int *cnt, int n, int *off, int 
     off[s] = r0; tb[s] = r1; pb[s] = r2;
     r0 += l0[q]; r1 += l1[q]; r2 += l2[q];
   }
-  if (lane == WAVE - 1) { off[MAX_E] = i0; tb[MAX_E] = i1; pb[MAX_E] = i2; }
+  if (lane == WAVE - 1) { off[SCAN_N] = i0; tb[SCAN_N] = i1; pb[SCAN_N] = i2; }
 }
 
 constexpr int CP_THREADS = 1024;
 constexpr int CP_WORDS = MAX_B / 32;
 
+// One workgroup: counting sort of the executed (token, rank) pairs by (kept
+// slot, token), then ns shared slots (slot n_sel + i runs expert E + i for
+// every token in token order, gate sigmoid(gdot[t]) = 1 / (1 + exp(-s)) in
+// fp32, or 1); offsets, the pair lists, pair_of [B][K + ns] and the FFN's
+// part table.
 __global__ __launch_bounds__(CP_THREADS)
-void k_compact(int B, int K, int E, int budget, const int32_t *__restrict__ exec_ids,
+void k_compact(int B, int K, int E, int budget, int ns, const int32_t *__restrict__ exec_ids,
                const float *__restrict__ exec_gates,
                const int32_t *__restrict__ slot_of,
-               const int32_t *__restrict__ n_sel_p,
+               const int32_t *__restrict__ n_sel_p, const float *__restrict__ gdot,
                int32_t *__restrict__ offsets, int32_t *__restrict__ pair_tok,
                float *__restrict__ pair_gate, int32_t *__restrict__ pair_of,
                const int32_t *__restrict__ sel_ids, PartRec *__restrict__ parts,
@@ -400,17 +408,18 @@ void k_compact(int B, int K, int E, int budget, const int32_t *__restrict__ exec
   // bits[s][w]: bit (t & 31) of word w = t >> 5 is set when token t runs slot s
   __shared__ uint32_t bits[MAX_E * CP_WORDS];
   __shared__ int pre[MAX_E * CP_WORDS];
-  __shared__ int cnt[MAX_E];
-  __shared__ int off[MAX_E + 1];
-  __shared__ int tb[MAX_E + 1];
-  __shared__ int pb[MAX_E + 1];
+  __shared__ int cnt[SCAN_N];
+  __shared__ int off[SCAN_N + 1];
+  __shared__ int tb[SCAN_N + 1];
+  __shared__ int pb[SCAN_N + 1];
   __shared__ int sel_s[MAX_E];
   __shared__ int slot_s[MAX_E];
   const int tid = threadIdx.x, lane = lane_id();
   const int nwords = (B + 31) / 32;
   const int t = tid;
+  const int kc = K + ns;   // columns of pair_of
   // every independent load first: the token's executed experts and gates,
-  // the kept list, n_sel
+  // its shared-expert gate, the kept list, n_sel
   int u_of[MAX_K];
   float g_of[MAX_K];
 #pragma unroll
@@ -421,6 +430,12 @@ void k_compact(int B, int K, int E, int budget, const int32_t *__restrict__ exec
       u_of[j] = exec_ids[(size_t)t * K + j];
       g_of[j] = exec_gates[(size_t)t * K + j];
     }
+  }
+  float gs = 1.0f;
+  if (gdot && t < B) {
+    const float e = base_exp(-gdot[t]);
+    const float den = 1.0f + e;
+    gs = 1.0f / den;
   }
   if (tid < budget) sel_s[tid] = sel_ids[tid];
   if (tid < E) slot_s[tid] = slot_of[tid];
@@ -445,14 +460,15 @@ void k_compact(int B, int K, int E, int budget, const int32_t *__restrict__ exec
     }
     cnt[s] = run;
   }
+  for (int i = tid; i < ns; i += CP_THREADS) cnt[n_sel + i] = B;
   __syncthreads();
-  if (tid < WAVE) wave_scan3(cnt, n_sel, off, tb, pb);
+  if (tid < WAVE) wave_scan3(cnt, n_sel + ns, off, tb, pb);
   __syncthreads();
   // the FFN's part table: every part of slot s gets the slot's entry
-  for (int s = wave_id(); s < n_sel; s += CP_THREADS / WAVE) {
+  for (int s = wave_id(); s < n_sel + ns; s += CP_THREADS / WAVE) {
     const int np = pb[s + 1] - pb[s];
     PartRec r;
-    r.u = sel_s[s];
+    r.u = s < n_sel ? sel_s[s] : E + (s - n_sel);
     r.off = off[s];
     r.n = cnt[s];
     r.tile0 = tb[s];
@@ -461,10 +477,11 @@ void k_compact(int B, int K, int E, int budget, const int32_t *__restrict__ exec
     r.pad0 = r.pad1 = 0;
     for (int i = lane; i < np; i += WAVE) parts[pb[s] + i] = r;
   }
-  if (tid == 0) *n_parts = pb[MAX_E];
-  const int total = off[MAX_E];
+  if (tid == 0) *n_parts = pb[SCAN_N];
+  const int routed = off[n_sel];   // pairs of the kept slots
   for (int s = tid; s <= budget; s += CP_THREADS)
-    offsets[s] = (s < n_sel) ? off[s] : total;
+    offsets[s] = (s < n_sel) ? off[s] : routed;
+  for (int i = tid; i < ns; i += CP_THREADS) offsets[budget + 1 + i] = off[n_sel + i + 1];
   if (t < B) {
 #pragma unroll
     for (int j = 0; j < MAX_K; ++j) {
@@ -477,8 +494,14 @@ void k_compact(int B, int K, int E, int budget, const int32_t *__restrict__ exec
           pair_tok[p] = t;
           pair_gate[p] = g_of[j];
         }
-        pair_of[(size_t)t * K + j] = p;
+        pair_of[(size_t)t * kc + j] = p;
       }
+    }
+    for (int i = 0; i < ns; ++i) {
+      const int p = off[n_sel + i] + t;
+      pair_tok[p] = t;
+      pair_gate[p] = gs;
+      pair_of[(size_t)t * kc + K + i] = p;
     }
   }
 }
@@ -514,14 +537,14 @@ hipError_t launch_backfill(int B, int E, int K, int norm_topk, int flags,
   return hipGetLastError();
 }
 
-hipError_t launch_compact(int B, int K, int E, int budget, const int32_t *exec_ids,
+hipError_t launch_compact(int B, int K, int E, int budget, int ns, const int32_t *exec_ids,
                           const float *exec_gates, const int32_t *slot_of,
-                          const int32_t *n_sel, int32_t *offsets,
+                          const int32_t *n_sel, const float *gdot, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
                           int32_t *pair_of, const int32_t *sel_ids,
                           PartRec *parts, int32_t *n_parts, hipStream_t st) {
-  launch_k(k_compact, dim3(1), dim3(CP_THREADS), 0, st, B, K, E, budget,
-                     exec_ids, exec_gates, slot_of, n_sel, offsets, pair_tok,
+  launch_k(k_compact, dim3(1), dim3(CP_THREADS), 0, st, B, K, E, budget, ns,
+                     exec_ids, exec_gates, slot_of, n_sel, gdot, offsets, pair_tok,
                      pair_gate, pair_of, sel_ids, parts, n_parts);
   return hipGetLastError();
 }

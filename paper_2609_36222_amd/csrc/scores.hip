@@ -98,7 +98,8 @@ union ScLds {
 };
 
 // rows r < n_router: W_r (logits, + beta); n_router <= r < n_router + n_pred:
-// the predictor matrix A (q).  With ss != nullptr the wavefronts of row
+// the predictor matrix A (q); with G != nullptr one more row, the shared
+// experts' gate vector (gdot).  With ss != nullptr the wavefronts of row
 // tile 0 also produce ||x_t||^2.  A workgroup covers 16 tokens x 16 rows
 // (2 x 4 wavefronts of 8 x 4); each 256-element chunk of its rows is staged
 // once in LDS, the next chunk's loads in flight meanwhile.  Grid
@@ -108,13 +109,14 @@ __global__ __launch_bounds__(SC_WAVES * WAVE, 2)
 void k_scores(const XT *__restrict__ x, int B, int d,
               const float *__restrict__ Wr, const float *__restrict__ beta,
               int n_router, const float *__restrict__ A, int n_pred,
-              float *__restrict__ logits, float *__restrict__ q,
+              const float *__restrict__ G, float *__restrict__ logits,
+              float *__restrict__ q, float *__restrict__ gdot,
               float *__restrict__ ss) {
   using St = ScStage<XT>;
   __shared__ ScLds<XT> lds;
   const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
   const int tw = wv % SC_WT, rw = wv / SC_WT;
-  const int rows = n_router + n_pred;
+  const int rows = n_router + n_pred + (G ? 1 : 0);
   const int tb0 = blockIdx.x * SC_TB, rb0 = blockIdx.y * SC_RB;
   const bool do_ss = ss != nullptr && rb0 == 0 && rw == 0;
 
@@ -130,7 +132,9 @@ void k_scores(const XT *__restrict__ x, int B, int d,
   for (int i = 0; i < St::WP; ++i) {
     const int c = tid + i * SC_WAVES * WAVE;
     const int r = min(rb0 + c / St::WS, rows - 1);
-    wsrc[i] = (r < n_router ? Wr + (size_t)r * d : A + (size_t)(r - n_router) * d) +
+    wsrc[i] = (r < n_router            ? Wr + (size_t)r * d
+               : r < n_router + n_pred ? A + (size_t)(r - n_router) * d
+                                       : G) +
               (c % St::WS) * 4;
   }
   St st[SC_PF];
@@ -222,8 +226,10 @@ void k_scores(const XT *__restrict__ x, int B, int d,
     if (t < B && r < rows) {
       if (r < n_router)
         logits[(size_t)t * n_router + r] = beta ? v + beta[r] : v;
-      else
+      else if (r < n_router + n_pred)
         q[(size_t)t * n_pred + (r - n_router)] = v;
+      else
+        gdot[t] = v;
     }
   }
   if (do_ss && lane < SC_T) {
@@ -343,24 +349,24 @@ void k_tail(int B, int E, int K, int norm_topk, const float *__restrict__ logits
 template <typename XT>
 static void launch_scores_t(const XT *x, int B, int d, const float *Wr,
                             const float *beta, int n_router, const float *A,
-                            int n_pred, float *logits, float *q, float *ss,
-                            hipStream_t st) {
-  const int rows = n_router + n_pred;
+                            int n_pred, const float *G, float *logits, float *q,
+                            float *gdot, float *ss, hipStream_t st) {
+  const int rows = n_router + n_pred + (G ? 1 : 0);
   dim3 grid((B + SC_TB - 1) / SC_TB, (rows + SC_RB - 1) / SC_RB);
   launch_k(k_scores<XT>, grid, dim3(SC_WAVES * WAVE), 0, st, x, B, d,
-                     Wr, beta, n_router, A, n_pred, logits, q, ss);
+                     Wr, beta, n_router, A, n_pred, G, logits, q, gdot, ss);
 }
 
 hipError_t launch_scores(bool bf16, const void *x, int B, int d, const float *Wr,
                          const float *beta, int n_router, const float *A,
-                         int n_pred, float *logits, float *q, float *ss,
-                         hipStream_t st) {
+                         int n_pred, const float *G, float *logits, float *q,
+                         float *gdot, float *ss, hipStream_t st) {
   if (bf16)
     launch_scores_t((const uint16_t *)x, B, d, Wr, beta, n_router, A, n_pred,
-                    logits, q, ss, st);
+                    G, logits, q, gdot, ss, st);
   else
     launch_scores_t((const float *)x, B, d, Wr, beta, n_router, A, n_pred,
-                    logits, q, ss, st);
+                    G, logits, q, gdot, ss, st);
   return hipGetLastError();
 }
 

@@ -46,8 +46,15 @@ class GpuLayer:
             self.w13, self.w2 = dev_bf16(inp["w13"]), dev_bf16(inp["w2"])
         else:
             self.w13, self.w2 = dev_f32(inp["w13"]), dev_f32(inp["w2"])
+        self.shared = None
+        self.ns = 0
+        if inp.get("w13_shared") is not None:
+            g = inp.get("shared_gate")
+            self.shared = (dev_bf16(inp["w13_shared"]), dev_bf16(inp["w2_shared"]),
+                           None if g is None else dev_f32(g))
+            self.ns = int(inp["w13_shared"].shape[0])
         self.layer = bd.Layer(self.wr, self.br, self.pa, self.pb, self.w13,
-                              self.w2, norm_topk, score_rule=score_rule)
+                              self.w2, norm_topk, score_rule=score_rule, shared=self.shared)
         if packed:
             self.layer = bd.packed_layer(self.layer, sh.K)
         self.desc = self.layer.desc(sh.K)
@@ -88,8 +95,8 @@ class GpuLayer:
         return torch.empty(B, self.d, dtype=self.w13.dtype, device="cuda")
 
 
-def plan_arrays(plan, ws, B, K, E, budget, full):
-    """Copy the plan arrays out of the workspace (numpy)."""
+def plan_arrays(plan, ws, B, K, E, budget, full, ns=0):
+    """Copy the plan arrays out of the workspace (numpy); ns shared experts."""
     bc = min(budget, E)
     base = ws.data_ptr()
     wsb = ws.cpu().numpy()
@@ -104,8 +111,8 @@ def plan_arrays(plan, ws, B, K, E, budget, full):
     out = dict(
         exec_ids=arr("exec_ids", B * K, np.int32).reshape(B, K),
         exec_gates=arr("exec_gates", B * K, np.float32).reshape(B, K),
-        offsets=arr("offsets", bc + 1, np.int32),
-        pair_of=arr("pair_of", B * K, np.int32).reshape(B, K))
+        offsets=arr("offsets", bc + ns + 1, np.int32),
+        pair_of=arr("pair_of", B * (K + ns), np.int32).reshape(B, K + ns))
     P = int(out["offsets"][-1])
     out["pair_tok"] = arr("pair_tok", P, np.int32)
     out["pair_gate"] = arr("pair_gate", P, np.float32)

@@ -54,9 +54,13 @@ def oracle_layer(inp, budget, flags=0, norm_topk=1, residual=None,
                  with_y=True, score_rule=0):
     sh = inp["shape"]
     ex = method.Experts(inp["w13"], inp["w2"], sh.bf16) if with_y else None
+    shared = None
+    if inp.get("w13_shared") is not None:
+        shared = dict(experts=method.Experts(inp["w13_shared"], inp["w2_shared"], True),
+                      gate=inp.get("shared_gate"))
     return method.decode_layer_c(inp["x"], inp["w_router"], inp["b_router"],
                                  inp["pred_a"], inp["pred_b"], sh.K, budget,
-                                 ex, norm_topk, flags, residual, score_rule)
+                                 ex, norm_topk, flags, residual, score_rule, shared)
 
 
 def check_scoring(gl, inp, ref, B, budget, score_rule=0):
@@ -114,7 +118,7 @@ def run_case(gu, inp, budget, flags=0, norm_topk=1, with_residual=False,
     plan = bd.base_moe_forward(gl.desc, x, B, logits, ids, sel, nsel, slot,
                                budget, flags, res_d, y, ws)
     torch.cuda.synchronize()
-    got = gu.plan_arrays(plan, ws, B, sh.K, sh.E, budget, full=False)
+    got = gu.plan_arrays(plan, ws, B, sh.K, sh.E, budget, full=False, ns=gl.ns)
     check_plan(got, ref)
     y_staged = gu.to_np_f32(y)
     if check_y:
@@ -125,7 +129,7 @@ def run_case(gu, inp, budget, flags=0, norm_topk=1, with_residual=False,
     y2 = gl.y_like(B)
     plan2 = bd.base_decode_layer(gl.desc, x, B, budget, flags, res_d, y2, ws2)
     torch.cuda.synchronize()
-    got2 = gu.plan_arrays(plan2, ws2, B, sh.K, sh.E, budget, full=True)
+    got2 = gu.plan_arrays(plan2, ws2, B, sh.K, sh.E, budget, full=True, ns=gl.ns)
     check_plan(got2, ref)
     for f in ("logits", "topk_ids", "topk_w", "cost", "scores", "counts",
               "sel_ids", "slot_of_expert"):
@@ -177,6 +181,17 @@ def test_selection_rules(gu, name, budget, rule):
     scores, ranking, kept set and everything after it bit for bit with the
     oracle, fused == staged, packed == row-major."""
     run_case(gu, named(name), budget, score_rule=rule)
+
+
+@pytest.mark.parametrize("name,budget", [("deepseek_v2_lite", 8), ("deepseek_v2_lite", 32),
+                                         ("qwen15_moe", 8), ("qwen15_moe", 16)])
+def test_shared_experts(gu, name, budget):
+    """Layers with always-active shared experts (DeepSeek-V2-Lite- and
+    Qwen1.5-MoE-shaped, raw-softmax router weights; the latter's wide shared
+    expert given as 4 of the routed width behind a sigmoid gate): the
+    routed plan and the shared slots bit for bit, y in full."""
+    run_case(gu, named(name), budget, norm_topk=0)
+    run_case(gu, named(name), budget, norm_topk=0, flags=2, with_residual=True)
 
 
 @pytest.mark.parametrize("rule", [1, 4], ids=["top1", "static"])

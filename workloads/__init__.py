@@ -39,6 +39,7 @@ SEED_ROOT = 2609
 
 # stream ids inside a layer's seed sequence
 _S_ROUTER, _S_BIAS, _S_CALIB, _S_EXPERT, _S_TOKENS, _S_PRED = 0, 1, 2, 3, 4, 5
+_S_SHARED, _S_SHARED_GATE = 6, 7
 
 
 @dataclasses.dataclass(frozen=True)
@@ -59,6 +60,9 @@ class LayerShape:
     bias_std: float = 0.5
     rmsnorm: bool = True
     calib_tokens: int = 8192
+    norm_topk: int = 1      # 1: top-K weights renormalised; 0: raw softmax
+    n_shared: int = 0       # always-active shared experts (the routed shape)
+    shared_gate: bool = False   # sigmoid gate on the shared experts' sum
 
 
 WORKLOADS = {
@@ -81,6 +85,15 @@ WORKLOADS = {
                                 (24,), True, layers=48),
     # Mixtral-shaped: few large experts.
     "mixtral": LayerShape("mixtral", 5, 4096, 8, 2, 14336, 128, (4,), True),
+    # DeepSeek-V2-Lite-shaped: 64 routed experts, top-6, I=1408, raw softmax
+    # weights, 2 shared experts without a gate.
+    "deepseek_v2_lite": LayerShape("deepseek_v2_lite", 6, 2048, 64, 6, 1408, 64,
+                                   (8, 16, 32), True, norm_topk=0, n_shared=2),
+    # Qwen1.5-MoE-A2.7B-shaped: 60 routed experts, top-4, I=1408, raw softmax
+    # weights, one shared expert of intermediate size 5632 given as 4 of
+    # width 1408, with a sigmoid gate.
+    "qwen15_moe": LayerShape("qwen15_moe", 7, 2048, 60, 4, 1408, 64, (8, 16), True,
+                             norm_topk=0, n_shared=4, shared_gate=True),
 }
 
 
@@ -200,6 +213,22 @@ def experts(shape: LayerShape, layer: int = 0):
     return w13.reshape(E, 2 * I, d), w2.reshape(E, d, I)
 
 
+def shared_experts(shape: LayerShape, layer: int = 0):
+    """The shared experts, with the routed experts' recipe and shape:
+    (w13 [S, 2I, d], w2 [S, d, I]) as bf16 bits, and the gate vector [d]
+    fp32 (N(0, 1/d), so x . gate is about N(0, 1)) or None."""
+    S, d, I = shape.n_shared, shape.d, shape.I
+    ss = seed_seq(shape, layer, _S_SHARED)
+    s13, s2 = ss.spawn(2)
+    w13 = _normal_chunked(s13, S * 2 * I * d, 1.0 / np.sqrt(d), bf16=shape.bf16)
+    w2 = _normal_chunked(s2, S * d * I, 1.0 / np.sqrt(I), bf16=shape.bf16)
+    gate = None
+    if shape.shared_gate:
+        g = np.random.Generator(np.random.PCG64(seed_seq(shape, layer, _S_SHARED_GATE)))
+        gate = (g.standard_normal(d) / np.sqrt(d)).astype(np.float32)
+    return w13.reshape(S, 2 * I, d), w2.reshape(S, d, I), gate
+
+
 def synthetic_predictor(shape: LayerShape, layer: int = 0):
     """A synthetic log-energy predictor (a [E,d] fp32, b [E] fp32).
 
@@ -250,6 +279,8 @@ def layer_inputs(name: str, layer: int = 0, data_seed: int = 0,
     out["pred_a"], out["pred_b"] = pa, pb
     if with_experts:
         out["w13"], out["w2"] = experts(shape, layer)
+        if shape.n_shared:
+            out["w13_shared"], out["w2_shared"], out["shared_gate"] = shared_experts(shape, layer)
     return out
 
 
