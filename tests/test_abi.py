@@ -49,12 +49,14 @@ def test_exported_symbols_in_dynamic_table(lib):
 def layer(**kw):
     v = dict(d=2048, E=128, K=8, I=768, dtype=1, norm_topk=1, w_layout=0,
              score_rule=0, w_router=FAKE, b_router=FAKE, pred_a=FAKE, pred_b=FAKE,
-             w13=FAKE, w2=FAKE)
+             w13=FAKE, w2=FAKE, n_shared=0, w13_shared=None, w2_shared=None,
+             shared_gate=None)
     v.update(kw)
     return bd.base_layer(v["d"], v["E"], v["K"], v["I"], v["dtype"],
                          v["norm_topk"], v["w_layout"], v["score_rule"], v["w_router"],
                          v["b_router"], v["pred_a"], v["pred_b"], v["w13"],
-                         v["w2"])
+                         v["w2"], v["n_shared"], v["w13_shared"], v["w2_shared"],
+                         v["shared_gate"])
 
 
 def route(lib, L, x=FAKE, B=16, lg=FAKE, ids=FAKE, w=FAKE):
@@ -165,6 +167,25 @@ def test_score_rules_read_only_their_parameters(lib):
     assert lib.base_predict_cost(ctypes.byref(L), FAKE, 4, FAKE, FAKE, 0, None) == NULL
     assert lib.base_predict_cost(ctypes.byref(layer(score_rule=9)), FAKE, 4, FAKE, FAKE,
                                  FAKE, None) == FLAGS
+
+
+def test_shared_expert_validation(lib):
+    """Shared experts: at most 8, bf16 layers only, their weights required
+    (and 16-B aligned) where the experts are read, the gate 16-B aligned;
+    they enlarge the workspace."""
+    sh = dict(w13_shared=FAKE, w2_shared=FAKE)
+    assert route(lib, layer(n_shared=9, **sh)) == SHAPE
+    assert route(lib, layer(n_shared=-1, **sh)) == SHAPE
+    assert route(lib, layer(n_shared=1, dtype=0, **sh)) == DTYPE
+    assert route(lib, layer(n_shared=1, shared_gate=FAKE + 4, **sh)) == ALIGN
+    assert decode(lib, layer(n_shared=2, w13_shared=None, w2_shared=FAKE)) == NULL
+    assert decode(lib, layer(n_shared=2, w13_shared=FAKE + 8, w2_shared=FAKE)) == ALIGN
+    a = lib.base_workspace_bytes(ctypes.byref(layer()), 64, 16)
+    b = lib.base_workspace_bytes(ctypes.byref(layer(n_shared=2, **sh)), 64, 16)
+    assert b > a
+    # packing shared experts: a descriptor with E = n_shared (K not read)
+    P = layer(E=2, K=8, n_shared=0)
+    assert lib.base_pack_experts(ctypes.byref(P), 0, FAKE, None) == NULL
 
 
 def test_workspace_grows_with_shape_and_clamps_budget(lib):
