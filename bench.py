@@ -80,6 +80,10 @@ def parse_args():
     p.add_argument("--sweep-steps", type=int, default=100)
     p.add_argument("--no-ceiling", action="store_true",
                    help="skip the streaming-read ceiling probe")
+    p.add_argument("--calibrate", action="store_true",
+                   help="only time the predictor's calibration on the workload's layer")
+    p.add_argument("--calib-tokens", type=int, default=8192)
+    p.add_argument("--calib-batch", type=int, default=1024)
     p.add_argument("--working-set-probe", action="store_true",
                    help="only measure the streaming-read rate by working-set size")
     p.add_argument("--copy-probe", action="store_true",
@@ -281,6 +285,74 @@ def cpu_baseline(inp, budget, seconds):
                        "scoring in C (1 thread) + fp64 NumPy/BLAS expert FFN")
 
 
+def bench_calibrate(args, shape, np, torch, W, bd):
+    """Calibration of one layer's predictor on the device (App. A): the
+    streaming statistics over --calib-tokens calibration hidden states in
+    batches of --calib-batch (every routed expert run on its tokens, the
+    moments and the fp32 Gram matrices updated), then the fit (one fp64
+    eigendecomposition per expert, 25 lambdas).  The oracle's statistics
+    are timed on a bounded sample of the same tokens."""
+    from oracle import calib
+    dev = torch.device("cuda", 0)
+    inp = W.layer_inputs(args.workload)
+
+    def f32(a):
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+
+    def bits(b):
+        return torch.from_numpy(np.ascontiguousarray(b).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    wdev = (bits(inp["w13"]), bits(inp["w2"])) if shape.bf16 else (f32(inp["w13"]), f32(inp["w2"]))
+    lay = bd.Layer(f32(inp["w_router"]), f32(inp["b_router"]), f32(inp["pred_a"]),
+                   f32(inp["pred_b"]), *wdev, norm_topk=shape.norm_topk)
+    if shape.bf16:
+        lay = bd.packed_layer(lay, shape.K)
+    desc = lay.desc(shape.K)
+    z = W.calibration_tokens(shape, n=args.calib_tokens)
+    zd = bits((z.view(np.uint32) >> 16).astype(np.uint16)) if shape.bf16 else f32(z)
+    nb = args.calib_batch
+    stats = bd.calib_stats(desc)
+    ws = bd.calib_accumulate(desc, zd[:nb], min(nb, len(z)), stats)   # warm-up
+    stats = bd.calib_stats(desc)
+    hip = hip_runtime()
+    sptr = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    t0, t1 = new_event(hip), new_event(hip)
+    torch.cuda.synchronize()
+    hip.hipEventRecord(t0, sptr)
+    for lo in range(0, len(z), nb):
+        n = min(nb, len(z) - lo)
+        bd.calib_accumulate(desc, zd[lo:lo + n], n, stats, ws)
+    hip.hipEventRecord(t1, sptr)
+    torch.cuda.synchronize()
+    acc_ms = elapsed_ms(hip, t0, t1)
+    pa = torch.empty(shape.E, shape.d, dtype=torch.float32, device=dev)
+    pb = torch.empty(shape.E, dtype=torch.float32, device=dev)
+    w0 = time.perf_counter()
+    bd.calib_fit(desc, stats, calib.LAMBDAS, pa, pb)
+    fit_s = time.perf_counter() - w0
+    out = {"metric": "predictor calibration (App. A) on one layer",
+           "value": round(len(z) / (acc_ms * 1e-3), 1), "unit": "calibration tokens/s",
+           "higher_is_better": True, "n_gpus": 1, "data": "synthetic",
+           "config": {"workload": f"{args.workload}: d={shape.d} E={shape.E} top-{shape.K} "
+                                  f"I={shape.I}", "calib_tokens": len(z), "batch": nb},
+           "statistics_ms": round(acc_ms, 2), "fit_s": round(fit_s, 3),
+           "gram_bytes": shape.E * shape.d * shape.d * 4}
+    if not args.no_cpu_baseline:
+        ex = __import__("oracle.method", fromlist=["method"]).Experts(inp["w13"], inp["w2"],
+                                                                       shape.bf16)
+        n, w0 = 0, time.perf_counter()
+        while time.perf_counter() - w0 < args.cpu_seconds and n < len(z):
+            calib.collect_stats(z[n:n + 64], inp["w_router"], inp["b_router"], shape.K, ex,
+                                shape.norm_topk, batch=64)
+            n += 64
+        dt = time.perf_counter() - w0
+        out["cpu_baseline"] = dict(value=round(n / dt, 1), unit="calibration tokens/s",
+                                   cores=blas_threads(), kind="oracle",
+                                   sample=f"{n} calibration tokens through the oracle's "
+                                          "streaming statistics (fp64 experts), batches of 64")
+    print(json.dumps(out), flush=True)
+
+
 def bench_stack(args, shape, np, torch, W, bd):
     """One step = the whole stack of MoE layers (48 Qwen3-shaped layers at
     batch 128, B_e = 24 each), every layer's experts resident and distinct.
@@ -466,6 +538,9 @@ def main():
     shape = W.WORKLOADS[args.workload]
     if args.budget is None:
         args.budget = shape.budgets[0]
+    if args.calibrate:
+        bench_calibrate(args, shape, np, torch, W, bd)
+        return
     if shape.layers > 1:
         bench_stack(args, shape, np, torch, W, bd)
         return

@@ -284,6 +284,32 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
 base_status base_pack_experts(const base_layer *L, void *w13_packed,
                               void *w2_packed, void *stream);
 
+/* Calibration statistics of the predictor (Sec. 3.4; App. A "Calibration
+ * Details"), accumulated batch by batch on the device; the fit is
+ * base_calib_fit (base_calib.h).  For a batch z [B][d] (L->dtype) of
+ * calibration hidden states, every routed pair (t, u) (router top-K of
+ * L's router) gets the target y = log(||E_u(z_t)||^2 + 1e-12), the expert's
+ * own output (the layer's FFN with every routed expert kept, gate 1), and
+ * z_bar = z_t / ||z_t|| (fp64); per expert u the statistics add
+ *   n_u, sum y, sum y^2                (fp64),
+ *   sum z_bar [d], sum z_bar y [d]     (fp64),
+ *   G_u = sum z_bar z_bar^T [d][d]     (fp32 products and sums per batch).
+ * Layout of `stats` (device, 256-B aligned, base_calib_stats_bytes(L)
+ * bytes; each array starts on a 256-byte boundary, in this order):
+ *   double head[E][4] (n, sum y, sum y^2, unused); double sz[E][d];
+ *   double q[E][d]; float G[E][d][d].
+ * Every statistic has one writer and a fixed order: results are
+ * deterministic.  Shared experts and score_rule are not used.
+ * base_calib_reset zeroes the statistics; base_calib_accumulate needs a
+ * workspace of base_calib_ws_bytes(L, B) bytes (256-B aligned).  Both only
+ * enqueue work, like every call here. */
+size_t base_calib_stats_bytes(const base_layer *L);
+size_t base_calib_ws_bytes(const base_layer *L, int32_t B);
+base_status base_calib_reset(const base_layer *L, void *stats, void *stream);
+base_status base_calib_accumulate(const base_layer *L, const void *z, int32_t B,
+                                  void *stats, void *ws, size_t ws_bytes,
+                                  void *stream);
+
 /* Kernel timing for profiling.  `events` holds 2 * BASE_N_STAGES hipEvent_t
  * handles created by the caller (hipEventCreate), or is NULL to switch
  * timing off (n_events is then ignored).  While set, the calls that run a

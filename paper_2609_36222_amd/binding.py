@@ -22,7 +22,10 @@ SCORE_BASE, SCORE_TOP1, SCORE_WEIGHT, SCORE_WEIGHT_SQ, SCORE_STATIC = 0, 1, 2, 3
 
 EXPORTS = ("base_workspace_bytes", "base_route", "base_predict_cost",
            "base_select", "base_moe_forward", "base_decode_layer",
-           "base_pack_experts", "base_set_stage_events", "base_status_string")
+           "base_pack_experts", "base_set_stage_events", "base_status_string",
+           "base_calib_stats_bytes", "base_calib_ws_bytes", "base_calib_reset",
+           "base_calib_accumulate")
+CALIB_LIB_PATH = os.path.join(HERE, "_lib", "libbase_calib.so")
 N_STAGES = 9     # one kernel each; base_set_stage_events takes 2 events per stage
 STAGES = ("scores", "tail", "select", "backfill", "compact", "gather",
           "ffn_gateup", "ffn_down", "combine")
@@ -98,7 +101,36 @@ def load(path: str = LIB_PATH):
     L.base_set_stage_events.argtypes = [ctypes.POINTER(ctypes.c_void_p), _i32]
     L.base_status_string.restype = ctypes.c_char_p
     L.base_status_string.argtypes = [_i32]
+    L.base_calib_stats_bytes.restype = ctypes.c_size_t
+    L.base_calib_stats_bytes.argtypes = [ctypes.POINTER(base_layer)]
+    L.base_calib_ws_bytes.restype = ctypes.c_size_t
+    L.base_calib_ws_bytes.argtypes = [ctypes.POINTER(base_layer), _i32]
+    L.base_calib_reset.restype = _i32
+    L.base_calib_reset.argtypes = [ctypes.POINTER(base_layer), _vp, _vp]
+    L.base_calib_accumulate.restype = _i32
+    L.base_calib_accumulate.argtypes = [ctypes.POINTER(base_layer), _vp, _i32, _vp, _vp,
+                                        ctypes.c_size_t, _vp]
     _lib = L
+    return L
+
+
+_calib = None
+
+
+def load_calib(path: str = CALIB_LIB_PATH):
+    """Load libbase_calib.so (the predictor fit, base_calib.h)."""
+    global _calib
+    if _calib is not None:
+        return _calib
+    load()
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with "
+                          "`python -m paper_2609_36222_amd.build`")
+    L = ctypes.CDLL(path)
+    L.base_calib_fit.restype = _i32
+    L.base_calib_fit.argtypes = [ctypes.POINTER(base_layer), _vp, _i32,
+                                 ctypes.POINTER(ctypes.c_double), _vp, _vp, _vp, _vp]
+    _calib = L
     return L
 
 
@@ -246,6 +278,37 @@ def base_set_stage_events(events):
     arr = (ctypes.c_void_p * len(events))(*events)
     _check(load().base_set_stage_events(arr, len(events)))
     return arr   # keep alive while timing is on
+
+
+def calib_stats(desc: base_layer):
+    """A zeroed statistics buffer (torch uint8 tensor on the device)."""
+    import torch
+    n = int(load().base_calib_stats_bytes(ctypes.byref(desc)))
+    if n == 0:
+        raise BaseError(-2, "shape outside the supported limits")
+    stats = torch.empty(n, dtype=torch.uint8, device="cuda")
+    _check(load().base_calib_reset(ctypes.byref(desc), _ptr(stats), _stream(None)))
+    return stats
+
+
+def calib_accumulate(desc, z, B, stats, ws=None, stream=None):
+    """Adds one batch of calibration hidden states z [B, d] to stats."""
+    import torch
+    if ws is None:
+        ws = torch.empty(int(load().base_calib_ws_bytes(ctypes.byref(desc), B)),
+                         dtype=torch.uint8, device="cuda")
+    _check(load().base_calib_accumulate(ctypes.byref(desc), _ptr(z), B, _ptr(stats),
+                                        _ptr(ws), ws.numel(), _stream(stream)))
+    return ws
+
+
+def calib_fit(desc, stats, lambdas, pred_a, pred_b, lam_out=None, stream=None):
+    """pred_a [E, d], pred_b [E] (fp32 device tensors) from the statistics;
+    lambdas: a sequence of positive floats (host)."""
+    lam = (ctypes.c_double * len(lambdas))(*[float(v) for v in lambdas])
+    _check(load_calib().base_calib_fit(ctypes.byref(desc), _ptr(stats), len(lambdas), lam,
+                                       _ptr(pred_a), _ptr(pred_b), _ptr(lam_out),
+                                       _stream(stream)))
 
 
 def plan_offset(plan: base_plan, field: str, ws) -> int:

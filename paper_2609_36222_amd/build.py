@@ -21,8 +21,9 @@ CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_lib")
 LIB = os.path.join(OUT_DIR, "libbase.so")
 PROBE_LIB = os.path.join(OUT_DIR, "libbase_probe.so")   # bench's streaming-read probe
+CALIB_LIB = os.path.join(OUT_DIR, "libbase_calib.so")   # predictor fit (links rocSOLVER)
 SOURCES = ["api.hip", "scores.hip", "route_predict.hip", "plan.hip", "ffn.hip",
-           "pack.hip"]
+           "pack.hip", "calib.hip"]
 ARCH = os.environ.get("BASE_OFFLOAD_ARCH", "gfx950")
 
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
@@ -38,9 +39,9 @@ def _hipcc():
     raise RuntimeError("hipcc not found")
 
 
-def _link(objs, out):
+def _link(objs, out, libs=()):
     tmp = out + ".tmp%d" % os.getpid()
-    cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+    cmd = [_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp, *libs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
@@ -64,10 +65,11 @@ def build(verbose: bool = False) -> str:
             print(r.stderr, file=sys.stderr)
         return obj
 
-    with cf.ThreadPoolExecutor(min(8, len(SOURCES) + 1)) as ex:
-        objs = list(ex.map(compile_one, SOURCES + ["probe.hip"]))
-    _link(objs[:-1], LIB)
-    _link(objs[-1:], PROBE_LIB)
+    with cf.ThreadPoolExecutor(min(8, len(SOURCES) + 2)) as ex:
+        objs = list(ex.map(compile_one, SOURCES + ["probe.hip", "calib_fit.hip"]))
+    _link(objs[:-2], LIB)
+    _link(objs[-2:-1], PROBE_LIB)
+    _link(objs[-1:], CALIB_LIB, ["-lrocsolver", "-lrocblas"])
     for o in objs:
         os.remove(o)
     return LIB

@@ -12,6 +12,10 @@ namespace {
 
 using namespace basek;
 
+constexpr int FILL_DROP_BIT = BASE_FILL_DROP;
+static_assert(FLAG_UNIT_GATES != BASE_GATE_RENORM && FLAG_UNIT_GATES != BASE_FILL_DROP,
+              "internal flag bit");
+
 static_assert(SCORE_BASE == BASE_SCORE_BASE && SCORE_TOP1 == BASE_SCORE_TOP1 &&
                   SCORE_WEIGHT == BASE_SCORE_WEIGHT && SCORE_WEIGHT_SQ == BASE_SCORE_WEIGHT_SQ &&
                   SCORE_STATIC == BASE_SCORE_STATIC,
@@ -393,6 +397,91 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
   BASE_TRY(run_forward(L, x, B, logits, ids, sel, nsel, slot, bc, flags,
                        residual, y, ws, o, st, true));
   fill_plan(plan_out, ws, o, true);
+  return BASE_OK;
+}
+
+// ------------------------------------------------------------ calibration --
+size_t base_calib_stats_bytes(const base_layer *L) {
+  if (!L || L->E < 1 || L->E > MAX_E || L->d < 256 || L->d > 16384 || L->d % 256) return 0;
+  return calib_stats_bytes(L->E, L->d);
+}
+
+// the routed layer the calibration runs (no shared experts, its own rule)
+static base_layer calib_layer(const base_layer *L) {
+  base_layer C = *L;
+  C.n_shared = 0;
+  C.score_rule = BASE_SCORE_WEIGHT;
+  return C;
+}
+
+size_t base_calib_ws_bytes(const base_layer *L, int32_t B) {
+  if (!L) return 0;
+  const base_layer C = calib_layer(L);
+  if (check_layer(&C, B, false, false, false) != BASE_OK) return 0;
+  return layout(&C, B, C.E).total + up256((size_t)B * 8) + up256((size_t)B * C.K * 8);
+}
+
+base_status base_calib_reset(const base_layer *L, void *stats, void *stream) {
+  const size_t n = base_calib_stats_bytes(L);
+  if (n == 0) return BASE_ERR_SHAPE;
+  BASE_TRY(check_ptr(stats, 256));
+  HIP_TRY(launch_calib_zero(stats, n, (hipStream_t)stream));
+  return BASE_OK;
+}
+
+base_status base_calib_accumulate(const base_layer *L, const void *z, int32_t B, void *stats,
+                                  void *ws, size_t ws_bytes, void *stream) {
+  if (!L) return BASE_ERR_NULL;
+  const base_layer C = calib_layer(L);
+  BASE_TRY(check_layer(&C, B, true, false, true));
+  BASE_TRY(check_ptr(z, 16));
+  BASE_TRY(check_ptr(stats, 256));
+  if (!ws) return BASE_ERR_NULL;
+  if (!aligned(ws, 256)) return BASE_ERR_ALIGN;
+  if (ws_bytes < base_calib_ws_bytes(L, B)) return BASE_ERR_WORKSPACE;
+  const int32_t bc = C.E;   // keep every routed expert
+  const Layout o = layout(&C, B, bc);
+  hipStream_t st = (hipStream_t)stream;
+  const bool bf16 = C.dtype == BASE_BF16;
+  float *logits = at<float>(ws, o.logits);
+  int32_t *ids = at<int32_t>(ws, o.topk_ids);
+  float *w = at<float>(ws, o.topk_w);
+  int32_t *sel = at<int32_t>(ws, o.sel_ids);
+  int32_t *nsel = at<int32_t>(ws, o.n_sel);
+  int32_t *slot = at<int32_t>(ws, o.slot_of);
+  HIP_TRY(launch_scores(bf16, z, B, C.d, C.w_router, C.b_router, C.E, nullptr, 0, nullptr,
+                        logits, nullptr, nullptr, nullptr, st));
+  HIP_TRY(launch_tail(B, C.E, C.K, C.norm_topk, logits, nullptr, nullptr, nullptr, ids, w,
+                      nullptr, 1, BASE_SCORE_BASE, st));
+  // the budget E keeps the whole batch union (any positive scores do)
+  HIP_TRY(launch_select(B, C.K, C.E, ids, w, bc, false, at<float>(ws, o.scores),
+                        at<int32_t>(ws, o.counts), sel, nsel, slot, st));
+  // every routed expert executed, with gate 1: the FFN writes E_u(z_t)
+  HIP_TRY(launch_backfill(B, C.E, C.K, C.norm_topk, FILL_DROP_BIT | FLAG_UNIT_GATES, logits,
+                          ids, slot, nsel, at<int32_t>(ws, o.exec_ids),
+                          at<float>(ws, o.exec_gates), st));
+  int32_t *offsets = at<int32_t>(ws, o.offsets);
+  int32_t *pair_tok = at<int32_t>(ws, o.pair_tok);
+  PartRec *parts = at<PartRec>(ws, o.parts);
+  int32_t *n_parts = at<int32_t>(ws, o.n_parts);
+  HIP_TRY(launch_compact(B, C.K, C.E, bc, 0, at<int32_t>(ws, o.exec_ids),
+                         at<float>(ws, o.exec_gates), slot, nsel, nullptr, offsets, pair_tok,
+                         at<float>(ws, o.pair_gate), at<int32_t>(ws, o.pair_of), sel, parts,
+                         n_parts, st));
+  if (bf16)
+    HIP_TRY(launch_gather(z, B, C.d, ffn_max_parts(B, C.K, bc, 0), parts, n_parts, pair_tok,
+                          at<void>(ws, o.xp), st));
+  const bool packed = C.w_layout == BASE_W_PACKED;
+  HIP_TRY(launch_gateup(bf16, packed, z, B, C.d, C.I, C.E, C.K, bc, 0, C.w13, nullptr, sel,
+                        nsel, offsets, pair_tok, parts, n_parts, at<void>(ws, o.xp),
+                        at<void>(ws, o.H), st));
+  HIP_TRY(launch_down(bf16, packed, B, C.d, C.I, C.E, C.K, bc, 0, C.w2, nullptr, sel, nsel,
+                      offsets, parts, n_parts, at<float>(ws, o.pair_gate), at<void>(ws, o.H),
+                      at<float>(ws, o.pairbuf), st));
+  double *inv = at<double>(ws, o.total);
+  double *y = at<double>(ws, o.total + up256((size_t)B * 8));
+  HIP_TRY(launch_calib_stats(z, bf16, B, C.d, C.E, C.K, at<float>(ws, o.pairbuf), nsel, sel,
+                             offsets, pair_tok, inv, y, calib_stats_at(stats, C.E, C.d), st));
   return BASE_OK;
 }
 

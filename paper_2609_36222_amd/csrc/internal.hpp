@@ -131,4 +131,39 @@ hipError_t launch_combine(bool bf16, int B, int d, int kc,
                           const int32_t *pair_of, const float *pairbuf,
                           const void *residual, void *y, hipStream_t st);
 
+// Calibration statistics (per expert u): head[u] = (n, sum y, sum y^2, 0)
+// fp64, sz[u][d] and q[u][d] fp64, G[u][d][d] fp32; each array 256-byte
+// aligned in the caller's buffer, in this order.
+struct CalibStats {
+  double *head, *sz, *q;
+  float *G;
+};
+inline size_t calib_up256(size_t v) { return (v + 255) & ~(size_t)255; }
+inline size_t calib_stats_bytes(int E, int d) {
+  return calib_up256((size_t)E * 4 * 8) + 2 * calib_up256((size_t)E * d * 8) +
+         calib_up256((size_t)E * d * d * 4);
+}
+inline CalibStats calib_stats_at(void *base, int E, int d) {
+  char *p = static_cast<char *>(base);
+  CalibStats s;
+  s.head = reinterpret_cast<double *>(p);
+  p += calib_up256((size_t)E * 4 * 8);
+  s.sz = reinterpret_cast<double *>(p);
+  p += calib_up256((size_t)E * d * 8);
+  s.q = reinterpret_cast<double *>(p);
+  p += calib_up256((size_t)E * d * 8);
+  s.G = reinterpret_cast<float *>(p);
+  return s;
+}
+hipError_t launch_calib_zero(void *stats, size_t bytes, hipStream_t st);
+hipError_t launch_calib_stats(const void *x, bool bf16, int B, int d, int E, int K,
+                              const float *pairbuf, const int32_t *n_sel,
+                              const int32_t *sel_ids, const int32_t *offsets,
+                              const int32_t *pair_tok, double *inv, double *y,
+                              CalibStats st, hipStream_t s);
+
+// internal flags bit of the backfill: unit gates (calibration runs the
+// experts' own outputs)
+constexpr int FLAG_UNIT_GATES = 4;
+
 }  // namespace basek

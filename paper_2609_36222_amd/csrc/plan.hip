@@ -286,7 +286,8 @@ __device__ __forceinline__ void backfill_body(BfLds<W> &S, bool active, int t, i
   }
   if (t < B && lane < K) {
     exec_ids[(size_t)t * K + lane] = (lane < nx) ? S.xs[wv][lane] : -1;
-    exec_gates[(size_t)t * K + lane] = (lane < nx) ? num / Ssum : 0.0f;
+    exec_gates[(size_t)t * K + lane] =
+        (lane < nx) ? ((flags & FLAG_UNIT_GATES) ? 1.0f : num / Ssum) : 0.0f;
   }
 }
 

@@ -244,3 +244,34 @@ def test_stream_read_probe_library():
     assert f(None, 8, 16, 0, FAKE, None, None, None) == 1      # no buffer
     assert f(FAKE, 8, 16, 0, None, None, None, None) == 1      # no sink
     assert f(FAKE, 8, 1 << 19, 0, FAKE, None, None, None) == 1  # share of 2 GiB
+
+
+def test_calibration_validation(lib):
+    """Calibration statistics: size of the documented layout, and host-side
+    refusals before anything is enqueued (the fit library's too)."""
+    L = layer(d=256, E=16, K=2, I=512, dtype=0)
+    up = lambda v: (v + 255) // 256 * 256
+    assert lib.base_calib_stats_bytes(ctypes.byref(L)) == \
+        up(16 * 4 * 8) + 2 * up(16 * 256 * 8) + up(16 * 256 * 256 * 4)
+    assert lib.base_calib_stats_bytes(ctypes.byref(layer(d=300))) == 0
+    assert lib.base_calib_ws_bytes(ctypes.byref(L), 64) > lib.base_workspace_bytes(ctypes.byref(L), 64, 16)
+    assert lib.base_calib_reset(ctypes.byref(L), None, None) == NULL
+    assert lib.base_calib_reset(ctypes.byref(L), FAKE + 64, None) == ALIGN
+    nb = lib.base_calib_ws_bytes(ctypes.byref(L), 64)
+    acc = lambda **k: lib.base_calib_accumulate(
+        ctypes.byref(k.get("L", L)), k.get("z", FAKE), 64, k.get("st", FAKE), k.get("ws", FAKE),
+        k.get("n", nb), None)
+    assert acc(z=0) == NULL
+    assert acc(st=FAKE + 8) == ALIGN
+    assert acc(n=nb - 1) == WS
+    assert acc(L=layer(d=256, E=16, K=2, I=512, dtype=0, w_router=0)) == NULL
+    cal = bd.load_calib()
+    lam = (ctypes.c_double * 3)(1e-3, 1e-1, 1.0)
+    fit = lambda **k: cal.base_calib_fit(ctypes.byref(L), k.get("st", FAKE), k.get("n", 3),
+                                         k.get("lam", lam), k.get("a", FAKE), FAKE, None, None)
+    assert fit(st=None) == NULL
+    assert fit(n=0) == SHAPE
+    assert fit(n=65) == SHAPE
+    assert fit(lam=(ctypes.c_double * 3)(1e-3, 0.0, 1.0)) == SHAPE
+    assert fit(st=FAKE + 8) == ALIGN
+    assert fit(a=FAKE + 2) == ALIGN
