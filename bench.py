@@ -292,7 +292,6 @@ def bench_calibrate(args, shape, np, torch, W, bd):
     moments and the fp32 Gram matrices updated), then the fit (one fp64
     eigendecomposition per expert, 25 lambdas).  The oracle's statistics
     are timed on a bounded sample of the same tokens."""
-    from oracle import calib
     dev = torch.device("cuda", 0)
     inp = W.layer_inputs(args.workload)
 
@@ -328,7 +327,7 @@ def bench_calibrate(args, shape, np, torch, W, bd):
     pa = torch.empty(shape.E, shape.d, dtype=torch.float32, device=dev)
     pb = torch.empty(shape.E, dtype=torch.float32, device=dev)
     w0 = time.perf_counter()
-    bd.calib_fit(desc, stats, calib.LAMBDAS, pa, pb)
+    bd.calib_fit(desc, stats, bd.CALIB_LAMBDAS, pa, pb)
     fit_s = time.perf_counter() - w0
     out = {"metric": "predictor calibration (App. A) on one layer",
            "value": round(len(z) / (acc_ms * 1e-3), 1), "unit": "calibration tokens/s",
@@ -338,8 +337,8 @@ def bench_calibrate(args, shape, np, torch, W, bd):
            "statistics_ms": round(acc_ms, 2), "fit_s": round(fit_s, 3),
            "gram_bytes": shape.E * shape.d * shape.d * 4}
     if not args.no_cpu_baseline:
-        ex = __import__("oracle.method", fromlist=["method"]).Experts(inp["w13"], inp["w2"],
-                                                                       shape.bf16)
+        from oracle import calib, method
+        ex = method.Experts(inp["w13"], inp["w2"], shape.bf16)
         n, w0 = 0, time.perf_counter()
         while time.perf_counter() - w0 < args.cpu_seconds and n < len(z):
             calib.collect_stats(z[n:n + 64], inp["w_router"], inp["b_router"], shape.K, ex,

@@ -280,6 +280,10 @@ def base_set_stage_events(events):
     return arr   # keep alive while timing is on
 
 
+# App. A: the ridge's lambdas, 25 values log-spaced over [1e-4, 1e2]
+CALIB_LAMBDAS = tuple(10.0 ** (-4.0 + 6.0 * i / 24) for i in range(25))
+
+
 def calib_stats(desc: base_layer):
     """A zeroed statistics buffer (torch uint8 tensor on the device)."""
     import torch

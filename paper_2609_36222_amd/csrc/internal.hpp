@@ -61,8 +61,6 @@ struct alignas(32) PartRec {
   int32_t u, off, n, tile0, part0, parts, pad0, pad1;
 };
 
-// rows: n_router of W_r (-> logits [B][n_router], + beta) then n_pred of A
-// (-> q [B][n_pred]); ss [B] = ||x||^2 when non-null
 // rows: n_router of Wr (logits, + beta), n_pred of A (q), then the vector G
 // when given (gdot); ss: ||x||^2 when given
 hipError_t launch_scores(bool bf16, const void *x, int B, int d, const float *Wr,
