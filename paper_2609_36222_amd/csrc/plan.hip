@@ -11,8 +11,8 @@
 // k_backfill one wavefront per token: the experts it executes -- its K
 //            highest-ranked experts inside the kept set, or only its kept
 //            routes under the drop rule -- and their gates (Sec. 3.5).
-// k_compact  one workgroup: counting sort of the executed (token, rank)
-//            pairs by (kept slot, token), the token lists of the grouped FFN.
+// k_compact  one workgroup: stable counting sort of the executed (token,
+//            rank) pairs by kept slot, the token lists of the grouped FFN.
 // k_select_backfill  the first two in one launch (the fused layer): every
 //            workgroup repeats the selection and backfills its own tokens.
 #include "common.hpp"
@@ -138,18 +138,19 @@ __device__ __forceinline__ int select_body(SelLds &S, int B, int K, int E, int b
   return n_sel;
 }
 
-// Thread t < B: token t's routes and costs.
+// Thread t: token min(t, B - 1)'s routes and costs (select_body reads them
+// for t < B only).
 __device__ __forceinline__ void load_routes(int B, int K, const int32_t *__restrict__ ids,
                                             const float *__restrict__ cost, int (&uk)[MAX_K],
                                             float (&ck)[MAX_K]) {
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, tc = min(tid, B - 1);
 #pragma unroll
   for (int k = 0; k < MAX_K; ++k) {
     uk[k] = -1;
     ck[k] = 0.0f;
-    if (k < K && tid < B) {
-      uk[k] = ids[(size_t)tid * K + k];
-      ck[k] = cost[(size_t)tid * K + k];
+    if (k < K) {   // a uniform branch; the loads themselves are unconditional
+      uk[k] = ids[(size_t)tc * K + k];
+      ck[k] = cost[(size_t)tc * K + k];
     }
   }
 }
@@ -194,19 +195,16 @@ struct BfLds {
 // routed experts that were kept, in routing order.  Gates: exp(l_v - l_max)
 // over the original denominator (its top-K, or all E for a plain softmax
 // router) or, with renormalisation, over the executed experts.
-// Lane k < K: routed expert k of token t (out-of-range ids read expert 0).
-__device__ __forceinline__ int route_of(const int32_t *__restrict__ ids, int t, int K, int E) {
-  const int lane = lane_id();
-  int r_k = 0;
-  if (lane < K) {
-    const int u = ids[(size_t)t * K + lane];
-    r_k = (u >= 0 && u < E) ? u : 0;
-  }
-  return r_k;
+// Lane k < K: routed expert k of token t as stored (lanes >= K read the
+// token's last one); backfill_body maps out-of-range ids to expert 0.  The
+// load has no branch and no use here, so that it is in flight with the
+// kernel's other loads.
+__device__ __forceinline__ int route_of(const int32_t *__restrict__ ids, int t, int K) {
+  return ids[(size_t)t * K + min(lane_id(), K - 1)];
 }
 
 // lt: the token's logits row (global memory or an LDS copy); r_k: lane k <
-// K's routed expert (0 for an out-of-range id).  An inactive wavefront
+// K's routed expert as loaded by route_of.  An inactive wavefront
 // only takes part in the workgroup's barriers.
 template <int W>
 __device__ __forceinline__ void backfill_body(BfLds<W> &S, bool active, int t, int B, int E,
@@ -215,6 +213,7 @@ __device__ __forceinline__ void backfill_body(BfLds<W> &S, bool active, int t, i
                                               int32_t *__restrict__ exec_ids,
                                               float *__restrict__ exec_gates) {
   const int lane = lane_id(), wv = wave_id();
+  r_k = (lane < K && r_k >= 0 && r_k < E) ? r_k : 0;
   const int r0 = __shfl(r_k, 0, WAVE);
   const float lmax = active ? lt[r0] : 0.0f;
 
@@ -300,7 +299,7 @@ void k_backfill(int B, int E, int K, int norm_topk, int flags,
   __shared__ BfLds<BF_WAVES> S;
   const int t = blockIdx.x * BF_WAVES + wave_id(), tc = min(t, B - 1);
   backfill_body<BF_WAVES>(S, true, t, B, E, K, norm_topk, flags, logits + (size_t)tc * E,
-                          route_of(ids, tc, K, E), slot_of, *n_sel_p, exec_ids, exec_gates);
+                          route_of(ids, tc, K), slot_of, *n_sel_p, exec_ids, exec_gates);
 }
 
 // Selection and backfill in one launch: every workgroup makes the batch's
@@ -334,7 +333,7 @@ void k_select_backfill(int B, int K, int E, const int32_t *__restrict__ ids,
     const int e = lane + WAVE * i;
     lv[i] = (active && e < E) ? logits[(size_t)tc * E + e] : 0.0f;
   }
-  const int r_k = active ? route_of(ids, tc, K, E) : 0;
+  const int r_k = route_of(ids, tc, K);
   int uk[MAX_K];
   float ck[MAX_K];
   load_routes(B, K, ids, cost, uk, ck);
@@ -390,119 +389,172 @@ __device__ __forceinline__ void wave_scan3(const int *cnt, int n, int *off, int 
 }
 
 constexpr int CP_THREADS = 1024;
-constexpr int CP_WORDS = MAX_B / 32;
+constexpr int CP_WAVES = CP_THREADS / WAVE;
+constexpr int CP_STAGE = 4096;   // output positions staged in LDS per pass
 
-// One workgroup: counting sort of the executed (token, rank) pairs by (kept
-// slot, token), then ns shared slots (slot n_sel + i runs expert E + i for
-// every token in token order, gate sigmoid(gdot[t]) = 1 / (1 + exp(-s)) in
-// fp32, or 1); offsets, the pair lists, pair_of [B][K + ns] and the FFN's
-// part table.
+// One workgroup: a stable counting sort of the executed pairs by kept slot.
+// The routed pairs are taken in flat order q = t K + j, so sorting by (slot,
+// q) is sorting by (slot, token, rank).  Wavefront w owns the pairs w 64 PPT
+// + r 64 + lane (r = 0 .. PPT - 1, PPT pairs per thread, PPT * CP_THREADS >=
+// B K) and ranks each sub-block r without atomics: the lanes holding the same
+// slot find each other by ballots over the slot's bits, the lowest of them
+// adds their number to the wavefront's own counter of that slot, and every
+// lane's rank is that counter's value before the add plus its peers below
+// it.  The counters are then turned into prefixes over wavefronts and slots,
+// and the pair lists are written through an LDS staging buffer so that the
+// global stores are contiguous.  Then ns shared slots (slot n_sel + i runs
+// expert E + i for every token in token order, gate sigmoid(gdot[t]) =
+// 1 / (1 + exp(-s)) in fp32, or 1); offsets, the pair lists, pair_of
+// [B][K + ns] and the FFN's part table.  With 16 wavefronts on one CU every
+// per-thread instruction costs about 16 cycles, so the per-pair work is kept
+// short: no division (t = q / K as a multiply-high by kmul = ceil(2^32 / K),
+// exact for q < 2^32 / K, far above B K), and every global load is issued
+// before the first wait.
+template <int PPT>
 __global__ __launch_bounds__(CP_THREADS)
-void k_compact(int B, int K, int E, int budget, int ns, const int32_t *__restrict__ exec_ids,
-               const float *__restrict__ exec_gates,
+void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
+               const int32_t *__restrict__ exec_ids, const float *__restrict__ exec_gates,
                const int32_t *__restrict__ slot_of,
                const int32_t *__restrict__ n_sel_p, const float *__restrict__ gdot,
                int32_t *__restrict__ offsets, int32_t *__restrict__ pair_tok,
                float *__restrict__ pair_gate, int32_t *__restrict__ pair_of,
                const int32_t *__restrict__ sel_ids, PartRec *__restrict__ parts,
                int32_t *__restrict__ n_parts) {
-  // bits[s][w]: bit (t & 31) of word w = t >> 5 is set when token t runs slot s
-  __shared__ uint32_t bits[MAX_E * CP_WORDS];
-  __shared__ int pre[MAX_E * CP_WORDS];
+  // cw[w][s]: pairs of slot s in wavefront w, then their first rank in slot s
+  __shared__ int cw[CP_WAVES][MAX_E];
   __shared__ int cnt[SCAN_N];
   __shared__ int off[SCAN_N + 1];
   __shared__ int tb[SCAN_N + 1];
   __shared__ int pb[SCAN_N + 1];
   __shared__ int sel_s[MAX_E];
   __shared__ int slot_s[MAX_E];
-  const int tid = threadIdx.x, lane = lane_id();
-  const int nwords = (B + 31) / 32;
-  const int t = tid;
+  __shared__ int stage_t[CP_STAGE];
+  __shared__ float stage_g[CP_STAGE];
+  const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
   const int kc = K + ns;   // columns of pair_of
-  // every independent load first: the token's executed experts and gates,
-  // its shared-expert gate, the kept list, n_sel
-  int u_of[MAX_K];
-  float g_of[MAX_K];
+  const int nq = B * K;
+  const int q0 = wv * WAVE * PPT + lane;
+  // every global load first (clamped indices, no branches): the pairs'
+  // experts and gates, the kept list, the slot map, n_sel, the token's
+  // shared-expert gate
+  int u_r[PPT];
+  float g_r[PPT];
 #pragma unroll
-  for (int j = 0; j < MAX_K; ++j) {
-    u_of[j] = -1;
-    g_of[j] = 0.0f;
-    if (t < B && j < K) {
-      u_of[j] = exec_ids[(size_t)t * K + j];
-      g_of[j] = exec_gates[(size_t)t * K + j];
-    }
+  for (int r = 0; r < PPT; ++r) {
+    const int qc = min(q0 + r * WAVE, nq - 1);
+    u_r[r] = exec_ids[qc];
+    g_r[r] = exec_gates[qc];
   }
+  const int sel_v = sel_ids[min(tid, budget - 1)];
+  const int slot_v = slot_of[min(tid, E - 1)];
+  const int n_sel = min(max(*n_sel_p, 0), budget);
   float gs = 1.0f;
-  if (gdot && t < B) {
-    const float e = base_exp(-gdot[t]);
+  if (gdot) {
+    const float e = base_exp(-gdot[min(tid, B - 1)]);
     const float den = 1.0f + e;
     gs = 1.0f / den;
   }
-  if (tid < budget) sel_s[tid] = sel_ids[tid];
-  if (tid < E) slot_s[tid] = slot_of[tid];
-  const int n_sel = min(max(*n_sel_p, 0), budget);
-  for (int i = tid; i < budget * CP_WORDS; i += CP_THREADS) bits[i] = 0u;
+  if (tid < budget) sel_s[tid] = sel_v;
+  if (tid < E) slot_s[tid] = slot_v;
+  for (int s = lane; s < n_sel; s += WAVE) cw[wv][s] = 0;   // the wavefront's own row
   __syncthreads();
-  int s_of[MAX_K];
+  const int nbits = n_sel > 1 ? 32 - __clz(n_sel - 1) : 0;
+  const uint64_t below = (1ull << lane) - 1ull;
+  int s_r[PPT], p_r[PPT];
 #pragma unroll
-  for (int j = 0; j < MAX_K; ++j) {
-    const int s = (u_of[j] >= 0 && u_of[j] < E) ? slot_s[u_of[j]] : -1;
-    s_of[j] = (s >= 0 && s < n_sel) ? s : -1;
+  for (int r = 0; r < PPT; ++r) {
+    const int u = u_r[r];
+    int s = (q0 + r * WAVE < nq && u >= 0 && u < E) ? slot_s[u] : -1;
+    s = (s >= 0 && s < n_sel) ? s : -1;
+    s_r[r] = s;
+    uint64_t peers = __ballot(s >= 0);
+    for (int b = 0; b < nbits; ++b) {
+      const bool bit = (s >> b) & 1;
+      const uint64_t m = __ballot(bit);
+      peers &= bit ? m : ~m;
+    }
+    p_r[r] = -1;
+    if (s >= 0) {
+      const int base = cw[wv][s];
+      p_r[r] = base + __popcll(peers & below);
+      if ((peers & below) == 0ull) cw[wv][s] = base + __popcll(peers);
+    }
   }
-#pragma unroll
-  for (int j = 0; j < MAX_K; ++j)
-    if (s_of[j] >= 0) atomicOr(&bits[s_of[j] * CP_WORDS + (t >> 5)], 1u << (t & 31));
   __syncthreads();
   for (int s = tid; s < n_sel; s += CP_THREADS) {
     int run = 0;
-    for (int w = 0; w < nwords; ++w) {
-      pre[s * CP_WORDS + w] = run;
-      run += __popc(bits[s * CP_WORDS + w]);
+#pragma unroll
+    for (int w = 0; w < CP_WAVES; ++w) {
+      const int c = cw[w][s];
+      cw[w][s] = run;
+      run += c;
     }
     cnt[s] = run;
   }
-  for (int i = tid; i < ns; i += CP_THREADS) cnt[n_sel + i] = B;
+  if (tid >= n_sel && tid < n_sel + ns) cnt[tid] = B;
   __syncthreads();
   if (tid < WAVE) wave_scan3(cnt, n_sel + ns, off, tb, pb);
   __syncthreads();
   // the FFN's part table: every part of slot s gets the slot's entry
-  for (int s = wave_id(); s < n_sel + ns; s += CP_THREADS / WAVE) {
+  for (int s = wv; s < n_sel + ns; s += CP_WAVES) {
     const int np = pb[s + 1] - pb[s];
-    PartRec r;
-    r.u = s < n_sel ? sel_s[s] : E + (s - n_sel);
-    r.off = off[s];
-    r.n = cnt[s];
-    r.tile0 = tb[s];
-    r.part0 = pb[s];
-    r.parts = np;
-    r.pad0 = r.pad1 = 0;
-    for (int i = lane; i < np; i += WAVE) parts[pb[s] + i] = r;
+    PartRec rec;
+    rec.u = s < n_sel ? sel_s[s] : E + (s - n_sel);
+    rec.off = off[s];
+    rec.n = cnt[s];
+    rec.tile0 = tb[s];
+    rec.part0 = pb[s];
+    rec.parts = np;
+    rec.pad0 = rec.pad1 = 0;
+    for (int i = lane; i < np; i += WAVE) parts[pb[s] + i] = rec;
   }
   if (tid == 0) *n_parts = pb[SCAN_N];
   const int routed = off[n_sel];   // pairs of the kept slots
-  for (int s = tid; s <= budget; s += CP_THREADS)
-    offsets[s] = (s < n_sel) ? off[s] : routed;
-  for (int i = tid; i < ns; i += CP_THREADS) offsets[budget + 1 + i] = off[n_sel + i + 1];
-  if (t < B) {
+  if (tid <= budget) offsets[tid] = (tid < n_sel) ? off[tid] : routed;
+  if (tid < ns) offsets[budget + 1 + tid] = off[n_sel + tid + 1];
+  // positions, pair_of and the first staging pass
+  int t_r[PPT];
 #pragma unroll
-    for (int j = 0; j < MAX_K; ++j) {
-      if (j < K) {
-        int p = -1;
-        const int s = s_of[j];
-        if (s >= 0) {
-          const uint32_t below = bits[s * CP_WORDS + (t >> 5)] & ((1u << (t & 31)) - 1u);
-          p = off[s] + pre[s * CP_WORDS + (t >> 5)] + __popc(below);
-          pair_tok[p] = t;
-          pair_gate[p] = g_of[j];
-        }
-        pair_of[(size_t)t * kc + j] = p;
+  for (int r = 0; r < PPT; ++r) {
+    const int q = q0 + r * WAVE;
+    const int t = (int)(((uint64_t)(uint32_t)q * kmul) >> 32);
+    t_r[r] = t;
+    const int s = s_r[r];
+    if (s >= 0) {
+      p_r[r] += off[s] + cw[wv][s];
+      if (p_r[r] < CP_STAGE) {
+        stage_t[p_r[r]] = t;
+        stage_g[p_r[r]] = g_r[r];
       }
     }
+    if (q < nq) pair_of[(size_t)t * kc + (q - t * K)] = p_r[r];
+  }
+  // the routed pair lists, CP_STAGE positions per pass
+  for (int c0 = 0; c0 < routed; c0 += CP_STAGE) {
+    if (c0 > 0) {
+#pragma unroll
+      for (int r = 0; r < PPT; ++r) {
+        const int i = p_r[r] - c0;
+        if (s_r[r] >= 0 && i >= 0 && i < CP_STAGE) {
+          stage_t[i] = t_r[r];
+          stage_g[i] = g_r[r];
+        }
+      }
+    }
+    __syncthreads();
+    const int n = min(CP_STAGE, routed - c0);
+    for (int i = tid; i < n; i += CP_THREADS) {
+      pair_tok[c0 + i] = stage_t[i];
+      pair_gate[c0 + i] = stage_g[i];
+    }
+    __syncthreads();
+  }
+  if (tid < B) {
     for (int i = 0; i < ns; ++i) {
-      const int p = off[n_sel + i] + t;
-      pair_tok[p] = t;
+      const int p = off[n_sel + i] + tid;
+      pair_tok[p] = tid;
       pair_gate[p] = gs;
-      pair_of[(size_t)t * kc + K + i] = p;
+      pair_of[(size_t)tid * kc + K + i] = p;
     }
   }
 }
@@ -544,9 +596,18 @@ hipError_t launch_compact(int B, int K, int E, int budget, int ns, const int32_t
                           int32_t *pair_tok, float *pair_gate,
                           int32_t *pair_of, const int32_t *sel_ids,
                           PartRec *parts, int32_t *n_parts, hipStream_t st) {
-  launch_k(k_compact, dim3(1), dim3(CP_THREADS), 0, st, B, K, E, budget, ns,
-                     exec_ids, exec_gates, slot_of, n_sel, gdot, offsets, pair_tok,
-                     pair_gate, pair_of, sel_ids, parts, n_parts);
+  const int ppt = (B * K + CP_THREADS - 1) / CP_THREADS;
+  const uint64_t kmul = ((1ull << 32) + (uint64_t)K - 1) / (uint64_t)K;
+#define BASE_COMPACT(P)                                                                    \
+  launch_k(k_compact<P>, dim3(1), dim3(CP_THREADS), 0, st, B, K, kmul, E, budget, ns,     \
+           exec_ids, exec_gates, slot_of, n_sel, gdot, offsets, pair_tok, pair_gate,      \
+           pair_of, sel_ids, parts, n_parts)
+  if (ppt <= 1) BASE_COMPACT(1);
+  else if (ppt <= 2) BASE_COMPACT(2);
+  else if (ppt <= 4) BASE_COMPACT(4);
+  else if (ppt <= 8) BASE_COMPACT(8);
+  else BASE_COMPACT(16);
+#undef BASE_COMPACT
   return hipGetLastError();
 }
 

@@ -240,7 +240,7 @@ void k_scores(const XT *__restrict__ x, int B, int d,
 }
 
 constexpr int TL_WAVES = 4;    // tokens (wavefronts) per workgroup
-
+constexpr int TL_NI = MAX_E / WAVE;
 
 // mode bit 0: route (top-K and weights from the logits into ids / w)
 // mode bit 1: per-pair scores of the routed pairs (ids / w, read back when
@@ -248,30 +248,57 @@ constexpr int TL_WAVES = 4;    // tokens (wavefronts) per workgroup
 //             from q and ss; SCORE_TOP1 1 for the first route, else 0;
 //             SCORE_WEIGHT w; SCORE_WEIGHT_SQ w * w; SCORE_STATIC
 //             (w * w) * exp(b_u)
+// One wavefront per token.  Every global load is issued first, with clamped
+// indices: the token's logits, its whole predictor row q[t][*], b and ||x||^2
+// (the routed experts are not known yet, so a pair's q and b are then read
+// from LDS rather than from memory); the kernel waits on memory once.
 __global__ __launch_bounds__(TL_WAVES * WAVE)
 void k_tail(int B, int E, int K, int norm_topk, const float *__restrict__ logits,
             const float *__restrict__ q, const float *__restrict__ ss,
             const float *__restrict__ bp, int32_t *__restrict__ ids_io,
             float *__restrict__ w_io, float *__restrict__ cost, int mode, int rule) {
   __shared__ float lrow[TL_WAVES][MAX_E];
+  __shared__ float qrow[TL_WAVES][MAX_E];
+  __shared__ float brow[TL_WAVES][MAX_E];
   __shared__ float eps_s[TL_WAVES][MAX_K];
   const int lane = lane_id(), wv = wave_id();
   const int t = blockIdx.x * TL_WAVES + wv;
   const int tc = min(t, B - 1);            // every wavefront takes part in the barriers
   const bool live = t < B;
-  const float *lt = logits + (size_t)tc * E;
+  const bool need_q = (mode & 2) && rule == SCORE_BASE;
+  const bool need_b = (mode & 2) && (rule == SCORE_BASE || rule == SCORE_STATIC);
 
+  float lv[TL_NI], qv[TL_NI], bv[TL_NI];
+#pragma unroll
+  for (int i = 0; i < TL_NI; ++i) {
+    const int ec = min(lane + WAVE * i, E - 1);
+    lv[i] = (mode & 1) ? logits[(size_t)tc * E + ec] : 0.0f;
+    qv[i] = need_q ? q[(size_t)tc * E + ec] : 0.0f;
+    bv[i] = need_b ? bp[ec] : 0.0f;
+  }
+  const float s2 = need_q ? ss[tc] : 0.0f;
   int my_id = 0;       // lane k < K: routed expert k
   float my_w = 0.0f;   // and its weight
-  if (mode & 1) {
-    float lv[MAX_E / WAVE];
-    uint64_t kv[MAX_E / WAVE];
+  if (!(mode & 1)) {
+    my_id = ids_io[(size_t)tc * K + min(lane, K - 1)];
+    my_w = w_io[(size_t)tc * K + min(lane, K - 1)];
+  }
 #pragma unroll
-    for (int i = 0; i < MAX_E / WAVE; ++i) {
+  for (int i = 0; i < TL_NI; ++i) {
+    const int e = lane + WAVE * i;
+    if (e < E) {
+      lrow[wv][e] = lv[i];
+      qrow[wv][e] = qv[i];
+      brow[wv][e] = bv[i];
+    }
+  }
+
+  if (mode & 1) {
+    uint64_t kv[TL_NI];
+#pragma unroll
+    for (int i = 0; i < TL_NI; ++i) {
       const int e = lane + WAVE * i;
-      lv[i] = (e < E) ? lt[e] : 0.0f;
       kv[i] = (e < E) ? rank_key(lv[i], e) : 0;    // 0 ranks after every expert
-      if (e < E) lrow[wv][e] = lv[i];
     }
     // the top K in the order (logit desc, index asc): K successive wave
     // maxima of the keys, each winner removed by the lane holding it (keys
@@ -280,13 +307,13 @@ void k_tail(int B, int E, int K, int norm_topk, const float *__restrict__ logits
     for (int k = 0; k < K; ++k) {
       uint64_t best = 0;
 #pragma unroll
-      for (int i = 0; i < MAX_E / WAVE; ++i) best = kv[i] > best ? kv[i] : best;
+      for (int i = 0; i < TL_NI; ++i) best = kv[i] > best ? kv[i] : best;
       const uint64_t win = wave_max_key(best);
       const int e = (int)(0xFFFFFFFFu - (uint32_t)win);
       if (k == 0) top0 = e;
       if (lane == k) my_id = e;
 #pragma unroll
-      for (int i = 0; i < MAX_E / WAVE; ++i)
+      for (int i = 0; i < TL_NI; ++i)
         if (kv[i] == win) kv[i] = 0;
     }
     __syncthreads();
@@ -300,7 +327,7 @@ void k_tail(int B, int E, int K, int norm_topk, const float *__restrict__ logits
     } else {
       float part = 0.0f;
 #pragma unroll
-      for (int i = 0; i < MAX_E / WAVE; ++i) {
+      for (int i = 0; i < TL_NI; ++i) {
         const int e = lane + WAVE * i;
         if (e < E) part = part + base_exp(lv[i] - lmax);
       }
@@ -313,23 +340,21 @@ void k_tail(int B, int E, int K, int norm_topk, const float *__restrict__ logits
         w_io[(size_t)t * K + lane] = my_w;
       }
     }
-  } else if (lane < K) {
-    my_id = ids_io[(size_t)tc * K + lane];
-    my_w = w_io[(size_t)tc * K + lane];
+  } else {
+    __syncthreads();   // the rows written above
   }
 
   if ((mode & 2) && live && lane < K) {
     const int u = (my_id >= 0 && my_id < E) ? my_id : 0;   // out-of-range ids read row 0
     float c;
     if (rule == SCORE_BASE) {
-      const float s2 = ss[t];
       float inv = 0.0f;
       if (s2 > 0.0f) {
         const float rt = sqrtf(s2);
         inv = 1.0f / rt;
       }
-      float s = q[(size_t)t * E + u] * inv;
-      s = s + bp[u];
+      float s = qrow[wv][u] * inv;
+      s = s + brow[wv][u];
       const float w2 = my_w * my_w;
       c = w2 * base_exp(s);
     } else if (rule == SCORE_TOP1) {
@@ -340,7 +365,7 @@ void k_tail(int B, int E, int K, int norm_topk, const float *__restrict__ logits
       c = my_w * my_w;
     } else {   // SCORE_STATIC
       const float w2 = my_w * my_w;
-      c = w2 * base_exp(bp[u]);
+      c = w2 * base_exp(brow[wv][u]);
     }
     cost[(size_t)t * K + lane] = c;
   }
