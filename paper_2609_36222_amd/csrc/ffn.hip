@@ -360,6 +360,11 @@ void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
       ws.r[t] = make_rsrc(w2 + ((size_t)u * d + 64 * g + 16 * t) * I, (uint32_t)(16 * I * 2));
     ws.voff = (uint32_t)row * (uint32_t)(I * 2) + (uint32_t)(lane >> 4) * 16u;
   }
+  // the gates first: loaded after the contraction, each would sit behind
+  // the previous tile's stores in the memory counter
+  float gt[FF_NT];
+#pragma unroll
+  for (int j = 0; j < FF_NT; ++j) gt[j] = pair_gate[p0 + min(16 * j + row, n - 1)];
   const uint32_t tstride = (uint32_t)(I / 32) * 1024u;
   const rsrc_t rt = make_rsrc(hp + (size_t)tile0 * (I / 32) * 512, (uint32_t)nt * tstride);
   f32x4 acc[FF_RT][FF_NT];
@@ -372,8 +377,7 @@ void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
     const int tk = 16 * j + row;
     if (j < nt && tk < n) {
       const f32x4 o = sum_partials(sh, t, j);
-      const float gt = pair_gate[p0 + tk];
-      float4 v = {gt * o[0], gt * o[1], gt * o[2], gt * o[3]};
+      float4 v = {gt[j] * o[0], gt[j] * o[1], gt[j] * o[2], gt[j] * o[3]};
       *reinterpret_cast<float4 *>(pairbuf + (size_t)(p0 + tk) * d + 64 * g + 16 * t +
                                   4 * (lane >> 4)) = v;
     }

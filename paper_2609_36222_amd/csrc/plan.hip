@@ -22,7 +22,7 @@ namespace basek {
 
 constexpr int SEL_THREADS = 1024;
 constexpr int SEL_PAD = WAVE + 1;                 // LDS row of one chunk tree
-constexpr int SEL_V = 2 * 128 * SEL_PAD;          // chunk-matrix capacity (floats)
+constexpr int SEL_V = 4 * 128 * SEL_PAD;          // chunk-matrix capacity (floats)
 
 // LDS of the selection (one workgroup of SEL_THREADS threads)
 struct SelLds {
@@ -138,20 +138,59 @@ __device__ __forceinline__ int select_body(SelLds &S, int B, int K, int E, int b
   return n_sel;
 }
 
-// Thread t: token min(t, B - 1)'s routes and costs (select_body reads them
-// for t < B only).
+// Thread t < B: token t's routes and costs (-1 / 0 past K; threads t >= B
+// get nothing).  The [B][K] arrays are read with contiguous loads (a
+// wavefront's load covers 64 consecutive words, not 64 rows K words apart)
+// into `stage` (SEL_V floats, free again on return), rows padded to an odd
+// stride, and each thread then reads its token's row from LDS.
 __device__ __forceinline__ void load_routes(int B, int K, const int32_t *__restrict__ ids,
-                                            const float *__restrict__ cost, int (&uk)[MAX_K],
-                                            float (&ck)[MAX_K]) {
-  const int tid = threadIdx.x, tc = min(tid, B - 1);
+                                            const float *__restrict__ cost, float *stage,
+                                            int (&uk)[MAX_K], float (&ck)[MAX_K]) {
+  constexpr int LG = 2;   // loads per thread and array in flight at once
+  const int tid = threadIdx.x;
+  const int KP = K | 1;                                   // odd row stride
+  const int tpp = (SEL_V / 2) / KP;                       // tokens per pass
+  const uint64_t kmul = ((1ull << 32) + (uint64_t)K - 1) / (uint64_t)K;
+  int *si = reinterpret_cast<int *>(stage);
+  float *sf = stage + SEL_V / 2;
 #pragma unroll
   for (int k = 0; k < MAX_K; ++k) {
     uk[k] = -1;
     ck[k] = 0.0f;
-    if (k < K) {   // a uniform branch; the loads themselves are unconditional
-      uk[k] = ids[(size_t)tc * K + k];
-      ck[k] = cost[(size_t)tc * K + k];
+  }
+  for (int t0 = 0; t0 < B; t0 += tpp) {
+    const int nt = min(tpp, B - t0);
+    const int n = nt * K;
+    const size_t q0 = (size_t)t0 * K;
+    for (int g0 = 0; g0 < n; g0 += LG * SEL_THREADS) {
+      int vi[LG];
+      float vf[LG];
+#pragma unroll
+      for (int r = 0; r < LG; ++r) {
+        const int ic = min(g0 + tid + r * SEL_THREADS, n - 1);
+        vi[r] = ids[q0 + ic];
+        vf[r] = cost[q0 + ic];
+      }
+#pragma unroll
+      for (int r = 0; r < LG; ++r) {
+        const int i = g0 + tid + r * SEL_THREADS;
+        if (i < n) {
+          const int tt = (int)(((uint64_t)(uint32_t)i * kmul) >> 32);
+          si[tt * KP + (i - tt * K)] = vi[r];
+          sf[tt * KP + (i - tt * K)] = vf[r];
+        }
+      }
     }
+    __syncthreads();
+    if (tid >= t0 && tid < t0 + nt) {
+#pragma unroll
+      for (int k = 0; k < MAX_K; ++k)
+        if (k < K) {
+          uk[k] = si[(tid - t0) * KP + k];
+          ck[k] = sf[(tid - t0) * KP + k];
+        }
+    }
+    __syncthreads();
   }
 }
 
@@ -165,7 +204,7 @@ void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
   __shared__ SelLds S;
   int uk[MAX_K];
   float ck[MAX_K];
-  load_routes(B, K, ids, cost, uk, ck);
+  load_routes(B, K, ids, cost, S.V, uk, ck);
   select_body(S, B, K, E, budget, binary, uk, ck, true, scores, counts, sel_ids, n_sel_out,
               slot_of, nullptr);
 }
@@ -336,7 +375,7 @@ void k_select_backfill(int B, int K, int E, const int32_t *__restrict__ ids,
   const int r_k = route_of(ids, tc, K);
   int uk[MAX_K];
   float ck[MAX_K];
-  load_routes(B, K, ids, cost, uk, ck);
+  load_routes(B, K, ids, cost, U.sel.V, uk, ck);
   const int n_sel = select_body(U.sel, B, K, E, budget, binary, uk, ck, blockIdx.x == 0,
                                 scores, counts, sel_ids, n_sel_out, slot_of, slot_s);
   if (active) {
