@@ -239,6 +239,57 @@ def test_no_router_bias(gu):
     run_case(gu, inp, 5)
 
 
+@pytest.mark.parametrize("flags", [0, 2], ids=["backfill", "drop"])
+def test_repeated_route_ids(gu, flags):
+    """Routes given to base_select / base_moe_forward in which some tokens
+    name one expert twice (not what base_route produces, but allowed by the
+    ABI): the aggregation keeps the last cost and counts both, the drop
+    rule executes both copies, and the compaction gives each copy its own
+    pair in (slot, token, rank) order -- all bit for bit with the oracle."""
+    from paper_2609_36222_amd import binding as bd
+    inp = W.custom_layer(512, 24, 4, 128, 70, seed=11)
+    sh = inp["shape"]
+    B, K, E, budget = inp["x"].shape[0], sh.K, sh.E, 9
+    logits, ids, w = carith.route(inp["x"], inp["w_router"], inp["b_router"], K, 1)
+    ids = ids.copy()
+    g = np.random.default_rng(5)
+    dup = g.choice(B, size=B // 3, replace=False)
+    ids[dup, K - 1] = ids[dup, 0]                 # rank K-1 repeats rank 0
+    ids[dup[: B // 6], 2] = ids[dup[: B // 6], 1]  # and some repeat rank 1 too
+    cost = method.pair_scores_c(0, inp["x"], inp["pred_a"], inp["pred_b"], ids, w)
+    scores, counts = carith.aggregate(ids, cost, E)
+    sel, n_sel, slot = method.select(scores, counts, budget)
+    ex, n_ex = method.backfill(logits, ids, slot, n_sel, K, flags)
+    gates = method.gates_c(logits, ids, ex, n_ex, 1, flags)
+    offsets, pair_tok, pair_gate, pair_of = method.compact(ex, n_ex, slot, gates, budget)
+    y_ref = method.moe_restricted64(inp["x"], ex, n_ex, gates,
+                                    method.Experts(inp["w13"], inp["w2"], sh.bf16))
+    _flush(f"case repeated ids flags={flags} B={B} dup={len(dup)}")
+    gl = gu.GpuLayer(inp)
+    x = gl.x(inp["x"])
+    ids_d = torch.from_numpy(ids.astype(np.int32)).cuda()
+    cost_d = gu.dev_f32(cost)
+    s_d, c_d, sel_d, nsel_d, slot_d = gl.select(B, ids_d, cost_d, budget)
+    assert np.array_equal(s_d.cpu().numpy(), scores)
+    assert np.array_equal(c_d.cpu().numpy(), counts)
+    assert int(nsel_d.item()) == n_sel
+    assert np.array_equal(sel_d.cpu().numpy(), sel)
+    assert np.array_equal(slot_d.cpu().numpy(), slot)
+    ws = gl.workspace(B, budget)
+    y = gl.y_like(B)
+    plan = bd.base_moe_forward(gl.desc, x, B, gu.dev_f32(logits), ids_d, sel_d, nsel_d,
+                               slot_d, budget, flags, None, y, ws)
+    torch.cuda.synchronize()
+    got = gu.plan_arrays(plan, ws, B, K, E, budget, full=False)
+    check_plan(got, dict(exec_ids=ex, exec_gates=gates, offsets=offsets, pair_tok=pair_tok,
+                         pair_gate=pair_gate, pair_of=pair_of))
+    if flags & 2:   # the drop rule executes both copies of a repeated route
+        assert int((np.sum(got["pair_of"] >= 0, axis=1) > np.array(
+            [len(set(r.tolist())) for r in ids])).sum()) > 0
+    err = np.max(np.abs(gu.to_np_f32(y).astype(np.float64) - y_ref))
+    assert err <= Y_TOL[sh.bf16], err
+
+
 def test_repeat_runs_are_bit_identical(gu, qwen3_b256):
     from paper_2609_36222_amd import binding as bd
     gl = gu.GpuLayer(qwen3_b256)
