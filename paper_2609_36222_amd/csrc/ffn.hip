@@ -80,30 +80,47 @@ __device__ __forceinline__ bf16x8 wload(const WeightSrc &w, int t, int ks) {
 // Padding rows are never written; they only meet discarded output columns.
 
 // One wavefront per (part, k-step): the part's tiles' fragments of that
-// k-step, 1 KiB each; padding rows of a part's last tile are zeroed.
+// k-step, 1 KiB each; padding rows of a part's last tile are zeroed.  The
+// loads go out in three rounds, each issued whole before its first use: the
+// part's entry with the part count (the grid covers the largest possible
+// part count, so the entry is inside the table even when q is past the
+// real count and it is discarded), then the tokens of all its rows, then
+// the rows themselves.
 __global__ __launch_bounds__(256)
 void k_gather(const uint16_t *__restrict__ x, int d,
               const PartRec *__restrict__ parts,
               const int32_t *__restrict__ n_parts,
               const int32_t *__restrict__ pair_tok,
               uint16_t *__restrict__ xp) {
+  constexpr int NJ = FFN_PART / 16;
   const int ksteps = d / 32;
   const int v = blockIdx.x * (blockDim.x / WAVE) + wave_id();
   const int q = v / ksteps, ks = v % ksteps;
-  if (q >= *n_parts) return;
+  const int np = *n_parts;
   const PartRec r = parts[q];
+  if (q >= np) return;
   const int ts = q - r.part0;
   const int p0 = r.off + FFN_PART * ts, n = min(FFN_PART, r.n - FFN_PART * ts);
   const int tile0 = r.tile0 + (FFN_PART / 16) * ts;
   const int lane = lane_id();
-  for (int j = 0; 16 * j < n; ++j) {
-    const int k = 16 * j + (lane & 15);
-    u32x4 v4 = {0u, 0u, 0u, 0u};
-    if (k < n)
-      v4 = *reinterpret_cast<const u32x4 *>(x + (size_t)pair_tok[p0 + k] * d + 32 * ks +
-                                            8 * (lane >> 4));
-    *reinterpret_cast<u32x4 *>(xp + (((size_t)(tile0 + j) * ksteps + ks) * WAVE + lane) * 8) =
-        v4;
+  int tok[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) tok[j] = pair_tok[p0 + min(16 * j + (lane & 15), n - 1)];
+  // unconditional (a tile past the part's rows reads its last row again):
+  // loads under a branch would each be waited for at the branch's end
+  u32x4 v4[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+    v4[j] = *reinterpret_cast<const u32x4 *>(x + (size_t)tok[j] * d + 32 * ks +
+                                             8 * (lane >> 4));
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    if (16 * j < n) {
+      const bool pad = 16 * j + (lane & 15) >= n;
+      const u32x4 z = {0u, 0u, 0u, 0u};
+      *reinterpret_cast<u32x4 *>(xp + (((size_t)(tile0 + j) * ksteps + ks) * WAVE + lane) * 8) =
+          pad ? z : v4[j];
+    }
   }
 }
 
@@ -444,6 +461,7 @@ void k_down_f32(int d, int I, int E, const float *__restrict__ w2,
 }
 
 constexpr int CB_THREADS = 256;
+constexpr int CB_GROUP = 8;   // ranks whose rows are in flight together
 
 template <bool BF16>
 __global__ __launch_bounds__(CB_THREADS)
@@ -458,12 +476,23 @@ void k_combine(int B, int d, int kc, const int32_t *__restrict__ pair_of,
     if (BF16) load4((const uint16_t *)res + (size_t)t * d + c, acc);
     else load4((const float *)res + (size_t)t * d + c, acc);
   }
-  for (int j = 0; j < kc; ++j) {
-    const int p = pair_of[(size_t)t * kc + j];
-    if (p < 0) continue;   // a routed rank the token does not execute
-    const float4 v = *reinterpret_cast<const float4 *>(pairbuf + (size_t)p * d + c);
-    acc[0] = acc[0] + v.x; acc[1] = acc[1] + v.y;
-    acc[2] = acc[2] + v.z; acc[3] = acc[3] + v.w;
+  // CB_GROUP ranks at a time: their pair indices, then their rows, all
+  // requested before the first is added (the adds stay in rank order)
+  for (int j0 = 0; j0 < kc; j0 += CB_GROUP) {
+    int p[CB_GROUP];
+#pragma unroll
+    for (int i = 0; i < CB_GROUP; ++i)
+      p[i] = (j0 + i < kc) ? pair_of[(size_t)t * kc + j0 + i] : -1;
+    float4 v[CB_GROUP];
+#pragma unroll
+    for (int i = 0; i < CB_GROUP; ++i)
+      if (p[i] >= 0) v[i] = *reinterpret_cast<const float4 *>(pairbuf + (size_t)p[i] * d + c);
+#pragma unroll
+    for (int i = 0; i < CB_GROUP; ++i) {
+      if (p[i] < 0) continue;   // a routed rank the token does not execute
+      acc[0] = acc[0] + v[i].x; acc[1] = acc[1] + v[i].y;
+      acc[2] = acc[2] + v[i].z; acc[3] = acc[3] + v[i].w;
+    }
   }
   if (BF16) {
     u32x2 pk = {(uint32_t)f32_to_bf16(acc[0]) | ((uint32_t)f32_to_bf16(acc[1]) << 16),
