@@ -113,13 +113,18 @@ void k_gather(const uint16_t *__restrict__ x, int d,
   for (int j = 0; j < NJ; ++j)
     v4[j] = *reinterpret_cast<const u32x4 *>(x + (size_t)tok[j] * d + 32 * ks +
                                              8 * (lane >> 4));
+  // streaming (non-temporal) stores: the fragments are read once, by the
+  // next launch; stores that stay dirty in L2 are written back when this
+  // launch ends, which the next launch waits for (measured: 2.5 us less per
+  // step at batch 256)
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
     if (16 * j < n) {
       const bool pad = 16 * j + (lane & 15) >= n;
       const u32x4 z = {0u, 0u, 0u, 0u};
-      *reinterpret_cast<u32x4 *>(xp + (((size_t)(tile0 + j) * ksteps + ks) * WAVE + lane) * 8) =
-          pad ? z : v4[j];
+      __builtin_nontemporal_store(
+          pad ? z : v4[j],
+          reinterpret_cast<u32x4 *>(xp + (((size_t)(tile0 + j) * ksteps + ks) * WAVE + lane) * 8));
     }
   }
 }
