@@ -46,6 +46,8 @@ HBM_PEAK_GBS = 8000.0
 METRIC = ("MoE decode-step latency (µs) + HBM GB/s vs peak at batch "
           "64/256, budget B_e")
 DOMINANT = "ffn_gateup"
+# stages base_decode_layer runs inside another stage's kernel
+EMPTY_STAGES = ("backfill", "gather")
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 SHAPE_LABEL = {"tiny": "tiny fp32", "olmoe": "OLMoE-shaped", "qwen3_b64": "Qwen3-30B-A3B-shaped",
                "qwen3_b256": "Qwen3-30B-A3B-shaped", "mixtral": "Mixtral-shaped",
@@ -457,7 +459,7 @@ def bench_stack(args, shape, np, torch, W, bd):
     stage_us = np.array([[elapsed_ms(hip, evs[layer][2 * s], evs[layer][2 * s + 1]) * 1e3
                           for s in range(bd.N_STAGES)] for layer in range(L)])
     stage_sum = {bd.STAGES[s]: round(float(stage_us[:, s].sum()), 1)
-                 for s in range(bd.N_STAGES) if bd.STAGES[s] != "backfill"}
+                 for s in range(bd.N_STAGES) if bd.STAGES[s] not in EMPTY_STAGES}
     gu_bytes = budget * 2 * shape.I * shape.d * 2
     gu_us = float(stage_us[:, bd.STAGES.index("ffn_gateup")].mean())
     ffn_us = float(stage_us[:, bd.STAGES.index("ffn_gateup")].sum()
@@ -677,9 +679,10 @@ def main():
     for i in range(args.steps):
         for s in range(bd.N_STAGES):
             stage_us[i, s] = elapsed_ms(hip, stage_ev[i][2 * s], stage_ev[i][2 * s + 1]) * 1e3
-    # base_decode_layer backfills inside the selection kernel: the backfill
-    # stage launches nothing, and its back-to-back event pair is left out
-    timed_stages = [s for s in range(bd.N_STAGES) if bd.STAGES[s] != "backfill"]
+    # base_decode_layer backfills inside the selection kernel and gathers the
+    # FFN's tokens inside the compaction kernel: those two stages launch
+    # nothing, and their back-to-back event pairs are left out
+    timed_stages = [s for s in range(bd.N_STAGES) if bd.STAGES[s] not in EMPTY_STAGES]
     stage_mean = {bd.STAGES[s]: round(float(stage_us[:, s].mean()), 2) for s in timed_stages}
     stage_pct = {bd.STAGES[s]: pct(stage_us[:, s]) for s in timed_stages}
 
@@ -745,7 +748,7 @@ def main():
     # selection
     predict_us = (stage_mean["scores"] - route_scores_us) + (stage_mean["tail"] - route_tail_us)
     pas_us = predict_us + select_only_us
-    pre_ffn_us = sum(stage_mean[k] for k in ("scores", "tail", "select", "compact", "gather"))
+    pre_ffn_us = sum(stage_mean[k] for k in ("scores", "tail", "select", "compact"))
     ceiling = None
     if not args.no_ceiling:
         print("[bench] streaming-read ceiling", file=sys.stderr, flush=True)

@@ -189,14 +189,13 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
   PartRec *parts = at<PartRec>(ws, o.parts);
   int32_t *n_parts = at<int32_t>(ws, o.n_parts);
   const int ns = L->n_shared;
+  // the same launch gathers the FFN's token operand (bf16)
   HIP_TRY(launch_compact(B, L->K, L->E, bc, ns, exec_ids, exec_gates, slot_of, n_sel,
                          shared_gate(L) ? at<float>(ws, o.gdot) : nullptr, offsets,
-                         pair_tok, pair_gate, pair_of, sel_ids, parts, n_parts, st));
+                         pair_tok, pair_gate, pair_of, sel_ids, parts, n_parts,
+                         bf16 ? x : nullptr, L->d, bf16 ? at<void>(ws, o.xp) : nullptr, st));
   stage_end(st);
-  stage(5);
-  if (bf16)
-    HIP_TRY(launch_gather(x, B, L->d, ffn_max_parts(B, L->K, bc, ns), parts, n_parts,
-                          pair_tok, at<void>(ws, o.xp), st));
+  stage(5);   // no launch of its own: the gather is part of stage 4
   stage_end(st);
   stage(6);
   const bool packed = L->w_layout == BASE_W_PACKED;
@@ -467,10 +466,8 @@ base_status base_calib_accumulate(const base_layer *L, const void *z, int32_t B,
   HIP_TRY(launch_compact(B, C.K, C.E, bc, 0, at<int32_t>(ws, o.exec_ids),
                          at<float>(ws, o.exec_gates), slot, nsel, nullptr, offsets, pair_tok,
                          at<float>(ws, o.pair_gate), at<int32_t>(ws, o.pair_of), sel, parts,
-                         n_parts, st));
-  if (bf16)
-    HIP_TRY(launch_gather(z, B, C.d, ffn_max_parts(B, C.K, bc, 0), parts, n_parts, pair_tok,
-                          at<void>(ws, o.xp), st));
+                         n_parts, bf16 ? z : nullptr, C.d, bf16 ? at<void>(ws, o.xp) : nullptr,
+                         st));
   const bool packed = C.w_layout == BASE_W_PACKED;
   HIP_TRY(launch_gateup(bf16, packed, z, B, C.d, C.I, C.E, C.K, bc, 0, C.w13, nullptr, sel,
                         nsel, offsets, pair_tok, parts, n_parts, at<void>(ws, o.xp),

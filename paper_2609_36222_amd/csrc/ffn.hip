@@ -75,59 +75,10 @@ __device__ __forceinline__ bf16x8 wload(const WeightSrc &w, int t, int ks) {
 // fragment (tile, k-step) = 64 lanes x 8 elements, lane l holding pair
 // 16 i' + l % 16, elements 32 k-step + 8 (l / 16) .. +7.  So every operand
 // load of the FFN reads one contiguous 1 KiB block.
-//   xp: the hidden states of the pairs (contraction d), built by k_gather
+//   xp: the hidden states of the pairs (contraction d), written by the
+//       compaction launch (k_compact)
 //   hp: the SwiGLU activations (contraction I), written by k_gateup
 // Padding rows are never written; they only meet discarded output columns.
-
-// One wavefront per (part, k-step): the part's tiles' fragments of that
-// k-step, 1 KiB each; padding rows of a part's last tile are zeroed.  The
-// loads go out in three rounds, each issued whole before its first use: the
-// part's entry with the part count (the grid covers the largest possible
-// part count, so the entry is inside the table even when q is past the
-// real count and it is discarded), then the tokens of all its rows, then
-// the rows themselves.
-__global__ __launch_bounds__(256)
-void k_gather(const uint16_t *__restrict__ x, int d,
-              const PartRec *__restrict__ parts,
-              const int32_t *__restrict__ n_parts,
-              const int32_t *__restrict__ pair_tok,
-              uint16_t *__restrict__ xp) {
-  constexpr int NJ = FFN_PART / 16;
-  const int ksteps = d / 32;
-  const int v = blockIdx.x * (blockDim.x / WAVE) + wave_id();
-  const int q = v / ksteps, ks = v % ksteps;
-  const int np = *n_parts;
-  const PartRec r = parts[q];
-  if (q >= np) return;
-  const int ts = q - r.part0;
-  const int p0 = r.off + FFN_PART * ts, n = min(FFN_PART, r.n - FFN_PART * ts);
-  const int tile0 = r.tile0 + (FFN_PART / 16) * ts;
-  const int lane = lane_id();
-  int tok[NJ];
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) tok[j] = pair_tok[p0 + min(16 * j + (lane & 15), n - 1)];
-  // unconditional (a tile past the part's rows reads its last row again):
-  // loads under a branch would each be waited for at the branch's end
-  u32x4 v4[NJ];
-#pragma unroll
-  for (int j = 0; j < NJ; ++j)
-    v4[j] = *reinterpret_cast<const u32x4 *>(x + (size_t)tok[j] * d + 32 * ks +
-                                             8 * (lane >> 4));
-  // streaming (non-temporal) stores: the fragments are read once, by the
-  // next launch; stores that stay dirty in L2 are written back when this
-  // launch ends, which the next launch waits for (measured: 2.5 us less per
-  // step at batch 256)
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    if (16 * j < n) {
-      const bool pad = 16 * j + (lane & 15) >= n;
-      const u32x4 z = {0u, 0u, 0u, 0u};
-      __builtin_nontemporal_store(
-          pad ? z : v4[j],
-          reinterpret_cast<u32x4 *>(xp + (((size_t)(tile0 + j) * ksteps + ks) * WAVE + lane) * 8));
-    }
-  }
-}
 
 // Work list: unit v = (kept slot s, row group g, token part ts of s),
 // ordered by slot, then group, then part, so that the units that read one
@@ -507,15 +458,6 @@ void k_combine(int B, int d, int kc, const int32_t *__restrict__ pair_of,
     *reinterpret_cast<float4 *>((float *)y + (size_t)t * d + c) =
         float4{acc[0], acc[1], acc[2], acc[3]};
   }
-}
-
-hipError_t launch_gather(const void *x, int B, int d, int max_parts,
-                         const PartRec *parts, const int32_t *n_parts,
-                         const int32_t *pair_tok, void *xp, hipStream_t st) {
-  const long long waves = (long long)max_parts * (d / 32);
-  launch_k(k_gather, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, st,
-                     (const uint16_t *)x, d, parts, n_parts, pair_tok, (uint16_t *)xp);
-  return hipGetLastError();
 }
 
 hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,

@@ -97,16 +97,16 @@ hipError_t launch_backfill(int B, int E, int K, int norm_topk, int flags,
                            int32_t *exec_ids, float *exec_gates,
                            hipStream_t st);
 // ns shared slots follow the kept ones (expert E + i, every token, gate
-// sigmoid(gdot[t]) or 1 when gdot is null)
+// sigmoid(gdot[t]) or 1 when gdot is null).  With x_bf16 (the layer's bf16
+// hidden states, rows of d) the same launch also writes the FFN's token
+// operand xp.
 hipError_t launch_compact(int B, int K, int E, int budget, int ns, const int32_t *exec_ids,
                           const float *exec_gates, const int32_t *slot_of,
                           const int32_t *n_sel, const float *gdot, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
                           int32_t *pair_of, const int32_t *sel_ids,
-                          PartRec *parts, int32_t *n_parts, hipStream_t st);
-hipError_t launch_gather(const void *x, int B, int d, int max_parts,
-                         const PartRec *parts, const int32_t *n_parts,
-                         const int32_t *pair_tok, void *xp, hipStream_t st);
+                          PartRec *parts, int32_t *n_parts, const void *x_bf16, int d,
+                          void *xp, hipStream_t st);
 hipError_t launch_pack(const void *w13, const void *w2, void *w13p, void *w2p,
                        int E, int d, int I, hipStream_t st);
 // parts of expert u >= E read the shared experts' weights (w13s / w2s, u - E)

@@ -15,6 +15,8 @@
 //            rank) pairs by kept slot, the token lists of the grouped FFN.
 // k_select_backfill  the first two in one launch (the fused layer): every
 //            workgroup repeats the selection and backfills its own tokens.
+#include <algorithm>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -429,9 +431,20 @@ __device__ __forceinline__ void wave_scan3(const int *cnt, int n, int *off, int 
 
 constexpr int CP_THREADS = 1024;
 constexpr int CP_WAVES = CP_THREADS / WAVE;
-constexpr int CP_STAGE = 4096;   // output positions staged in LDS per pass
+constexpr int CP_STAGE = 4096;   // pair gates staged in LDS per pass
+constexpr int CP_PAIRS = MAX_B * MAX_K;   // routed pairs at most
+constexpr int CP_MAXPARTS = CP_PAIRS / FFN_PART + MAX_E + MAX_SHARED * (MAX_B / FFN_PART);
 
-// One workgroup: a stable counting sort of the executed pairs by kept slot.
+// A stable counting sort of the executed pairs by kept slot, then the FFN's
+// token operand.  Every workgroup of the launch makes the whole sort in its
+// own LDS (the same arithmetic, so the same result everywhere) and
+// workgroup 0 alone writes the plan; then all of them share the token
+// gather: for every (part, k-step) the part's hidden-state rows are copied
+// from x into xp in the FFN's fragment order (tile-major 1 KiB fragments:
+// fragment (tile, k-step) holds lane l = pair 16 tile' + l % 16 of the part's
+// tile, elements 32 k-step + 8 (l / 16) .. + 7; padding rows zeroed), with
+// streaming stores.  With x null (fp32 layers) there is no gather and one
+// workgroup.
 // The routed pairs are taken in flat order q = t K + j, so sorting by (slot,
 // q) is sorting by (slot, token, rank).  Wavefront w owns the pairs w 64 PPT
 // + r 64 + lane (r = 0 .. PPT - 1, PPT pairs per thread, PPT * CP_THREADS >=
@@ -458,7 +471,8 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
                int32_t *__restrict__ offsets, int32_t *__restrict__ pair_tok,
                float *__restrict__ pair_gate, int32_t *__restrict__ pair_of,
                const int32_t *__restrict__ sel_ids, PartRec *__restrict__ parts,
-               int32_t *__restrict__ n_parts) {
+               int32_t *__restrict__ n_parts, const uint16_t *__restrict__ x, int d,
+               uint16_t *__restrict__ xp) {
   // cw[w][s]: pairs of slot s in wavefront w, then their first rank in slot s
   __shared__ int cw[CP_WAVES][MAX_E];
   __shared__ int cnt[SCAN_N];
@@ -467,9 +481,11 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
   __shared__ int pb[SCAN_N + 1];
   __shared__ int sel_s[MAX_E];
   __shared__ int slot_s[MAX_E];
-  __shared__ int stage_t[CP_STAGE];
-  __shared__ float stage_g[CP_STAGE];
+  __shared__ int stage_t[CP_PAIRS];     // token of every routed position
+  __shared__ float stage_g[CP_STAGE];   // gates, CP_STAGE positions per pass
+  __shared__ int part_slot[CP_MAXPARTS];
   const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
+  const bool out = blockIdx.x == 0;     // the workgroup that writes the plan
   const int kc = K + ns;   // columns of pair_of
   const int nq = B * K;
   const int q0 = wv * WAVE * PPT + lane;
@@ -545,55 +561,89 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
     rec.part0 = pb[s];
     rec.parts = np;
     rec.pad0 = rec.pad1 = 0;
-    for (int i = lane; i < np; i += WAVE) parts[pb[s] + i] = rec;
+    for (int i = lane; i < np; i += WAVE) {
+      part_slot[pb[s] + i] = s;
+      if (out) parts[pb[s] + i] = rec;
+    }
   }
-  if (tid == 0) *n_parts = pb[SCAN_N];
+  if (out && tid == 0) *n_parts = pb[SCAN_N];
   const int routed = off[n_sel];   // pairs of the kept slots
-  if (tid <= budget) offsets[tid] = (tid < n_sel) ? off[tid] : routed;
-  if (tid < ns) offsets[budget + 1 + tid] = off[n_sel + tid + 1];
-  // positions, pair_of and the first staging pass
-  int t_r[PPT];
+  if (out && tid <= budget) offsets[tid] = (tid < n_sel) ? off[tid] : routed;
+  if (out && tid < ns) offsets[budget + 1 + tid] = off[n_sel + tid + 1];
+  // positions, pair_of, every routed position's token and the first pass
+  // of gates
 #pragma unroll
   for (int r = 0; r < PPT; ++r) {
     const int q = q0 + r * WAVE;
     const int t = (int)(((uint64_t)(uint32_t)q * kmul) >> 32);
-    t_r[r] = t;
     const int s = s_r[r];
     if (s >= 0) {
       p_r[r] += off[s] + cw[wv][s];
-      if (p_r[r] < CP_STAGE) {
-        stage_t[p_r[r]] = t;
-        stage_g[p_r[r]] = g_r[r];
-      }
+      stage_t[p_r[r]] = t;
+      if (p_r[r] < CP_STAGE) stage_g[p_r[r]] = g_r[r];
     }
-    if (q < nq) pair_of[(size_t)t * kc + (q - t * K)] = p_r[r];
+    if (out && q < nq) pair_of[(size_t)t * kc + (q - t * K)] = p_r[r];
   }
-  // the routed pair lists, CP_STAGE positions per pass
-  for (int c0 = 0; c0 < routed; c0 += CP_STAGE) {
-    if (c0 > 0) {
+  __syncthreads();
+  if (out) {
+    for (int i = tid; i < routed; i += CP_THREADS) pair_tok[i] = stage_t[i];
+    // the gates, CP_STAGE positions per pass
+    for (int c0 = 0; c0 < routed; c0 += CP_STAGE) {
+      if (c0 > 0) {
 #pragma unroll
-      for (int r = 0; r < PPT; ++r) {
-        const int i = p_r[r] - c0;
-        if (s_r[r] >= 0 && i >= 0 && i < CP_STAGE) {
-          stage_t[i] = t_r[r];
-          stage_g[i] = g_r[r];
+        for (int r = 0; r < PPT; ++r) {
+          const int i = p_r[r] - c0;
+          if (s_r[r] >= 0 && i >= 0 && i < CP_STAGE) stage_g[i] = g_r[r];
         }
+        __syncthreads();
+      }
+      const int n = min(CP_STAGE, routed - c0);
+      for (int i = tid; i < n; i += CP_THREADS) pair_gate[c0 + i] = stage_g[i];
+      __syncthreads();
+    }
+    if (tid < B) {
+      for (int i = 0; i < ns; ++i) {
+        const int p = off[n_sel + i] + tid;
+        pair_tok[p] = tid;
+        pair_gate[p] = gs;
+        pair_of[(size_t)tid * kc + K + i] = p;
       }
     }
-    __syncthreads();
-    const int n = min(CP_STAGE, routed - c0);
-    for (int i = tid; i < n; i += CP_THREADS) {
-      pair_tok[c0 + i] = stage_t[i];
-      pair_gate[c0 + i] = stage_g[i];
-    }
-    __syncthreads();
   }
-  if (tid < B) {
-    for (int i = 0; i < ns; ++i) {
-      const int p = off[n_sel + i] + tid;
-      pair_tok[p] = tid;
-      pair_gate[p] = gs;
-      pair_of[(size_t)tid * kc + K + i] = p;
+  if (!x) return;
+  // the token gather: one wavefront per (part, k-step); every load of a
+  // task is issued before its first use
+  constexpr int NJ = FFN_PART / 16;
+  const int ksteps = d / 32;
+  const int tasks = pb[SCAN_N] * ksteps;
+  for (int v = blockIdx.x * CP_WAVES + wv; v < tasks; v += gridDim.x * CP_WAVES) {
+    const int q = v / ksteps, ks = v - q * ksteps;
+    const int s = part_slot[q];
+    const int pr = FFN_PART * (q - pb[s]);   // the part's first pair within its slot
+    const int p0 = off[s] + pr, n = min(FFN_PART, cnt[s] - pr);
+    const int tile0 = tb[s] + (FFN_PART / 16) * (q - pb[s]);
+    int tok[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int k = min(16 * j + (lane & 15), n - 1);
+      tok[j] = s < n_sel ? stage_t[p0 + k] : pr + k;   // a shared slot lists every token
+    }
+    u32x4 v4[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      v4[j] = *reinterpret_cast<const u32x4 *>(x + (size_t)tok[j] * d + 32 * ks + 8 * (lane >> 4));
+    // streaming stores: the fragments are read once, by the FFN's launch;
+    // stores left dirty in L2 would be written back when this launch ends,
+    // which the next launch waits for
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      if (16 * j < n) {
+        const bool pad = 16 * j + (lane & 15) >= n;
+        const u32x4 z = {0u, 0u, 0u, 0u};
+        __builtin_nontemporal_store(
+            pad ? z : v4[j],
+            reinterpret_cast<u32x4 *>(xp + (((size_t)(tile0 + j) * ksteps + ks) * WAVE + lane) * 8));
+      }
     }
   }
 }
@@ -634,13 +684,19 @@ hipError_t launch_compact(int B, int K, int E, int budget, int ns, const int32_t
                           const int32_t *n_sel, const float *gdot, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
                           int32_t *pair_of, const int32_t *sel_ids,
-                          PartRec *parts, int32_t *n_parts, hipStream_t st) {
+                          PartRec *parts, int32_t *n_parts, const void *x_bf16, int d,
+                          void *xp, hipStream_t st) {
   const int ppt = (B * K + CP_THREADS - 1) / CP_THREADS;
+  // with a gather: one wavefront per (part, k-step) at most, 256 workgroups
+  // at most (one per CU: each holds the whole sort in its LDS)
+  const long long tasks = (long long)ffn_max_parts(B, K, budget, ns) * (d / 32);
+  const unsigned blocks =
+      x_bf16 ? (unsigned)std::min<long long>(256, (tasks + CP_WAVES - 1) / CP_WAVES) : 1u;
   const uint64_t kmul = ((1ull << 32) + (uint64_t)K - 1) / (uint64_t)K;
 #define BASE_COMPACT(P)                                                                    \
-  launch_k(k_compact<P>, dim3(1), dim3(CP_THREADS), 0, st, B, K, kmul, E, budget, ns,     \
+  launch_k(k_compact<P>, dim3(blocks), dim3(CP_THREADS), 0, st, B, K, kmul, E, budget, ns, \
            exec_ids, exec_gates, slot_of, n_sel, gdot, offsets, pair_tok, pair_gate,      \
-           pair_of, sel_ids, parts, n_parts)
+           pair_of, sel_ids, parts, n_parts, (const uint16_t *)x_bf16, d, (uint16_t *)xp)
   if (ppt <= 1) BASE_COMPACT(1);
   else if (ppt <= 2) BASE_COMPACT(2);
   else if (ppt <= 4) BASE_COMPACT(4);
