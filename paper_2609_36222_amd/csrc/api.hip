@@ -91,7 +91,7 @@ base_status check_ptr(const void *p, size_t a) {
 struct Layout {
   size_t logits, q, ss, gdot, topk_ids, topk_w, cost, scores, counts, sel_ids, n_sel,
       slot_of, exec_ids, exec_gates, offsets, pair_tok, pair_gate, pair_of,
-      parts, n_parts, xp, H, pairbuf, total;
+      units, xp, H, pairbuf, total;
 };
 
 size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -125,8 +125,11 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
   o.pair_tok = take(P * 4);
   o.pair_gate = take(P * 4);
   o.pair_of = take((size_t)B * (L->K + ns) * 4);
-  o.parts = take((size_t)ffn_max_parts(B, L->K, bc, ns) * sizeof(PartRec));
-  o.n_parts = take(4);
+  // the FFN's work units (bf16): gate/up workgroups, then down workgroups
+  o.units = L->dtype == BASE_BF16
+                ? take(((size_t)ffn_gu_blocks(B, L->K, bc, ns, L->I) +
+                        ffn_dn_blocks(B, L->K, bc, ns, L->d)) * sizeof(UnitRec))
+                : take(0);
   if (L->dtype == BASE_BF16) {
     // fragment-ordered tokens and SwiGLU activations (16-pair tiles)
     const size_t tiles = (size_t)ffn_max_tiles(B, L->K, bc, ns);
@@ -186,26 +189,27 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
                             slot_of, n_sel, exec_ids, exec_gates, st));
   stage_end(st);
   stage(4);
-  PartRec *parts = at<PartRec>(ws, o.parts);
-  int32_t *n_parts = at<int32_t>(ws, o.n_parts);
+  UnitRec *units = at<UnitRec>(ws, o.units);
+  UnitRec *dn_units = units + (bf16 ? ffn_gu_blocks(B, L->K, bc, L->n_shared, L->I) : 0);
   const int ns = L->n_shared;
-  // the same launch gathers the FFN's token operand (bf16)
+  // the same launch gathers the FFN's token operand and lists its work
+  // units (bf16)
   HIP_TRY(launch_compact(B, L->K, L->E, bc, ns, exec_ids, exec_gates, slot_of, n_sel,
                          shared_gate(L) ? at<float>(ws, o.gdot) : nullptr, offsets,
-                         pair_tok, pair_gate, pair_of, sel_ids, parts, n_parts,
-                         bf16 ? x : nullptr, L->d, bf16 ? at<void>(ws, o.xp) : nullptr, st));
+                         pair_tok, pair_gate, pair_of, sel_ids, bf16 ? x : nullptr, L->d,
+                         L->I, bf16 ? at<void>(ws, o.xp) : nullptr, units, st));
   stage_end(st);
   stage(5);   // no launch of its own: the gather is part of stage 4
   stage_end(st);
   stage(6);
   const bool packed = L->w_layout == BASE_W_PACKED;
   HIP_TRY(launch_gateup(bf16, packed, x, B, L->d, L->I, L->E, L->K, bc, ns, L->w13,
-                        L->w13_shared, sel_ids, n_sel, offsets, pair_tok, parts, n_parts,
+                        L->w13_shared, sel_ids, n_sel, offsets, pair_tok, units,
                         at<void>(ws, o.xp), at<void>(ws, o.H), st));
   stage_end(st);
   stage(7);
   HIP_TRY(launch_down(bf16, packed, B, L->d, L->I, L->E, L->K, bc, ns, L->w2,
-                      L->w2_shared, sel_ids, n_sel, offsets, parts, n_parts, pair_gate,
+                      L->w2_shared, sel_ids, n_sel, offsets, dn_units, pair_gate,
                       at<void>(ws, o.H), at<float>(ws, o.pairbuf), st));
   stage_end(st);
   stage(8);
@@ -461,19 +465,19 @@ base_status base_calib_accumulate(const base_layer *L, const void *z, int32_t B,
                           at<float>(ws, o.exec_gates), st));
   int32_t *offsets = at<int32_t>(ws, o.offsets);
   int32_t *pair_tok = at<int32_t>(ws, o.pair_tok);
-  PartRec *parts = at<PartRec>(ws, o.parts);
-  int32_t *n_parts = at<int32_t>(ws, o.n_parts);
+  UnitRec *units = at<UnitRec>(ws, o.units);
+  UnitRec *dn_units = units + (bf16 ? ffn_gu_blocks(B, C.K, bc, 0, C.I) : 0);
   HIP_TRY(launch_compact(B, C.K, C.E, bc, 0, at<int32_t>(ws, o.exec_ids),
                          at<float>(ws, o.exec_gates), slot, nsel, nullptr, offsets, pair_tok,
-                         at<float>(ws, o.pair_gate), at<int32_t>(ws, o.pair_of), sel, parts,
-                         n_parts, bf16 ? z : nullptr, C.d, bf16 ? at<void>(ws, o.xp) : nullptr,
-                         st));
+                         at<float>(ws, o.pair_gate), at<int32_t>(ws, o.pair_of), sel,
+                         bf16 ? z : nullptr, C.d, C.I, bf16 ? at<void>(ws, o.xp) : nullptr,
+                         units, st));
   const bool packed = C.w_layout == BASE_W_PACKED;
   HIP_TRY(launch_gateup(bf16, packed, z, B, C.d, C.I, C.E, C.K, bc, 0, C.w13, nullptr, sel,
-                        nsel, offsets, pair_tok, parts, n_parts, at<void>(ws, o.xp),
+                        nsel, offsets, pair_tok, units, at<void>(ws, o.xp),
                         at<void>(ws, o.H), st));
   HIP_TRY(launch_down(bf16, packed, B, C.d, C.I, C.E, C.K, bc, 0, C.w2, nullptr, sel, nsel,
-                      offsets, parts, n_parts, at<float>(ws, o.pair_gate), at<void>(ws, o.H),
+                      offsets, dn_units, at<float>(ws, o.pair_gate), at<void>(ws, o.H),
                       at<float>(ws, o.pairbuf), st));
   double *inv = at<double>(ws, o.total);
   double *y = at<double>(ws, o.total + up256((size_t)B * 8));

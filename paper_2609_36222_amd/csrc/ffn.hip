@@ -23,7 +23,6 @@ namespace basek {
 
 constexpr int GU_SPLIT = 4;      // gate/up: wavefronts per workgroup = contraction shares
 constexpr int DN_SPLIT = 1;      // down: one wavefront per unit
-constexpr int N_XCD = 8;         // accelerator dies, one L2 each
 constexpr int FF_RT = 4;         // 16-row weight tiles per wavefront
 constexpr int FF_NT = 4;         // 16-token tiles per wavefront (64 tokens)
 constexpr int FF_TOK = 16 * FF_NT;
@@ -80,61 +79,29 @@ __device__ __forceinline__ bf16x8 wload(const WeightSrc &w, int t, int ks) {
 //   hp: the SwiGLU activations (contraction I), written by k_gateup
 // Padding rows are never written; they only meet discarded output columns.
 
-// Work list: unit v = (kept slot s, row group g, token part ts of s),
-// ordered by slot, then group, then part, so that the units that read one
-// row group's weights are neighbours (and run at about the same time on
-// one XCD, the later ones finding the weights in L2).  The units of slot s
-// are v = groups * part0_s + g * parts_s + ts, so floor(v / groups) is one
-// of s's parts and its part-table entry describes s.  One workgroup per
-// unit; its wavefronts (GU_SPLIT, DN_SPLIT) each take an equal share of the
-// contraction and their partial sums are added through LDS in a fixed
+// Work units: one per workgroup, unit b of a launch at units[b], written by
+// the compaction launch (see k_compact for their order and their XCD runs).
+// A gate/up unit is (slot, row group of 32 gate + 32 up rows, 64-token
+// part), a down unit (slot, row group of 64 rows of d, part); the
+// workgroup's wavefronts (GU_SPLIT, DN_SPLIT) each take an equal share of
+// the contraction and their partial sums are added through LDS in a fixed
 // order.
 struct Unit {
   int u, p0, n, tile0, g;
 };
 
-// The dispatcher deals the workgroups of a launch round-robin over the
-// XCDs (workgroup b runs on XCD b % 8).  The unit list is cut into 8
-// contiguous runs, run x for XCD x, so the units that read one slot's
-// tokens or one row group's weights mostly share an L2.  Returns the unit
-// of the calling workgroup, or -1.
-__device__ __forceinline__ int xcd_unit(int units) {
-  const int per = (units + N_XCD - 1) / N_XCD;
-  const int local = blockIdx.x / N_XCD;
-  if (local >= per) return -1;
-  return (blockIdx.x % N_XCD) * per + local;
-}
-
 // Every value here is uniform over the workgroup, and is said to be so
 // (readfirstlane), so that the addresses derived from it stay in scalar
 // registers: a buffer resource held in vector registers would turn each
 // load into a loop over the lanes.
-__device__ __forceinline__ bool find_unit(int groups, const PartRec *parts,
-                                          const int32_t *n_parts, Unit &w) {
-  const int units = __builtin_amdgcn_readfirstlane(groups * *n_parts);
-  const int v = __builtin_amdgcn_readfirstlane(xcd_unit(units));
-  if (v < 0 || v >= units) return false;
-  const PartRec r = parts[v / groups];
-  const int u = __builtin_amdgcn_readfirstlane(r.u);
-  const int off = __builtin_amdgcn_readfirstlane(r.off);
-  const int n = __builtin_amdgcn_readfirstlane(r.n);
-  const int tile0 = __builtin_amdgcn_readfirstlane(r.tile0);
-  const int part0 = __builtin_amdgcn_readfirstlane(r.part0);
-  const int np = __builtin_amdgcn_readfirstlane(r.parts);
-  const int rel = v - groups * part0;
-  const int ts = rel % np;
-  w.g = rel / np;
-  w.u = u;
-  w.p0 = off + FFN_PART * ts;
-  w.n = min(FFN_PART, n - FFN_PART * ts);
-  w.tile0 = tile0 + (FFN_PART / 16) * ts;
-  return true;
-}
-
-// Workgroups for up to `units` units: a multiple of N_XCD, so that every
-// XCD's run of xcd_unit has all its workgroups.
-inline unsigned ffn_grid(long long units) {
-  return (unsigned)(((units + N_XCD - 1) / N_XCD) * N_XCD);
+__device__ __forceinline__ bool load_unit(const UnitRec *units, Unit &w) {
+  const UnitRec r = units[blockIdx.x];
+  w.u = __builtin_amdgcn_readfirstlane(r.u);
+  w.g = __builtin_amdgcn_readfirstlane(r.g);
+  w.p0 = __builtin_amdgcn_readfirstlane(r.p0);
+  w.n = __builtin_amdgcn_readfirstlane(r.n);
+  w.tile0 = __builtin_amdgcn_readfirstlane(r.tile0);
+  return w.u >= 0;
 }
 
 // One wavefront: FF_RT row tiles against NT token tiles over k-steps
@@ -253,13 +220,12 @@ template <bool PACKED>
 __global__ __launch_bounds__(GU_SPLIT * WAVE, 2)
 void k_gateup_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w13r,
                    const uint16_t *__restrict__ w13s,
-                   const PartRec *__restrict__ parts,
-                   const int32_t *__restrict__ n_parts,
+                   const UnitRec *__restrict__ units,
                    const uint16_t *__restrict__ xp, uint16_t *__restrict__ hp) {
   __shared__ Partials<GU_SPLIT> sh;
   const int groups = I / 32;
   Unit un;
-  if (!find_unit(groups, parts, n_parts, un)) return;
+  if (!load_unit(units, un)) return;
   if (un.u < 0 || un.u >= E + ns) return;   // only for a plan not made by base_select
   // experts E .. E + ns - 1 are the shared ones
   const uint16_t *w13 = un.u < E ? w13r : w13s;
@@ -309,14 +275,13 @@ template <bool PACKED>
 __global__ __launch_bounds__(DN_SPLIT * WAVE, 2)
 void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
                  const uint16_t *__restrict__ w2s,
-                 const PartRec *__restrict__ parts,
-                 const int32_t *__restrict__ n_parts,
+                 const UnitRec *__restrict__ units,
                  const float *__restrict__ pair_gate,
                  const uint16_t *__restrict__ hp, float *__restrict__ pairbuf) {
   __shared__ Partials<DN_SPLIT> sh;
   const int groups = d / 64;
   Unit un;
-  if (!find_unit(groups, parts, n_parts, un)) return;
+  if (!load_unit(units, un)) return;
   if (un.u < 0 || un.u >= E + ns) return;   // only for a plan not made by base_select
   const uint16_t *w2 = un.u < E ? w2r : w2s;
   const int u = un.u < E ? un.u : un.u - E, n = un.n, tile0 = un.tile0, p0 = un.p0;
@@ -464,13 +429,11 @@ hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
                          int I, int E, int K, int budget, int ns, const void *w13,
                          const void *w13s, const int32_t *sel_ids, const int32_t *n_sel,
                          const int32_t *offsets, const int32_t *pair_tok,
-                         const PartRec *parts, const int32_t *n_parts,
-                         const void *xp, void *H, hipStream_t st) {
+                         const UnitRec *units, const void *xp, void *H, hipStream_t st) {
   if (bf16) {
-    const long long units = (long long)ffn_max_parts(B, K, budget, ns) * (I / 32);
     launch_k(packed ? k_gateup_bf16<true> : k_gateup_bf16<false>,
-                       dim3(ffn_grid(units)), dim3(GU_SPLIT * WAVE), 0, st, d, I, E, ns,
-                       (const uint16_t *)w13, (const uint16_t *)w13s, parts, n_parts,
+                       dim3(ffn_gu_blocks(B, K, budget, ns, I)), dim3(GU_SPLIT * WAVE), 0, st,
+                       d, I, E, ns, (const uint16_t *)w13, (const uint16_t *)w13s, units,
                        (const uint16_t *)xp, (uint16_t *)H);
   } else {
     launch_k(k_gateup_f32, dim3(budget, (I + F32_ROWS - 1) / F32_ROWS),
@@ -485,14 +448,12 @@ hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K
                        int budget, int ns, const void *w2, const void *w2s,
                        const int32_t *sel_ids,
                        const int32_t *n_sel, const int32_t *offsets,
-                       const PartRec *parts, const int32_t *n_parts,
-                       const float *pair_gate, const void *H, float *pairbuf,
-                       hipStream_t st) {
+                       const UnitRec *units, const float *pair_gate, const void *H,
+                       float *pairbuf, hipStream_t st) {
   if (bf16) {
-    const long long units = (long long)ffn_max_parts(B, K, budget, ns) * (d / 64);
     launch_k(packed ? k_down_bf16<true> : k_down_bf16<false>,
-                       dim3(ffn_grid(units)), dim3(DN_SPLIT * WAVE), 0, st, d, I, E, ns,
-                       (const uint16_t *)w2, (const uint16_t *)w2s, parts, n_parts,
+                       dim3(ffn_dn_blocks(B, K, budget, ns, d)), dim3(DN_SPLIT * WAVE), 0, st,
+                       d, I, E, ns, (const uint16_t *)w2, (const uint16_t *)w2s, units,
                        pair_gate, (const uint16_t *)H, pairbuf);
   } else {
     launch_k(k_down_f32, dim3(budget, (d + F32_ROWS - 1) / F32_ROWS),

@@ -47,19 +47,28 @@ inline int ffn_max_parts(int B, int K, int budget, int ns) {
   return (B * K + FFN_PART - 1) / FFN_PART + budget + ns * ((B + FFN_PART - 1) / FFN_PART);
 }
 
-// The FFN's part table: entry q (one per 64-token part) describes the kept
-// slot s that part q belongs to, so that any FFN work unit decodes from the
-// one entry:
-//   u      the slot's expert
-//   off    its first pair (pairs off .. off + n - 1 in the compacted order)
-//   n      its pair count (>= 1)
-//   tile0  its first 16-pair tile in the fragment-ordered operands
-//   part0  its first part (the slot's parts are part0 .. part0 + parts - 1;
-//          part part0 + i covers its pairs 64 i .. 64 i + 63)
-//   parts  ceil(n / 64)
-struct alignas(32) PartRec {
-  int32_t u, off, n, tile0, part0, parts, pad0, pad1;
+// One FFN work unit: expert u (u >= E: shared expert u - E; -1: no unit),
+// its row group g, its pairs p0 .. p0 + n - 1 in the compacted order and
+// their first 16-pair tile.
+struct alignas(32) UnitRec {
+  int32_t u, g, p0, n, tile0, pad0, pad1, pad2;
 };
+
+constexpr int N_XCD = 8;   // accelerator dies, one L2 each
+
+// Workgroups for up to `units` units: a multiple of N_XCD, so that every
+// XCD's run of units has all its workgroups.
+inline unsigned ffn_grid(long long units) {
+  return (unsigned)(((units + N_XCD - 1) / N_XCD) * N_XCD);
+}
+// The FFN launches' workgroups (bf16): gate/up row groups of 32 gate + 32
+// up rows, down row groups of 64 rows of d, one unit per workgroup.
+inline unsigned ffn_gu_blocks(int B, int K, int budget, int ns, int I) {
+  return ffn_grid((long long)ffn_max_parts(B, K, budget, ns) * (I / 32));
+}
+inline unsigned ffn_dn_blocks(int B, int K, int budget, int ns, int d) {
+  return ffn_grid((long long)ffn_max_parts(B, K, budget, ns) * (d / 64));
+}
 
 // rows: n_router of Wr (logits, + beta), n_pred of A (q), then the vector G
 // when given (gdot); ss: ||x||^2 when given
@@ -99,14 +108,14 @@ hipError_t launch_backfill(int B, int E, int K, int norm_topk, int flags,
 // ns shared slots follow the kept ones (expert E + i, every token, gate
 // sigmoid(gdot[t]) or 1 when gdot is null).  With x_bf16 (the layer's bf16
 // hidden states, rows of d) the same launch also writes the FFN's token
-// operand xp.
+// operand xp and its work units: units[b] for gate/up workgroup b, then
+// units[ffn_gu_blocks + b] for down workgroup b.
 hipError_t launch_compact(int B, int K, int E, int budget, int ns, const int32_t *exec_ids,
                           const float *exec_gates, const int32_t *slot_of,
                           const int32_t *n_sel, const float *gdot, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
-                          int32_t *pair_of, const int32_t *sel_ids,
-                          PartRec *parts, int32_t *n_parts, const void *x_bf16, int d,
-                          void *xp, hipStream_t st);
+                          int32_t *pair_of, const int32_t *sel_ids, const void *x_bf16, int d,
+                          int I, void *xp, UnitRec *units, hipStream_t st);
 hipError_t launch_pack(const void *w13, const void *w2, void *w13p, void *w2p,
                        int E, int d, int I, hipStream_t st);
 // parts of expert u >= E read the shared experts' weights (w13s / w2s, u - E)
@@ -115,15 +124,13 @@ hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
                          const void *w13s,
                          const int32_t *sel_ids, const int32_t *n_sel,
                          const int32_t *offsets, const int32_t *pair_tok,
-                         const PartRec *parts, const int32_t *n_parts,
-                         const void *xp, void *H, hipStream_t st);
+                         const UnitRec *units, const void *xp, void *H, hipStream_t st);
 hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K,
                        int budget, int ns, const void *w2, const void *w2s,
                        const int32_t *sel_ids,
                        const int32_t *n_sel, const int32_t *offsets,
-                       const PartRec *parts, const int32_t *n_parts,
-                       const float *pair_gate, const void *H, float *pairbuf,
-                       hipStream_t st);
+                       const UnitRec *units, const float *pair_gate, const void *H,
+                       float *pairbuf, hipStream_t st);
 // kc: columns of pair_of (K routed + the shared experts)
 hipError_t launch_combine(bool bf16, int B, int d, int kc,
                           const int32_t *pair_of, const float *pairbuf,

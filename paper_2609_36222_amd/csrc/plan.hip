@@ -470,9 +470,9 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
                const int32_t *__restrict__ n_sel_p, const float *__restrict__ gdot,
                int32_t *__restrict__ offsets, int32_t *__restrict__ pair_tok,
                float *__restrict__ pair_gate, int32_t *__restrict__ pair_of,
-               const int32_t *__restrict__ sel_ids, PartRec *__restrict__ parts,
-               int32_t *__restrict__ n_parts, const uint16_t *__restrict__ x, int d,
-               uint16_t *__restrict__ xp) {
+               const int32_t *__restrict__ sel_ids, const uint16_t *__restrict__ x, int d,
+               int I, uint16_t *__restrict__ xp, UnitRec *__restrict__ units, int gu_blocks,
+               int dn_blocks) {
   // cw[w][s]: pairs of slot s in wavefront w, then their first rank in slot s
   __shared__ int cw[CP_WAVES][MAX_E];
   __shared__ int cnt[SCAN_N];
@@ -550,23 +550,9 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
   __syncthreads();
   if (tid < WAVE) wave_scan3(cnt, n_sel + ns, off, tb, pb);
   __syncthreads();
-  // the FFN's part table: every part of slot s gets the slot's entry
-  for (int s = wv; s < n_sel + ns; s += CP_WAVES) {
-    const int np = pb[s + 1] - pb[s];
-    PartRec rec;
-    rec.u = s < n_sel ? sel_s[s] : E + (s - n_sel);
-    rec.off = off[s];
-    rec.n = cnt[s];
-    rec.tile0 = tb[s];
-    rec.part0 = pb[s];
-    rec.parts = np;
-    rec.pad0 = rec.pad1 = 0;
-    for (int i = lane; i < np; i += WAVE) {
-      part_slot[pb[s] + i] = s;
-      if (out) parts[pb[s] + i] = rec;
-    }
-  }
-  if (out && tid == 0) *n_parts = pb[SCAN_N];
+  // the slot of every 64-token part
+  for (int s = wv; s < n_sel + ns; s += CP_WAVES)
+    for (int i = lane; i < pb[s + 1] - pb[s]; i += WAVE) part_slot[pb[s] + i] = s;
   const int routed = off[n_sel];   // pairs of the kept slots
   if (out && tid <= budget) offsets[tid] = (tid < n_sel) ? off[tid] : routed;
   if (out && tid < ns) offsets[budget + 1 + tid] = off[n_sel + tid + 1];
@@ -611,6 +597,41 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
     }
   }
   if (!x) return;
+  __syncthreads();   // part_slot complete
+  // The FFN's work units, one per workgroup of its two launches, shared out
+  // over this launch's workgroups.  Unit v of a launch with `groups` row
+  // groups is (slot s, row group g, part ts of s), ordered by slot, then
+  // group, then part (v = groups * first part of s + g * parts of s + ts),
+  // so that the units that read one row group's weights are neighbours;
+  // the list is cut into N_XCD contiguous runs and workgroup b (which the
+  // dispatcher runs on XCD b % N_XCD) takes unit local b / N_XCD of run
+  // b % N_XCD: the units that share a slot's tokens or a row group's
+  // weights mostly share an L2.
+  {
+    const int n_parts = pb[SCAN_N];
+    for (int e = blockIdx.x * CP_THREADS + tid; e < gu_blocks + dn_blocks;
+         e += gridDim.x * CP_THREADS) {
+      const bool gu = e < gu_blocks;
+      const int b = gu ? e : e - gu_blocks;
+      const int groups = gu ? I / 32 : d / 64;
+      const int nu = groups * n_parts;
+      const int per = (nu + N_XCD - 1) / N_XCD;
+      const int v = (b % N_XCD) * per + b / N_XCD;
+      UnitRec rec = {-1, 0, 0, 0, 0, 0, 0, 0};
+      if (b / N_XCD < per && v < nu) {
+        const int s = part_slot[v / groups];
+        const int np = pb[s + 1] - pb[s];
+        const int rel = v - groups * pb[s];
+        const int ts = rel % np;
+        rec.u = s < n_sel ? sel_s[s] : E + (s - n_sel);
+        rec.g = rel / np;
+        rec.p0 = off[s] + FFN_PART * ts;
+        rec.n = min(FFN_PART, cnt[s] - FFN_PART * ts);
+        rec.tile0 = tb[s] + (FFN_PART / 16) * ts;
+      }
+      units[e] = rec;
+    }
+  }
   // the token gather: one wavefront per (part, k-step); every load of a
   // task is issued before its first use
   constexpr int NJ = FFN_PART / 16;
@@ -684,19 +705,22 @@ hipError_t launch_compact(int B, int K, int E, int budget, int ns, const int32_t
                           const int32_t *n_sel, const float *gdot, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
                           int32_t *pair_of, const int32_t *sel_ids,
-                          PartRec *parts, int32_t *n_parts, const void *x_bf16, int d,
-                          void *xp, hipStream_t st) {
+                          const void *x_bf16, int d, int I, void *xp, UnitRec *units,
+                          hipStream_t st) {
   const int ppt = (B * K + CP_THREADS - 1) / CP_THREADS;
   // with a gather: one wavefront per (part, k-step) at most, 256 workgroups
   // at most (one per CU: each holds the whole sort in its LDS)
   const long long tasks = (long long)ffn_max_parts(B, K, budget, ns) * (d / 32);
   const unsigned blocks =
       x_bf16 ? (unsigned)std::min<long long>(256, (tasks + CP_WAVES - 1) / CP_WAVES) : 1u;
+  const unsigned gu_blocks = x_bf16 ? ffn_gu_blocks(B, K, budget, ns, I) : 0u;
+  const unsigned dn_blocks = x_bf16 ? ffn_dn_blocks(B, K, budget, ns, d) : 0u;
   const uint64_t kmul = ((1ull << 32) + (uint64_t)K - 1) / (uint64_t)K;
 #define BASE_COMPACT(P)                                                                    \
   launch_k(k_compact<P>, dim3(blocks), dim3(CP_THREADS), 0, st, B, K, kmul, E, budget, ns, \
            exec_ids, exec_gates, slot_of, n_sel, gdot, offsets, pair_tok, pair_gate,      \
-           pair_of, sel_ids, parts, n_parts, (const uint16_t *)x_bf16, d, (uint16_t *)xp)
+           pair_of, sel_ids, (const uint16_t *)x_bf16, d, I, (uint16_t *)xp, units,          \
+           (int)gu_blocks, (int)dn_blocks)
   if (ppt <= 1) BASE_COMPACT(1);
   else if (ppt <= 2) BASE_COMPACT(2);
   else if (ppt <= 4) BASE_COMPACT(4);
