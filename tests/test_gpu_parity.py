@@ -217,6 +217,8 @@ EDGE = [
     (768, 64, 6, 128, 100, True, {"zero_token": True}, 12),     # x = 0 row
     (256, 256, 16, 64, 200, True, {}, 40),     # E and K at their maxima
     (1024, 60, 4, 320, 1024, True, {}, 14),    # B at its maximum
+    (256, 32, 8, 64, 1000, True, {}, 20),      # 8000 routed pairs: 8 per compaction thread
+    (256, 64, 16, 64, 1024, True, {}, 40),     # B and K at their maxima: 16384 pairs
 ]
 
 
