@@ -144,8 +144,17 @@ __device__ __forceinline__ float base_exp(float x) {
 }
 
 // SwiGLU activation of the expert FFN (not part of the bit-exact path).
+// silu(a) = a / (1 + exp(-a)) for fp32 results
 __device__ __forceinline__ float silu(float a) {
   return a / (1.0f + __expf(-a));
+}
+
+// The same for a result that is rounded to bf16 next: the quotient as a
+// product with the hardware reciprocal (within an ulp or two of fp32, far
+// below bf16's rounding; the limits agree with the quotient's: -0 for a ->
+// -inf, a for large a, NaN for NaN)
+__device__ __forceinline__ float silu_bf16(float a) {
+  return a * __builtin_amdgcn_rcpf(1.0f + __expf(-a));
 }
 
 }  // namespace basek

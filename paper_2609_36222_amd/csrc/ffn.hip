@@ -214,8 +214,8 @@ __device__ __forceinline__ f32x4 sum_partials(const Partials<S> &sh, int t, int 
 // rows I + 32 g .. I + 32 g + 31 (tiles 2, 3).  Writes H in fragment order:
 // SwiGLU column i = 32 g + 16 t + 4 (l / 16) + r of pair tk sits in
 // fragment (tile of tk, k-step g), lane tk % 16 + 16 (2 t + (l / 16) / 2),
-// element 4 ((l / 16) % 2) + r.  Wavefront w finishes the gate tiles
-// t = w, w + GU_SPLIT, .. < 2, each with its up tile t + 2.
+// element 4 ((l / 16) % 2) + r.  After the partial sums are exchanged,
+// every wavefront finishes a share of the (gate tile, token tile) pairs.
 template <bool PACKED>
 __global__ __launch_bounds__(GU_SPLIT * WAVE, 2)
 void k_gateup_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w13r,
@@ -250,15 +250,20 @@ void k_gateup_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w13
   stream_share<GU_SPLIT, PACKED>(nt, ws, rt, tstride, d / 32, acc);
   put_partials(sh, nt, acc);
   __syncthreads();
-  for (int t = wave_id(); t < 2; t += GU_SPLIT)
+  // the SwiGLU of the 2 gate tiles x FF_NT token tiles, spread over the
+  // wavefronts: wavefront w takes gate tile w % 2 (with its up tile) for the
+  // token tiles w / 2, w / 2 + 2, ..
+  static_assert(GU_SPLIT % 2 == 0, "gate tile pairs per wavefront");
+  const int t = wave_id() % 2;
 #pragma unroll
-  for (int j = 0; j < FF_NT; ++j) {
+  for (int jj = 0; jj < FF_NT * 2 / GU_SPLIT; ++jj) {
+    const int j = wave_id() / 2 + (GU_SPLIT / 2) * jj;
     const int tk = 16 * j + row;
     if (j < nt && tk < n) {
       const f32x4 ga = sum_partials(sh, t, j), up = sum_partials(sh, t + 2, j);
       uint16_t h[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) h[r] = f32_to_bf16(silu(ga[r]) * up[r]);
+      for (int r = 0; r < 4; ++r) h[r] = f32_to_bf16(silu_bf16(ga[r]) * up[r]);
       u32x2 pk = {(uint32_t)h[0] | ((uint32_t)h[1] << 16),
                   (uint32_t)h[2] | ((uint32_t)h[3] << 16)};
       uint16_t *frag = hp + (((size_t)(tile0 + j) * (I / 32) + g) * WAVE) * 8;
@@ -269,8 +274,7 @@ void k_gateup_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w13
 }
 
 // down: row group g = rows 64 g .. 64 g + 63 of W_d (tiles 0..3); tokens
-// are the SwiGLU activations in fragment order.  Wavefront w finishes the
-// row tiles t = w, w + DN_SPLIT, ...
+// are the SwiGLU activations in fragment order.  One wavefront per unit.
 template <bool PACKED>
 __global__ __launch_bounds__(DN_SPLIT * WAVE, 2)
 void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
@@ -278,7 +282,7 @@ void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
                  const UnitRec *__restrict__ units,
                  const float *__restrict__ pair_gate,
                  const uint16_t *__restrict__ hp, float *__restrict__ pairbuf) {
-  __shared__ Partials<DN_SPLIT> sh;
+  static_assert(DN_SPLIT == 1, "the down epilogue takes the accumulators as they are");
   const int groups = d / 64;
   Unit un;
   if (!load_unit(units, un)) return;
@@ -307,14 +311,14 @@ void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
   const rsrc_t rt = make_rsrc(hp + (size_t)tile0 * (I / 32) * 512, (uint32_t)nt * tstride);
   f32x4 acc[FF_RT][FF_NT];
   stream_share<DN_SPLIT, PACKED>(nt, ws, rt, tstride, I / 32, acc);
-  put_partials(sh, nt, acc);
-  __syncthreads();
-  for (int t = wave_id(); t < FF_RT; t += DN_SPLIT)
+  // one wavefront per unit: its accumulators are the sums
+#pragma unroll
+  for (int t = 0; t < FF_RT; ++t)
 #pragma unroll
   for (int j = 0; j < FF_NT; ++j) {
     const int tk = 16 * j + row;
     if (j < nt && tk < n) {
-      const f32x4 o = sum_partials(sh, t, j);
+      const f32x4 o = acc[t][j];
       float4 v = {gt[j] * o[0], gt[j] * o[1], gt[j] * o[2], gt[j] * o[3]};
       *reinterpret_cast<float4 *>(pairbuf + (size_t)(p0 + tk) * d + 64 * g + 16 * t +
                                   4 * (lane >> 4)) = v;
