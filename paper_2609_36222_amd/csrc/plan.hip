@@ -457,12 +457,11 @@ constexpr int CP_MAXPARTS = CP_PAIRS / FFN_PART + MAX_E + MAX_SHARED * (MAX_B / 
 // global stores are contiguous.  Then ns shared slots (slot n_sel + i runs
 // expert E + i for every token in token order, gate sigmoid(gdot[t]) =
 // 1 / (1 + exp(-s)) in fp32, or 1); offsets, the pair lists and pair_of
-// [B][K + ns] (and, with x, the FFN's operand and work units, below).  With
-// 16 wavefronts on one CU every
-// per-thread instruction costs about 16 cycles, so the per-pair work is kept
-// short: no division (t = q / K as a multiply-high by kmul = ceil(2^32 / K),
-// exact for q < 2^32 / K, far above B K), and every global load is issued
-// before the first wait.
+// [B][K + ns] (and, with x, the FFN's operand and work units, below).
+// With 16 wavefronts on one CU every per-thread instruction costs about 16
+// cycles, so the per-pair work is kept short: no division (t = q / K as a
+// multiply-high by kmul = ceil(2^32 / K), exact for q < 2^32 / K, far above
+// B K), and every global load is issued before the first wait.
 template <int PPT>
 __global__ __launch_bounds__(CP_THREADS)
 void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
