@@ -229,6 +229,44 @@ def test_edge_shapes(gu, case):
     run_case(gu, inp, budget)
 
 
+def _random_cases(n, seed=2609):
+    """Seeded random layer shapes inside the ABI's limits (d a multiple of
+    256, I of 64, K <= E <= 256, K <= 16, B <= 1024; most batches small),
+    with random budget, gate / fill flags, router normalisation, selection
+    rule and (on some bf16 layers) shared experts."""
+    g = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        K = int(g.integers(1, 17))
+        E = int(g.integers(K, 257))
+        d = int(g.choice([256, 512, 768]))
+        I = 64 * int(g.integers(1, 6))
+        B = int(g.integers(1, 301)) if g.random() < 0.75 else int(g.integers(301, 1025))
+        bf16 = bool(g.random() < 0.8)
+        budget = int(g.integers(1, E + 4))
+        flags = int(g.integers(0, 4))
+        norm_topk = int(g.integers(0, 2))
+        rule = int(g.integers(0, 5))
+        # shared experts (bf16 layers only): 1 .. 8, gated or not
+        ns = int(g.integers(1, 9)) if bf16 and g.random() < 0.3 else 0
+        sg = bool(ns and g.random() < 0.5)
+        cases.append((d, E, K, I, B, bf16, budget, flags, norm_topk, rule, ns, sg, 1000 + i))
+    return cases
+
+
+RANDOM = _random_cases(64)
+
+
+@pytest.mark.parametrize("case", RANDOM, ids=[f"rand{i}" for i in range(len(RANDOM))])
+def test_random_shapes(gu, case):
+    """Seeded random shapes, budgets, options and shared experts: every plan
+    array bit for bit, y within tolerance, fused == staged, packed ==
+    row-major."""
+    d, E, K, I, B, bf16, budget, flags, norm_topk, rule, ns, sg, seed = case
+    inp = W.custom_layer(d, E, K, I, B, bf16=bf16, seed=seed, n_shared=ns, shared_gate=sg)
+    run_case(gu, inp, budget, flags=flags, norm_topk=norm_topk, score_rule=rule)
+
+
 def test_raw_softmax_weights(gu):
     inp = W.custom_layer(512, 40, 4, 128, 50, seed=3)
     run_case(gu, inp, 9, norm_topk=0)

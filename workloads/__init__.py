@@ -314,13 +314,14 @@ def rules_layer(seed=0, d=256, E=32, K=4, I=128, B=16, n_calib=4096):
 
 def custom_layer(d, E, K, I, B, bf16=True, seed=0, router_std=0.075,
                  zipf_bias=True, rmsnorm=True, identical_tokens=False,
-                 zero_token=False):
+                 zero_token=False, n_shared=0, shared_gate=False):
     """A seeded layer of arbitrary shape for edge cases (same recipe as the
-    named workloads; index 99 keeps its seeds apart from theirs)."""
-    shape = LayerShape(f"custom_d{d}_E{E}_K{K}_I{I}_B{B}", 99, d, E, K, I, B,
+    named workloads; index 99 keeps its seeds apart from theirs), with
+    n_shared always-active shared experts (bf16) when asked."""
+    shape = LayerShape(f"custom_d{d}_E{E}_K{K}_I{I}_B{B}_S{n_shared}", 99, d, E, K, I, B,
                        (1,), bf16, router_std=router_std,
                        bias_kind="zipf" if zipf_bias else "normal",
-                       rmsnorm=rmsnorm)
+                       rmsnorm=rmsnorm, n_shared=n_shared, shared_gate=shared_gate)
     wr, br = router(shape, seed)
     pa, pb = synthetic_predictor(shape, seed)
     x = decode_tokens(shape, seed)
@@ -329,5 +330,8 @@ def custom_layer(d, E, K, I, B, bf16=True, seed=0, router_std=0.075,
     if zero_token:
         x[0] = 0.0
     w13, w2 = experts(shape, seed)
-    return dict(shape=shape, x=x, w_router=wr, b_router=br, pred_a=pa,
-                pred_b=pb, w13=w13, w2=w2)
+    out = dict(shape=shape, x=x, w_router=wr, b_router=br, pred_a=pa,
+               pred_b=pb, w13=w13, w2=w2)
+    if n_shared:
+        out["w13_shared"], out["w2_shared"], out["shared_gate"] = shared_experts(shape, seed)
+    return out
