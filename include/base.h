@@ -226,7 +226,10 @@ base_status base_predict_cost(const base_layer *L, const void *x, int32_t B,
  *                   (D_hat > 0) desc, index asc) among experts with
  *                   count > 0; -1 beyond n_sel
  *   n_sel           [1] int32 out: min(budget, |batch union|)
- *   slot_of_expert  [E] int32 out: rank of u in sel_ids, or -1 */
+ *   slot_of_expert  [E] int32 out: rank of u in sel_ids, or -1
+ * Route ids are device data and are not validated: an id outside [0, E)
+ * is skipped here and in moe_forward (no access out of bounds), and what
+ * the call then computes is unspecified. */
 base_status base_select(const base_layer *L, int32_t B,
                         const int32_t *topk_ids, const float *cost,
                         int32_t budget, float *scores, int32_t *counts,
