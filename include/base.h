@@ -228,8 +228,8 @@ base_status base_predict_cost(const base_layer *L, const void *x, int32_t B,
  *   n_sel           [1] int32 out: min(budget, |batch union|)
  *   slot_of_expert  [E] int32 out: rank of u in sel_ids, or -1
  * Route ids are device data and are not validated: an id outside [0, E)
- * is skipped here and in moe_forward (no access out of bounds), and what
- * the call then computes is unspecified. */
+ * is ignored here and read as expert 0 by moe_forward; no access goes out
+ * of bounds, and the results are then unspecified. */
 base_status base_select(const base_layer *L, int32_t B,
                         const int32_t *topk_ids, const float *cost,
                         int32_t budget, float *scores, int32_t *counts,
