@@ -81,6 +81,10 @@ CASES = {
     "tiny": lambda: (W.layer_inputs("tiny"), 256, 2048, 2e-5),
     # a bf16 layer, 1024 tokens in batches of 128 (and a ragged last one)
     "bf16": lambda: (W.custom_layer(512, 16, 4, 128, 8, seed=5), 128, 1000, 2e-3),
+    # wider tokens, K = 16 of 48, batches of 97 (ragged throughout)
+    "k16": lambda: (W.custom_layer(768, 48, 16, 64, 8, seed=22), 97, 700, 2e-3),
+    # 120 tokens over 128 experts, top-2: many experts see 0, 1 or 2 tokens
+    "sparse": lambda: (W.custom_layer(256, 128, 2, 64, 8, seed=23), 64, 120, 2e-3),
 }
 
 
