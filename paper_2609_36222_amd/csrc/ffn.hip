@@ -189,25 +189,55 @@ struct Partials {
   f32x4 v[S][FF_RT][FF_NT][WAVE];
 };
 
-template <int S>
-__device__ __forceinline__ void put_partials(Partials<S> &sh, int nt,
-                                             const f32x4 (&acc)[FF_RT][FF_NT]) {
-  const int w = wave_id(), l = lane_id();
+// The gate/up exchange as a reduce-scatter: wavefront W finishes gate tile
+// W % 2 with its up tile for the token tiles j = W / 2 (mod 2); it keeps
+// those partial sums in registers and writes only the other twelve tiles.
+// Every sum still runs over the wavefronts in order 0 .. 3.
+template <int W>
+__device__ __forceinline__ bool rs_own(int t, int j) {
+  return (t % 2) == (W % 2) && (j % 2) == (W / 2);
+}
+template <int W>
+__device__ __forceinline__ void put_partials_rs(Partials<GU_SPLIT> &sh, int nt,
+                                                const f32x4 (&acc)[FF_RT][FF_NT]) {
+  const int l = lane_id();
 #pragma unroll
   for (int t = 0; t < FF_RT; ++t)
 #pragma unroll
     for (int j = 0; j < FF_NT; ++j)
-      if (j < nt) sh.v[w][t][j][l] = acc[t][j];
+      if (j < nt && !rs_own<W>(t, j)) sh.v[W][t][j][l] = acc[t][j];
 }
-
-// Sum of the partials of row tile t, token tile j, in wave order.
-template <int S>
-__device__ __forceinline__ f32x4 sum_partials(const Partials<S> &sh, int t, int j) {
+template <int W>
+__device__ __forceinline__ f32x4 sum_rs(const Partials<GU_SPLIT> &sh, const f32x4 &own,
+                                        int t, int j) {
   const int l = lane_id();
-  f32x4 r = sh.v[0][t][j][l];
+  f32x4 r = W == 0 ? own : sh.v[0][t][j][l];
 #pragma unroll
-  for (int w = 1; w < S; ++w) r += sh.v[w][t][j][l];
+  for (int w = 1; w < GU_SPLIT; ++w) r += (w == W) ? own : sh.v[w][t][j][l];
   return r;
+}
+template <int W>
+__device__ __forceinline__ void gu_epilogue(const Partials<GU_SPLIT> &sh,
+                                            const f32x4 (&acc)[FF_RT][FF_NT], int nt, int n,
+                                            int I, int g, int tile0, uint16_t *hp) {
+  const int lane = lane_id(), row = lane & 15;
+  constexpr int t = W % 2;
+#pragma unroll
+  for (int jj = 0; jj < FF_NT * 2 / GU_SPLIT; ++jj) {
+    const int j = W / 2 + (GU_SPLIT / 2) * jj;
+    const int tk = 16 * j + row;
+    if (j < nt && tk < n) {
+      const f32x4 ga = sum_rs<W>(sh, acc[t][j], t, j), up = sum_rs<W>(sh, acc[t + 2][j], t + 2, j);
+      uint16_t h[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) h[r] = f32_to_bf16(silu_bf16(ga[r]) * up[r]);
+      u32x2 pk = {(uint32_t)h[0] | ((uint32_t)h[1] << 16),
+                  (uint32_t)h[2] | ((uint32_t)h[3] << 16)};
+      uint16_t *frag = hp + (((size_t)(tile0 + j) * (I / 32) + g) * WAVE) * 8;
+      const int l2 = row + 16 * (2 * t + (lane >> 5));
+      *reinterpret_cast<u32x2 *>(frag + l2 * 8 + 4 * ((lane >> 4) & 1)) = pk;
+    }
+  }
 }
 
 // gate/up: row group g = gate rows 32 g .. 32 g + 31 (tiles 0, 1) and up
@@ -248,28 +278,22 @@ void k_gateup_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w13
   const rsrc_t rt = make_rsrc(xp + (size_t)tile0 * (d / 32) * 512, (uint32_t)nt * tstride);
   f32x4 acc[FF_RT][FF_NT];
   stream_share<GU_SPLIT, PACKED>(nt, ws, rt, tstride, d / 32, acc);
-  put_partials(sh, nt, acc);
-  __syncthreads();
   // the SwiGLU of the 2 gate tiles x FF_NT token tiles, spread over the
-  // wavefronts: wavefront w takes gate tile w % 2 (with its up tile) for the
-  // token tiles w / 2, w / 2 + 2, ..
-  static_assert(GU_SPLIT % 2 == 0, "gate tile pairs per wavefront");
-  const int t = wave_id() % 2;
-#pragma unroll
-  for (int jj = 0; jj < FF_NT * 2 / GU_SPLIT; ++jj) {
-    const int j = wave_id() / 2 + (GU_SPLIT / 2) * jj;
-    const int tk = 16 * j + row;
-    if (j < nt && tk < n) {
-      const f32x4 ga = sum_partials(sh, t, j), up = sum_partials(sh, t + 2, j);
-      uint16_t h[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) h[r] = f32_to_bf16(silu_bf16(ga[r]) * up[r]);
-      u32x2 pk = {(uint32_t)h[0] | ((uint32_t)h[1] << 16),
-                  (uint32_t)h[2] | ((uint32_t)h[3] << 16)};
-      uint16_t *frag = hp + (((size_t)(tile0 + j) * (I / 32) + g) * WAVE) * 8;
-      const int l2 = row + 16 * (2 * t + (lane >> 5));
-      *reinterpret_cast<u32x2 *>(frag + l2 * 8 + 4 * ((lane >> 4) & 1)) = pk;
-    }
+  // wavefronts (template argument: the wavefront, so that the tiles it
+  // keeps are fixed registers)
+  static_assert(GU_SPLIT == 4, "reduce-scatter exchange");
+  switch (wave_id()) {
+    case 0: put_partials_rs<0>(sh, nt, acc); break;
+    case 1: put_partials_rs<1>(sh, nt, acc); break;
+    case 2: put_partials_rs<2>(sh, nt, acc); break;
+    default: put_partials_rs<3>(sh, nt, acc); break;
+  }
+  __syncthreads();
+  switch (wave_id()) {
+    case 0: gu_epilogue<0>(sh, acc, nt, n, I, g, tile0, hp); break;
+    case 1: gu_epilogue<1>(sh, acc, nt, n, I, g, tile0, hp); break;
+    case 2: gu_epilogue<2>(sh, acc, nt, n, I, g, tile0, hp); break;
+    default: gu_epilogue<3>(sh, acc, nt, n, I, g, tile0, hp); break;
   }
 }
 
