@@ -350,12 +350,15 @@ void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
   }
 }
 
-// fp32 experts (small layers): one thread per (intermediate row, token
-// group), plain sequential dot products.
-constexpr int F32_ROWS = 64;
-constexpr int F32_TG = 4;
+// fp32 experts (small layers): one wavefront per (kept slot, output row).
+// The lanes split the contraction (lane l takes elements l, l + 64, ..., so
+// every load of a row is contiguous across the wavefront) and each token's
+// dot product is summed across the lanes by the butterfly of
+// wave_tree_sum.  The slot's tokens are taken one after another; the row
+// stays in L1 between them.
+constexpr int F32_WAVES = 4;   // rows per workgroup
 
-__global__ __launch_bounds__(F32_ROWS * F32_TG)
+__global__ __launch_bounds__(F32_WAVES * WAVE)
 void k_gateup_f32(const float *__restrict__ x, int d, int I, int E,
                   const float *__restrict__ w13,
                   const int32_t *__restrict__ sel_ids,
@@ -368,23 +371,25 @@ void k_gateup_f32(const float *__restrict__ x, int d, int I, int E,
   if (u < 0 || u >= E) return;   // only for a plan not made by base_select
   const int p0 = offsets[s];
   const int n = offsets[s + 1] - p0;
-  const int i = blockIdx.y * F32_ROWS + (threadIdx.x % F32_ROWS);
-  const int tg = threadIdx.x / F32_ROWS;
+  const int i = blockIdx.y * F32_WAVES + wave_id(), lane = lane_id();
   if (i >= I) return;
   const float *wg = w13 + ((size_t)u * 2 * I + i) * d;
   const float *wu = w13 + ((size_t)u * 2 * I + I + i) * d;
-  for (int tk = tg; tk < n; tk += F32_TG) {
+  for (int tk = 0; tk < n; ++tk) {
     const float *xr = x + (size_t)pair_tok[p0 + tk] * d;
     float g = 0.0f, v = 0.0f;
-    for (int k = 0; k < d; ++k) {
-      g = __builtin_fmaf(xr[k], wg[k], g);
-      v = __builtin_fmaf(xr[k], wu[k], v);
+    for (int k = lane; k < d; k += WAVE) {
+      const float xv = xr[k];
+      g = __builtin_fmaf(xv, wg[k], g);
+      v = __builtin_fmaf(xv, wu[k], v);
     }
-    H[(size_t)(p0 + tk) * I + i] = silu(g) * v;
+    g = wave_tree_sum(g);
+    v = wave_tree_sum(v);
+    if (lane == 0) H[(size_t)(p0 + tk) * I + i] = silu(g) * v;
   }
 }
 
-__global__ __launch_bounds__(F32_ROWS * F32_TG)
+__global__ __launch_bounds__(F32_WAVES * WAVE)
 void k_down_f32(int d, int I, int E, const float *__restrict__ w2,
                 const int32_t *__restrict__ sel_ids,
                 const int32_t *__restrict__ n_sel_p,
@@ -397,15 +402,15 @@ void k_down_f32(int d, int I, int E, const float *__restrict__ w2,
   if (u < 0 || u >= E) return;   // only for a plan not made by base_select
   const int p0 = offsets[s];
   const int n = offsets[s + 1] - p0;
-  const int c = blockIdx.y * F32_ROWS + (threadIdx.x % F32_ROWS);
-  const int tg = threadIdx.x / F32_ROWS;
+  const int c = blockIdx.y * F32_WAVES + wave_id(), lane = lane_id();
   if (c >= d) return;
   const float *wd = w2 + ((size_t)u * d + c) * I;
-  for (int tk = tg; tk < n; tk += F32_TG) {
+  for (int tk = 0; tk < n; ++tk) {
     const float *hr = H + (size_t)(p0 + tk) * I;
     float o = 0.0f;
-    for (int k = 0; k < I; ++k) o = __builtin_fmaf(hr[k], wd[k], o);
-    pairbuf[(size_t)(p0 + tk) * d + c] = pair_gate[p0 + tk] * o;
+    for (int k = lane; k < I; k += WAVE) o = __builtin_fmaf(hr[k], wd[k], o);
+    o = wave_tree_sum(o);
+    if (lane == 0) pairbuf[(size_t)(p0 + tk) * d + c] = pair_gate[p0 + tk] * o;
   }
 }
 
@@ -464,8 +469,8 @@ hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
                        d, I, E, ns, (const uint16_t *)w13, (const uint16_t *)w13s, units,
                        (const uint16_t *)xp, (uint16_t *)H);
   } else {
-    launch_k(k_gateup_f32, dim3(budget, (I + F32_ROWS - 1) / F32_ROWS),
-                       dim3(F32_ROWS * F32_TG), 0, st, (const float *)x, d, I,
+    launch_k(k_gateup_f32, dim3(budget, (I + F32_WAVES - 1) / F32_WAVES),
+                       dim3(F32_WAVES * WAVE), 0, st, (const float *)x, d, I,
                        E, (const float *)w13, sel_ids, n_sel, offsets, pair_tok,
                        (float *)H);
   }
@@ -484,8 +489,8 @@ hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K
                        d, I, E, ns, (const uint16_t *)w2, (const uint16_t *)w2s, units,
                        pair_gate, (const uint16_t *)H, pairbuf);
   } else {
-    launch_k(k_down_f32, dim3(budget, (d + F32_ROWS - 1) / F32_ROWS),
-                       dim3(F32_ROWS * F32_TG), 0, st, d, I, E,
+    launch_k(k_down_f32, dim3(budget, (d + F32_WAVES - 1) / F32_WAVES),
+                       dim3(F32_WAVES * WAVE), 0, st, d, I, E,
                        (const float *)w2, sel_ids, n_sel, offsets, pair_gate,
                        (const float *)H, pairbuf);
   }
