@@ -275,3 +275,12 @@ def test_calibration_validation(lib):
     assert fit(lam=(ctypes.c_double * 3)(1e-3, 0.0, 1.0)) == SHAPE
     assert fit(st=FAKE + 8) == ALIGN
     assert fit(a=FAKE + 2) == ALIGN
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    """Without the built library the binding raises: there is no CPU
+    fallback for any entry point."""
+    from paper_2609_36222_amd import binding as bd
+    monkeypatch.setattr(bd, "_lib", None)
+    with pytest.raises(ImportError, match="no CPU fallback"):
+        bd.load(str(tmp_path / "libbase.so"))
