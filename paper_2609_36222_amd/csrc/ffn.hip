@@ -415,7 +415,7 @@ void k_down_f32(int d, int I, int E, const float *__restrict__ w2,
 }
 
 constexpr int CB_THREADS = 256;
-constexpr int CB_GROUP = 8;   // ranks whose rows are in flight together
+constexpr int CB_GROUP = 4;   // ranks whose rows are in flight together
 
 template <bool BF16>
 __global__ __launch_bounds__(CB_THREADS)

@@ -33,7 +33,7 @@ constexpr int SC_WAVES = SC_WT * SC_WR;
 constexpr int SC_TB = SC_T * SC_WT;           // tokens per workgroup
 constexpr int SC_RB = SC_R * SC_WR;           // rows per workgroup
 constexpr int SC_CH = 256;                    // elements per chunk
-constexpr int SC_PF = 3;                      // chunks requested ahead (register stages)
+constexpr int SC_PF = 2;                      // chunks requested ahead (register stages)
 constexpr int SC_DOTS = SC_T * SC_R + SC_T;   // + ||x||^2 of the tile's tokens
 constexpr int SC_PAD = WAVE + 1;              // LDS row of one dot's partials
 
