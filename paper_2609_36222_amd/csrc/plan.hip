@@ -213,7 +213,7 @@ void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
 
 constexpr int BF_WAVES = 4;
 constexpr int SB_WAVES = SEL_THREADS / WAVE;   // wavefronts of k_select_backfill
-constexpr int SB_TOK = 4;                      // its tokens per workgroup (wavefronts 0 ..)
+constexpr int SB_TOK = 2;                      // its tokens per workgroup (wavefronts 0 ..)
 
 // Per-wavefront LDS of the backfill
 template <int W>
