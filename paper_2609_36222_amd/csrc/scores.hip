@@ -239,7 +239,7 @@ void k_scores(const XT *__restrict__ x, int B, int d,
   }
 }
 
-constexpr int TL_WAVES = 2;    // tokens (wavefronts) per workgroup
+constexpr int TL_WAVES = 1;    // tokens (wavefronts) per workgroup
 constexpr int TL_NI = MAX_E / WAVE;
 
 // mode bit 0: route (top-K and weights from the logits into ids / w)
