@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "../../include/base.h"
 #include "internal.hpp"
 
@@ -91,7 +93,7 @@ base_status check_ptr(const void *p, size_t a) {
 struct Layout {
   size_t logits, q, ss, gdot, topk_ids, topk_w, cost, scores, counts, sel_ids, n_sel,
       slot_of, exec_ids, exec_gates, offsets, pair_tok, pair_gate, pair_of,
-      units, xp, H, pairbuf, total;
+      hdr, parts_gu, parts_dn, xp, H, pairbuf, total;
 };
 
 size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -125,11 +127,11 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
   o.pair_tok = take(P * 4);
   o.pair_gate = take(P * 4);
   o.pair_of = take((size_t)B * (L->K + ns) * 4);
-  // the FFN's work units (bf16): gate/up workgroups, then down workgroups
-  o.units = L->dtype == BASE_BF16
-                ? take(((size_t)ffn_gu_blocks(B, L->K, bc, ns, L->I) +
-                        ffn_dn_blocks(B, L->K, bc, ns, L->d)) * sizeof(UnitRec))
-                : take(0);
+  // the FFN's part tables and their header (bf16)
+  const bool bf = L->dtype == BASE_BF16;
+  o.hdr = take(bf ? sizeof(FfnHdr) : 0);
+  o.parts_gu = take(bf ? (size_t)ffn_parts_bound(B, L->K, bc, ns, FFN_GU_PT) * sizeof(FfnPart) : 0);
+  o.parts_dn = take(bf ? (size_t)ffn_parts_bound(B, L->K, bc, ns, FFN_DN_PT) * sizeof(FfnPart) : 0);
   if (L->dtype == BASE_BF16) {
     // fragment-ordered tokens and SwiGLU activations (16-pair tiles)
     const size_t tiles = (size_t)ffn_max_tiles(B, L->K, bc, ns);
@@ -163,6 +165,23 @@ void stage_end(hipStream_t st) {
   }
 }
 
+// Compute units of the current device (queried once per device): the FFN
+// launches are sized from it.
+int device_cus() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+  const int slot = dev < 64 ? dev : 63;
+  int n = cache[slot].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      n = 256;
+    if (dev < 64) cache[slot].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
 template <typename T>
 T *at(void *ws, size_t off) {
   return reinterpret_cast<T *>(static_cast<char *>(ws) + off);
@@ -189,27 +208,29 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
                             slot_of, n_sel, exec_ids, exec_gates, st));
   stage_end(st);
   stage(4);
-  UnitRec *units = at<UnitRec>(ws, o.units);
-  UnitRec *dn_units = units + (bf16 ? ffn_gu_blocks(B, L->K, bc, L->n_shared, L->I) : 0);
   const int ns = L->n_shared;
-  // the same launch gathers the FFN's token operand and lists its work
-  // units (bf16)
+  const int n_cu = device_cus();
+  FfnHdr *hdr = at<FfnHdr>(ws, o.hdr);
+  FfnPart *parts_gu = at<FfnPart>(ws, o.parts_gu), *parts_dn = at<FfnPart>(ws, o.parts_dn);
+  // the same launch gathers the FFN's token operand and lists its parts
+  // (bf16)
   HIP_TRY(launch_compact(B, L->K, L->E, bc, ns, exec_ids, exec_gates, slot_of, n_sel,
                          shared_gate(L) ? at<float>(ws, o.gdot) : nullptr, offsets,
                          pair_tok, pair_gate, pair_of, sel_ids, bf16 ? x : nullptr, L->d,
-                         L->I, bf16 ? at<void>(ws, o.xp) : nullptr, units, st));
+                         L->I, bf16 ? at<void>(ws, o.xp) : nullptr, hdr, parts_gu, parts_dn,
+                         n_cu, st));
   stage_end(st);
   stage(5);   // no launch of its own: the gather is part of stage 4
   stage_end(st);
   stage(6);
   const bool packed = L->w_layout == BASE_W_PACKED;
   HIP_TRY(launch_gateup(bf16, packed, x, B, L->d, L->I, L->E, L->K, bc, ns, L->w13,
-                        L->w13_shared, sel_ids, n_sel, offsets, pair_tok, units,
+                        L->w13_shared, sel_ids, n_sel, offsets, pair_tok, hdr, parts_gu, n_cu,
                         at<void>(ws, o.xp), at<void>(ws, o.H), st));
   stage_end(st);
   stage(7);
   HIP_TRY(launch_down(bf16, packed, B, L->d, L->I, L->E, L->K, bc, ns, L->w2,
-                      L->w2_shared, sel_ids, n_sel, offsets, dn_units, pair_gate,
+                      L->w2_shared, sel_ids, n_sel, offsets, hdr, parts_dn, n_cu, pair_gate,
                       at<void>(ws, o.H), at<float>(ws, o.pairbuf), st));
   stage_end(st);
   stage(8);
@@ -465,20 +486,21 @@ base_status base_calib_accumulate(const base_layer *L, const void *z, int32_t B,
                           at<float>(ws, o.exec_gates), st));
   int32_t *offsets = at<int32_t>(ws, o.offsets);
   int32_t *pair_tok = at<int32_t>(ws, o.pair_tok);
-  UnitRec *units = at<UnitRec>(ws, o.units);
-  UnitRec *dn_units = units + (bf16 ? ffn_gu_blocks(B, C.K, bc, 0, C.I) : 0);
+  const int n_cu = device_cus();
+  FfnHdr *hdr = at<FfnHdr>(ws, o.hdr);
+  FfnPart *parts_gu = at<FfnPart>(ws, o.parts_gu), *parts_dn = at<FfnPart>(ws, o.parts_dn);
   HIP_TRY(launch_compact(B, C.K, C.E, bc, 0, at<int32_t>(ws, o.exec_ids),
                          at<float>(ws, o.exec_gates), slot, nsel, nullptr, offsets, pair_tok,
                          at<float>(ws, o.pair_gate), at<int32_t>(ws, o.pair_of), sel,
                          bf16 ? z : nullptr, C.d, C.I, bf16 ? at<void>(ws, o.xp) : nullptr,
-                         units, st));
+                         hdr, parts_gu, parts_dn, n_cu, st));
   const bool packed = C.w_layout == BASE_W_PACKED;
   HIP_TRY(launch_gateup(bf16, packed, z, B, C.d, C.I, C.E, C.K, bc, 0, C.w13, nullptr, sel,
-                        nsel, offsets, pair_tok, units, at<void>(ws, o.xp),
+                        nsel, offsets, pair_tok, hdr, parts_gu, n_cu, at<void>(ws, o.xp),
                         at<void>(ws, o.H), st));
   HIP_TRY(launch_down(bf16, packed, B, C.d, C.I, C.E, C.K, bc, 0, C.w2, nullptr, sel, nsel,
-                      offsets, dn_units, at<float>(ws, o.pair_gate), at<void>(ws, o.H),
-                      at<float>(ws, o.pairbuf), st));
+                      offsets, hdr, parts_dn, n_cu, at<float>(ws, o.pair_gate),
+                      at<void>(ws, o.H), at<float>(ws, o.pairbuf), st));
   double *inv = at<double>(ws, o.total);
   double *y = at<double>(ws, o.total + up256((size_t)B * 8));
   HIP_TRY(launch_calib_stats(z, bf16, B, C.d, C.E, C.K, at<float>(ws, o.pairbuf), nsel, sel,

@@ -3,12 +3,12 @@
 // only those experts' weights are read; Sec. 3.1: y_t = sum_v g_{t,v} E_v(z_t)
 // with E_v(z) = W_d (silu(W_g z) * (W_u z)).
 //
-// k_gateup (slot s, 64-row tile of I): H[p][i] = bf16(silu(g) * u) for the
-//   pairs p of slot s, g = x . W_g[i], u = x . W_u[i], fp32 accumulation on
-//   MFMA 16x16x32 bf16 (16 weight rows x 16 tokens x 32 k per instruction,
-//   tokens padded to 16).  Each workgroup streams its 64 gate rows and 64
-//   up rows of the expert once.
-// k_down (slot s, 64-row tile of d): pairbuf[p][c] = gate_p * (H[p] . W_d[c]).
+// k_gateup_bf16 (part of a kept slot's pairs, row-pair tiles of I):
+//   H[p][i] = bf16(silu(g) * u), g = x . W_g[i], u = x . W_u[i], fp32
+//   accumulation on MFMA 16x16x32 bf16 (16 weight rows x 16 tokens x 32 k
+//   per instruction, tokens padded to 16).
+// k_down_bf16 (part, row tiles of d): pairbuf[p][c] = gate_p * (H[p] . W_d[c]).
+// Each unit streams its weight rows once; see "Grouped bf16 FFN" below.
 // k_combine: y_t = residual_t + sum_j pairbuf[pair_of[t][j]] in j order
 //   (the K routed ranks, then the shared experts).
 //
@@ -21,26 +21,17 @@
 
 namespace basek {
 
-constexpr int GU_SPLIT = 4;      // gate/up: wavefronts per workgroup = contraction shares
-constexpr int DN_SPLIT = 1;      // down: one wavefront per unit
-constexpr int FF_RT = 4;         // 16-row weight tiles per wavefront
-constexpr int FF_NT = 4;         // 16-token tiles per wavefront (64 tokens)
-constexpr int FF_TOK = 16 * FF_NT;
-static_assert(FF_TOK == FFN_PART, "FFN token part");
-
-__device__ __forceinline__ bf16x8 ld_bf16x8(const uint16_t *p) {
-  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
-}
-
 __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
 // Buffer loads: a wave-uniform resource (base, size) in scalar registers,
-// a 32-bit per-lane offset, a uniform scalar offset and an immediate.  Reads
-// past the resource's size return zero instead of touching memory.
+// a 32-bit per-lane offset and a uniform scalar offset.  Reads past the
+// resource's size return zero without touching memory.
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
 constexpr int RSRC_CFG = 0x00020000;
+constexpr uint32_t OOB = 0x40000000u;   // a scalar offset past every resource used here
 
 __device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes, RSRC_CFG);
@@ -51,304 +42,371 @@ __device__ __forceinline__ bf16x8 bload(rsrc_t r, uint32_t voff, uint32_t soff) 
                             __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0));
 }
 
-// The weight operand of one wavefront: FF_RT tiles of 16 rows.
-//  packed:    one resource over the row group's stream; tile t of k-step ks
-//             at lane * 16 + t * 1024 + ks * 4096 bytes
+// 16 bytes per lane from a buffer straight into LDS: lane l's bytes land at
+// lds + 16 l (lds: uniform over the wavefront).  Counted by vmcnt like any
+// buffer load; the compiler does not track these writes, so every reader
+// waits for them explicitly (wait_vm, then a barrier).
+__device__ __forceinline__ void load_lds(rsrc_t r, void *lds, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)lds, 16, voff, soff, 0, 0);
+}
+
+// Wait until at most N vector-memory operations of this wavefront are in
+// flight (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// ----------------------------------------------------------------------------
+// Grouped bf16 FFN (K3, K4).  Work is cut by the compaction launch into
+// parts: a kept (or shared) slot's pairs, as 16-pair tiles, split into parts
+// of at most FFN_GU_PT (gate/up) or FFN_DN_PT (down) tiles of balanced size.
+// Every slot is dealt to one die (an expert's weights are read through one
+// L2, and down finds there the activations gate/up wrote), the slots with
+// several parts first, and each die's parts are consecutive rows of the
+// launch's part table (FfnPart, written by k_compact).  A unit is (part, row
+// group); the units of die x are taken by the workgroups that run on die x
+// (workgroup b runs on die b % N_XCD), workgroup b taking units b / N_XCD,
+// b / N_XCD + gridDim.x / N_XCD, ... of its die, so the heaviest parts start
+// first.
+//
+// Inside a unit every wavefront owns its rows over the whole contraction (so
+// it finishes its outputs alone, in one fixed order: k ascending), and the
+// unit's token operand is shared: for each 32-wide k-step the part's token
+// fragments (1 KiB each, fragment order, see below) are loaded once into an
+// LDS ring of DT + 1 k-steps, DT k-steps ahead (FFN_GU_DT, FFN_DN_DT), by
+// the wavefronts in turn; each wavefront requests its own weight fragments FFN_GU_DW or
+// FFN_DN_DW k-steps ahead into registers.  Per k-step: wait for this wavefront's share of the
+// k-step's token loads, meet the other wavefronts (the barrier also tells
+// every wavefront that the ring slot about to be refilled has been read),
+// read the fragments from LDS one ahead of the MFMAs, then request the next
+// k-steps.  Waves without rows in a unit (a short last row group) read past
+// their resource (zero, no memory access) and skip the MFMAs, but still take
+// their share of the token loads.
+//
+// Token operands in fragment order: the pairs of slot s occupy consecutive
+// 16-pair tiles (its i-th tile holds its pairs 16 i .. 16 i + 15, padding
+// rows zero); a tile is ksteps fragments of 1 KiB, fragment (tile, k-step) =
+// 64 lanes x 8 elements, lane l holding pair 16 i' + l % 16, elements
+// 32 k-step + 8 (l / 16) .. +7 -- the MFMA B-operand layout.
+//   xp: the pairs' hidden states (contraction d), written by k_compact with
+//       its padding rows zeroed
+//   hp: the SwiGLU activations (contraction I), written by k_gateup_bf16;
+//       its padding rows are never written (they meet only the discarded
+//       output columns of padding pairs)
+
+// The weight operand of one wavefront: one 16-row tile (two for gate/up:
+// the gate rows and their up rows).
+//  packed:    one resource over the row group's stream; the tile's fragment
+//             of k-step ks at lane * 16 + tile * 1024 + ks * 4096 bytes
 //  row-major: one resource per tile (its 16 rows); k-step ks of lane l at
 //             (l % 16) * rowbytes + (l / 16) * 16 + ks * 64 bytes
-struct WeightSrc {
-  rsrc_t r[FF_RT];
-  uint32_t voff;
+struct TileSrc {
+  rsrc_t r0, r1;       // gate/up: gate tile, up tile; down: r0 only
+  uint32_t v0, v1;     // lane offsets
+  uint32_t kstride;    // bytes per k-step (4096 packed, 64 row-major)
 };
 
-template <bool PACKED>
-__device__ __forceinline__ bf16x8 wload(const WeightSrc &w, int t, int ks) {
-  if (PACKED) return bload(w.r[0], w.voff + t * 1024, (uint32_t)ks * 4096u);
-  return bload(w.r[t], w.voff, (uint32_t)ks * 64u);
+__device__ __forceinline__ uint32_t ksoff(const TileSrc &s, int ks, int KS) {
+  return ks < KS ? (uint32_t)ks * s.kstride : OOB;
 }
 
-// Token operands in fragment order.  The pairs of kept slot s occupy
-// consecutive 16-pair tiles (its i-th tile holds its pairs 16 i .. 16 i +
-// 15, the last one padded); a part's tiles start at its tile0.
-// For a contraction of `ks` k-steps a tile is ks fragments of 1 KiB:
-// fragment (tile, k-step) = 64 lanes x 8 elements, lane l holding pair
-// 16 i' + l % 16, elements 32 k-step + 8 (l / 16) .. +7.  So every operand
-// load of the FFN reads one contiguous 1 KiB block.
-//   xp: the hidden states of the pairs (contraction d), written by the
-//       compaction launch (k_compact)
-//   hp: the SwiGLU activations (contraction I), written by k_gateup
-// Padding rows are never written; they only meet discarded output columns.
-
-// Work units: one per workgroup, unit b of a launch at units[b], written by
-// the compaction launch (see k_compact for their order and their XCD runs).
-// A gate/up unit is (slot, row group of 32 gate + 32 up rows, 64-token
-// part), a down unit (slot, row group of 64 rows of d, part); the
-// workgroup's wavefronts (GU_SPLIT, DN_SPLIT) each take an equal share of
-// the contraction and their partial sums are added through LDS in a fixed
-// order.
-struct Unit {
-  int u, p0, n, tile0, g;
+// Every value here is uniform over the workgroup and is said to be so, so
+// that the addresses derived from it stay in scalar registers (a buffer
+// resource held in vector registers would turn each load into a loop).
+struct PartU {
+  int u, tile0, nt, p0, n;
 };
-
-// Every value here is uniform over the workgroup, and is said to be so
-// (readfirstlane), so that the addresses derived from it stay in scalar
-// registers: a buffer resource held in vector registers would turn each
-// load into a loop over the lanes.
-__device__ __forceinline__ bool load_unit(const UnitRec *units, Unit &w) {
-  const UnitRec r = units[blockIdx.x];
-  w.u = __builtin_amdgcn_readfirstlane(r.u);
-  w.g = __builtin_amdgcn_readfirstlane(r.g);
-  w.p0 = __builtin_amdgcn_readfirstlane(r.p0);
-  w.n = __builtin_amdgcn_readfirstlane(r.n);
-  w.tile0 = __builtin_amdgcn_readfirstlane(r.tile0);
-  return w.u >= 0;
+__device__ __forceinline__ PartU load_part(const FfnPart *p) {
+  const FfnPart r = *p;
+  return {__builtin_amdgcn_readfirstlane(r.u), __builtin_amdgcn_readfirstlane(r.tile0),
+          __builtin_amdgcn_readfirstlane(r.nt), __builtin_amdgcn_readfirstlane(r.p0),
+          __builtin_amdgcn_readfirstlane(r.n)};
 }
 
-// One wavefront: FF_RT row tiles against NT token tiles over k-steps
-// k0 .. k0 + cnt - 1 (cnt a multiple of D).  Token fragment (j, ks) at
-// byte j * tstride + ks * 1024 + lane * 16 of resource rt.  Weights and
-// tokens are requested D k-steps ahead of their MFMAs, both at the same
-// distance: loads complete in issue order, so waiting for the oldest
-// k-step's data never waits for anything requested after it.
-template <int NT, int D, bool PACKED>
-__device__ __forceinline__ void stream_wave(const WeightSrc &ws, rsrc_t rt,
-                                            uint32_t tstride, int k0, int cnt,
-                                            f32x4 (&acc)[FF_RT][FF_NT]) {
-  const uint32_t tl = lane_id() * 16;
-  const int kend = k0 + cnt;
-  bf16x8 wb[D][FF_RT], xb[D][NT];
-#pragma unroll
-  for (int p = 0; p < D; ++p) {
-#pragma unroll
-    for (int t = 0; t < FF_RT; ++t) wb[p][t] = wload<PACKED>(ws, t, k0 + p);
-#pragma unroll
-    for (int j = 0; j < NT; ++j)
-      xb[p][j] = bload(rt, tl + j * tstride, (uint32_t)(k0 + p) * 1024u);
+// One unit of gate/up: wavefront w owns row-pair tile r = rp0 + w (gate rows
+// 16 r .. 16 r + 15 and their up rows I + 16 r ..), if w < nrp.  NT: the
+// part's tile count.  Writes H = bf16(silu(g) * u) in fragment order: column
+// i = 16 r + 4 (l / 16) + q of pair tk sits in fragment (tile of tk, k-step
+// r / 2), lane tk % 16 + 16 (2 (r % 2) + (l / 16) / 2), element
+// 4 ((l / 16) % 2) + q.
+template <int NT, bool PACKED>
+__device__ __forceinline__ void gateup_unit(uint8_t *ring, uint8_t *dummy, int d, int I,
+                                            const uint16_t *__restrict__ w13, const PartU &pt,
+                                            int rp0, int nrp, const uint16_t *__restrict__ xp,
+                                            uint16_t *__restrict__ hp) {
+  constexpr int W = FFN_WAVES, DW = FFN_GU_DW, DT = FFN_GU_DT;
+  constexpr int NTK = (NT + W - 1) / W;   // token loads per wavefront per k-step
+  const int w = wave_id_u(), lane = lane_id();
+  const int KS = d / 32;
+  const bool active = w < nrp;
+  const int r = rp0 + (active ? w : 0);
+  TileSrc ws;
+  if (PACKED) {
+    const uint32_t gbytes = (uint32_t)KS * 4096u;
+    ws.r0 = make_rsrc(w13 + ((size_t)pt.u * (I / 32) + (r >> 1)) * (gbytes / 2),
+                      active ? gbytes : 0u);
+    ws.r1 = ws.r0;
+    ws.v0 = lane * 16 + (r & 1) * 1024;
+    ws.v1 = ws.v0 + 2048;
+    ws.kstride = 4096;
+  } else {
+    const uint32_t tb = (uint32_t)(16 * d * 2);
+    ws.r0 = make_rsrc(w13 + ((size_t)pt.u * 2 * I + 16 * r) * d, active ? tb : 0u);
+    ws.r1 = make_rsrc(w13 + ((size_t)pt.u * 2 * I + I + 16 * r) * d, active ? tb : 0u);
+    ws.v0 = ws.v1 = (uint32_t)(lane & 15) * (uint32_t)(d * 2) + (uint32_t)(lane >> 4) * 16u;
+    ws.kstride = 64;
   }
-  int ks = k0;
-  for (; ks + D < kend; ks += D) {
+  const uint32_t tbytes = (uint32_t)KS * 1024u;
+  const rsrc_t rt = make_rsrc(xp + (size_t)pt.tile0 * (tbytes / 2), (uint32_t)pt.nt * tbytes);
+  const uint32_t vl = lane * 16;
+  auto tok_load = [&](int ks) {
+    uint8_t *slot = ring + (ks % (DT + 1)) * (NT * 1024);
 #pragma unroll
-    for (int p = 0; p < D; ++p) {
+    for (int q = 0; q < NTK; ++q) {
+      const int j = w + W * q;
+      if (j < NT)
+        load_lds(rt, slot + j * 1024, vl,
+                 ks < KS ? (uint32_t)j * tbytes + (uint32_t)ks * 1024u : OOB);
+      else
+        load_lds(rt, dummy + w * 1024, vl, OOB);
+    }
+  };
+  f32x4 ag[NT], au[NT];
 #pragma unroll
-      for (int j = 0; j < NT; ++j)
+  for (int j = 0; j < NT; ++j) { ag[j] = f32x4{0, 0, 0, 0}; au[j] = f32x4{0, 0, 0, 0}; }
+  // the first token loads before the first weight loads: the wait of
+  // k-step ks below allows (DT - 1) * (2 + NTK) younger loads, and for the
+  // first k-steps the prologue's weight loads are among them
 #pragma unroll
-        for (int t = 0; t < FF_RT; ++t) acc[t][j] = mfma16(wb[p][t], xb[p][j], acc[t][j]);
-      const int kn = ks + D + p;
+  for (int p = 0; p < DT; ++p) tok_load(p);
+  bf16x8 wg[DW], wu[DW];
 #pragma unroll
-      for (int t = 0; t < FF_RT; ++t) wb[p][t] = wload<PACKED>(ws, t, kn);
+  for (int p = 0; p < DW; ++p) {
+    wg[p] = bload(ws.r0, ws.v0, ksoff(ws, p, KS));
+    wu[p] = bload(ws.r1, ws.v1, ksoff(ws, p, KS));
+  }
+  for (int k0 = 0; k0 < KS; k0 += DW) {
 #pragma unroll
-      for (int j = 0; j < NT; ++j) xb[p][j] = bload(rt, tl + j * tstride, (uint32_t)kn * 1024u);
-      // keep this k-step's refill here: sunk to the end of the loop, the
-      // refills of all D k-steps would wait for nearly every load in flight
+    for (int p = 0; p < DW; ++p) {
+      const int ks = k0 + p;
+      // this wavefront's loads of k-step ks are done: at most the loads of
+      // the DT - 1 later iterations are in flight
+      wait_vm<(DT - 1) * (2 + NTK)>();
+      wg_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      if (active) {
+        const uint8_t *sb = ring + (ks % (DT + 1)) * (NT * 1024) + lane * 16;
+        bf16x8 xc = *reinterpret_cast<const bf16x8 *>(sb);
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+          bf16x8 xn = xc;
+          if (j + 1 < NT) xn = *reinterpret_cast<const bf16x8 *>(sb + (j + 1) * 1024);
+          ag[j] = mfma16(wg[p], xc, ag[j]);
+          au[j] = mfma16(wu[p], xc, au[j]);
+          __builtin_amdgcn_sched_barrier(0);
+          xc = xn;
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      wg[p] = bload(ws.r0, ws.v0, ksoff(ws, ks + DW, KS));
+      wu[p] = bload(ws.r1, ws.v1, ksoff(ws, ks + DW, KS));
+      tok_load(ks + DT);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
+  wait_vm<0>();
+  if (!active) return;
+  const int row = lane & 15, g = r >> 1, t = r & 1;
 #pragma unroll
-  for (int p = 0; p < D; ++p)
-#pragma unroll
-    for (int j = 0; j < NT; ++j)
-#pragma unroll
-      for (int t = 0; t < FF_RT; ++t) acc[t][j] = mfma16(wb[p][t], xb[p][j], acc[t][j]);
-}
-
-template <int NT, bool PACKED>
-__device__ __forceinline__ void stream_wave_d(const WeightSrc &ws, rsrc_t rt,
-                                              uint32_t tstride, int k0, int cnt,
-                                              f32x4 (&acc)[FF_RT][FF_NT]) {
-  if (cnt % 4 == 0) stream_wave<NT, 4, PACKED>(ws, rt, tstride, k0, cnt, acc);
-  else if (cnt % 2 == 0) stream_wave<NT, 2, PACKED>(ws, rt, tstride, k0, cnt, acc);
-  else stream_wave<NT, 1, PACKED>(ws, rt, tstride, k0, cnt, acc);
-}
-
-// This wavefront's share of a unit's contraction (ksteps k-steps of 32)
-// when S wavefronts split it: k-steps [w ksteps / S, (w + 1) ksteps / S);
-// possibly empty.
-template <int S, bool PACKED>
-__device__ __forceinline__ void stream_share(int nt, const WeightSrc &ws, rsrc_t rt,
-                                             uint32_t tstride, int ksteps,
-                                             f32x4 (&acc)[FF_RT][FF_NT]) {
-#pragma unroll
-  for (int t = 0; t < FF_RT; ++t)
-#pragma unroll
-    for (int j = 0; j < FF_NT; ++j) acc[t][j] = f32x4{0, 0, 0, 0};
-  const int w = wave_id();
-  const int k0 = __builtin_amdgcn_readfirstlane(ksteps * w / S);
-  const int cnt = __builtin_amdgcn_readfirstlane(ksteps * (w + 1) / S) - k0;
-  if (cnt <= 0) return;
-  switch (nt) {
-    case 1: stream_wave_d<1, PACKED>(ws, rt, tstride, k0, cnt, acc); break;
-    case 2: stream_wave_d<2, PACKED>(ws, rt, tstride, k0, cnt, acc); break;
-    case 3: stream_wave_d<3, PACKED>(ws, rt, tstride, k0, cnt, acc); break;
-    default: stream_wave_d<4, PACKED>(ws, rt, tstride, k0, cnt, acc); break;
-  }
-}
-
-// Partial sums of the S wavefronts: [wave][row tile][token tile][lane]
-template <int S>
-struct Partials {
-  f32x4 v[S][FF_RT][FF_NT][WAVE];
-};
-
-// The gate/up exchange as a reduce-scatter: wavefront W finishes gate tile
-// W % 2 with its up tile for the token tiles j = W / 2 (mod 2); it keeps
-// those partial sums in registers and writes only the other twelve tiles.
-// Every sum still runs over the wavefronts in order 0 .. 3.
-template <int W>
-__device__ __forceinline__ bool rs_own(int t, int j) {
-  return (t % 2) == (W % 2) && (j % 2) == (W / 2);
-}
-template <int W>
-__device__ __forceinline__ void put_partials_rs(Partials<GU_SPLIT> &sh, int nt,
-                                                const f32x4 (&acc)[FF_RT][FF_NT]) {
-  const int l = lane_id();
-#pragma unroll
-  for (int t = 0; t < FF_RT; ++t)
-#pragma unroll
-    for (int j = 0; j < FF_NT; ++j)
-      if (j < nt && !rs_own<W>(t, j)) sh.v[W][t][j][l] = acc[t][j];
-}
-template <int W>
-__device__ __forceinline__ f32x4 sum_rs(const Partials<GU_SPLIT> &sh, const f32x4 &own,
-                                        int t, int j) {
-  const int l = lane_id();
-  f32x4 r = W == 0 ? own : sh.v[0][t][j][l];
-#pragma unroll
-  for (int w = 1; w < GU_SPLIT; ++w) r += (w == W) ? own : sh.v[w][t][j][l];
-  return r;
-}
-template <int W>
-__device__ __forceinline__ void gu_epilogue(const Partials<GU_SPLIT> &sh,
-                                            const f32x4 (&acc)[FF_RT][FF_NT], int nt, int n,
-                                            int I, int g, int tile0, uint16_t *hp) {
-  const int lane = lane_id(), row = lane & 15;
-  constexpr int t = W % 2;
-#pragma unroll
-  for (int jj = 0; jj < FF_NT * 2 / GU_SPLIT; ++jj) {
-    const int j = W / 2 + (GU_SPLIT / 2) * jj;
+  for (int j = 0; j < NT; ++j) {
     const int tk = 16 * j + row;
-    if (j < nt && tk < n) {
-      const f32x4 ga = sum_rs<W>(sh, acc[t][j], t, j), up = sum_rs<W>(sh, acc[t + 2][j], t + 2, j);
+    if (tk < pt.n) {
       uint16_t h[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) h[r] = f32_to_bf16(silu_bf16(ga[r]) * up[r]);
-      u32x2 pk = {(uint32_t)h[0] | ((uint32_t)h[1] << 16),
-                  (uint32_t)h[2] | ((uint32_t)h[3] << 16)};
-      uint16_t *frag = hp + (((size_t)(tile0 + j) * (I / 32) + g) * WAVE) * 8;
+      for (int q = 0; q < 4; ++q) h[q] = f32_to_bf16(silu_bf16(ag[j][q]) * au[j][q]);
+      const u32x2 pk = {(uint32_t)h[0] | ((uint32_t)h[1] << 16),
+                        (uint32_t)h[2] | ((uint32_t)h[3] << 16)};
+      uint16_t *frag = hp + (((size_t)(pt.tile0 + j) * (I / 32) + g) * WAVE) * 8;
       const int l2 = row + 16 * (2 * t + (lane >> 5));
       *reinterpret_cast<u32x2 *>(frag + l2 * 8 + 4 * ((lane >> 4) & 1)) = pk;
     }
   }
 }
 
-// gate/up: row group g = gate rows 32 g .. 32 g + 31 (tiles 0, 1) and up
-// rows I + 32 g .. I + 32 g + 31 (tiles 2, 3).  Writes H in fragment order:
-// SwiGLU column i = 32 g + 16 t + 4 (l / 16) + r of pair tk sits in
-// fragment (tile of tk, k-step g), lane tk % 16 + 16 (2 t + (l / 16) / 2),
-// element 4 ((l / 16) % 2) + r.  After the partial sums are exchanged,
-// every wavefront finishes a share of the (gate tile, token tile) pairs.
-template <bool PACKED>
-__global__ __launch_bounds__(GU_SPLIT * WAVE, 2)
-void k_gateup_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w13r,
-                   const uint16_t *__restrict__ w13s,
-                   const UnitRec *__restrict__ units,
-                   const uint16_t *__restrict__ xp, uint16_t *__restrict__ hp) {
-  __shared__ Partials<GU_SPLIT> sh;
-  const int groups = I / 32;
-  Unit un;
-  if (!load_unit(units, un)) return;
-  if (un.u < 0 || un.u >= E + ns) return;   // only for a plan not made by base_select
-  // experts E .. E + ns - 1 are the shared ones
-  const uint16_t *w13 = un.u < E ? w13r : w13s;
-  const int u = un.u < E ? un.u : un.u - E, n = un.n, tile0 = un.tile0;
-  const int nt = (n + 15) / 16;
-  const int lane = lane_id(), row = lane & 15, g = un.g;
-  WeightSrc ws;
+// One unit of down: wavefront w owns row tile rt = rt0 + w (rows 16 rt ..
+// 16 rt + 15 of W_d), if w < nrt; the tokens are the part's SwiGLU
+// activations.  pairbuf[p][c] = gate_p * (H[p] . W_d[c]).
+template <int NT, bool PACKED>
+__device__ __forceinline__ void down_unit(uint8_t *ring, uint8_t *dummy, int d, int I,
+                                          const uint16_t *__restrict__ w2, const PartU &pt,
+                                          int rt0, int nrt, const float *__restrict__ pair_gate,
+                                          const uint16_t *__restrict__ hp,
+                                          float *__restrict__ pairbuf) {
+  constexpr int W = FFN_WAVES, DW = FFN_DN_DW, DT = FFN_DN_DT;
+  constexpr int NTK = (NT + W - 1) / W;
+  const int w = wave_id_u(), lane = lane_id();
+  const int KS = I / 32;
+  const bool active = w < nrt;
+  const int rtile = rt0 + (active ? w : 0);
+  TileSrc ws;
   if (PACKED) {
-    const uint32_t bytes = (uint32_t)(d / 32) * 4096u;
-    ws.r[0] = make_rsrc(w13 + ((size_t)u * groups + g) * (size_t)bytes / 2, bytes);
-    ws.voff = lane * 16;
+    const uint32_t gbytes = (uint32_t)KS * 4096u;
+    ws.r0 = make_rsrc(w2 + ((size_t)pt.u * (d / 64) + (rtile >> 2)) * (gbytes / 2),
+                      active ? gbytes : 0u);
+    ws.v0 = lane * 16 + (rtile & 3) * 1024;
+    ws.kstride = 4096;
   } else {
-#pragma unroll
-    for (int t = 0; t < FF_RT; ++t)
-      ws.r[t] = make_rsrc(w13 + ((size_t)u * 2 * I + (t < 2 ? 0 : I) + 32 * g + 16 * (t & 1)) * d,
-                          (uint32_t)(16 * d * 2));
-    ws.voff = (uint32_t)row * (uint32_t)(d * 2) + (uint32_t)(lane >> 4) * 16u;
+    ws.r0 = make_rsrc(w2 + ((size_t)pt.u * d + 16 * rtile) * I,
+                      active ? (uint32_t)(16 * I * 2) : 0u);
+    ws.v0 = (uint32_t)(lane & 15) * (uint32_t)(I * 2) + (uint32_t)(lane >> 4) * 16u;
+    ws.kstride = 64;
   }
-  const uint32_t tstride = (uint32_t)(d / 32) * 1024u;        // one tile
-  const rsrc_t rt = make_rsrc(xp + (size_t)tile0 * (d / 32) * 512, (uint32_t)nt * tstride);
-  f32x4 acc[FF_RT][FF_NT];
-  stream_share<GU_SPLIT, PACKED>(nt, ws, rt, tstride, d / 32, acc);
-  // the SwiGLU of the 2 gate tiles x FF_NT token tiles, spread over the
-  // wavefronts (template argument: the wavefront, so that the tiles it
-  // keeps are fixed registers)
-  static_assert(GU_SPLIT == 4, "reduce-scatter exchange");
-  switch (wave_id()) {
-    case 0: put_partials_rs<0>(sh, nt, acc); break;
-    case 1: put_partials_rs<1>(sh, nt, acc); break;
-    case 2: put_partials_rs<2>(sh, nt, acc); break;
-    default: put_partials_rs<3>(sh, nt, acc); break;
+  ws.r1 = ws.r0;
+  ws.v1 = ws.v0;
+  const uint32_t tbytes = (uint32_t)KS * 1024u;
+  const rsrc_t rt = make_rsrc(hp + (size_t)pt.tile0 * (tbytes / 2), (uint32_t)pt.nt * tbytes);
+  const uint32_t vl = lane * 16;
+  const int row = lane & 15;
+  // the gates first: loaded after the contraction, each would wait behind
+  // the previous tile's stores
+  float gt[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) gt[j] = pair_gate[pt.p0 + min(16 * j + row, pt.n - 1)];
+  auto tok_load = [&](int ks) {
+    uint8_t *slot = ring + (ks % (DT + 1)) * (NT * 1024);
+#pragma unroll
+    for (int q = 0; q < NTK; ++q) {
+      const int j = w + W * q;
+      if (j < NT)
+        load_lds(rt, slot + j * 1024, vl,
+                 ks < KS ? (uint32_t)j * tbytes + (uint32_t)ks * 1024u : OOB);
+      else
+        load_lds(rt, dummy + w * 1024, vl, OOB);
+    }
+  };
+  f32x4 acc[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) acc[j] = f32x4{0, 0, 0, 0};
+  bf16x8 wb[DW];
+  // token loads next, then the weights (see gateup_unit); the gate loads are
+  // older still, so the first k-step's wait also covers them (their L2 round
+  // trip overlaps the first weights' HBM one)
+#pragma unroll
+  for (int p = 0; p < DT; ++p) tok_load(p);
+#pragma unroll
+  for (int p = 0; p < DW; ++p) wb[p] = bload(ws.r0, ws.v0, ksoff(ws, p, KS));
+  for (int k0 = 0; k0 < KS; k0 += DW) {
+#pragma unroll
+    for (int p = 0; p < DW; ++p) {
+      const int ks = k0 + p;
+      wait_vm<(DT - 1) * (1 + NTK)>();
+      wg_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      if (active) {
+        const uint8_t *sb = ring + (ks % (DT + 1)) * (NT * 1024) + lane * 16;
+        bf16x8 xc = *reinterpret_cast<const bf16x8 *>(sb);
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+          bf16x8 xn = xc;
+          if (j + 1 < NT) xn = *reinterpret_cast<const bf16x8 *>(sb + (j + 1) * 1024);
+          acc[j] = mfma16(wb[p], xc, acc[j]);
+          __builtin_amdgcn_sched_barrier(0);
+          xc = xn;
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      wb[p] = bload(ws.r0, ws.v0, ksoff(ws, ks + DW, KS));
+      tok_load(ks + DT);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
-  __syncthreads();
-  switch (wave_id()) {
-    case 0: gu_epilogue<0>(sh, acc, nt, n, I, g, tile0, hp); break;
-    case 1: gu_epilogue<1>(sh, acc, nt, n, I, g, tile0, hp); break;
-    case 2: gu_epilogue<2>(sh, acc, nt, n, I, g, tile0, hp); break;
-    default: gu_epilogue<3>(sh, acc, nt, n, I, g, tile0, hp); break;
-  }
-}
-
-// down: row group g = rows 64 g .. 64 g + 63 of W_d (tiles 0..3); tokens
-// are the SwiGLU activations in fragment order.  One wavefront per unit.
-template <bool PACKED>
-__global__ __launch_bounds__(DN_SPLIT * WAVE, 2)
-void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
-                 const uint16_t *__restrict__ w2s,
-                 const UnitRec *__restrict__ units,
-                 const float *__restrict__ pair_gate,
-                 const uint16_t *__restrict__ hp, float *__restrict__ pairbuf) {
-  static_assert(DN_SPLIT == 1, "the down epilogue takes the accumulators as they are");
-  const int groups = d / 64;
-  Unit un;
-  if (!load_unit(units, un)) return;
-  if (un.u < 0 || un.u >= E + ns) return;   // only for a plan not made by base_select
-  const uint16_t *w2 = un.u < E ? w2r : w2s;
-  const int u = un.u < E ? un.u : un.u - E, n = un.n, tile0 = un.tile0, p0 = un.p0;
-  const int nt = (n + 15) / 16;
-  const int lane = lane_id(), row = lane & 15, g = un.g;
-  WeightSrc ws;
-  if (PACKED) {
-    const uint32_t bytes = (uint32_t)(I / 32) * 4096u;
-    ws.r[0] = make_rsrc(w2 + ((size_t)u * groups + g) * (size_t)bytes / 2, bytes);
-    ws.voff = lane * 16;
-  } else {
+  wait_vm<0>();
+  if (!active) return;
 #pragma unroll
-    for (int t = 0; t < FF_RT; ++t)
-      ws.r[t] = make_rsrc(w2 + ((size_t)u * d + 64 * g + 16 * t) * I, (uint32_t)(16 * I * 2));
-    ws.voff = (uint32_t)row * (uint32_t)(I * 2) + (uint32_t)(lane >> 4) * 16u;
-  }
-  // the gates first: loaded after the contraction, each would sit behind
-  // the previous tile's stores in the memory counter
-  float gt[FF_NT];
-#pragma unroll
-  for (int j = 0; j < FF_NT; ++j) gt[j] = pair_gate[p0 + min(16 * j + row, n - 1)];
-  const uint32_t tstride = (uint32_t)(I / 32) * 1024u;
-  const rsrc_t rt = make_rsrc(hp + (size_t)tile0 * (I / 32) * 512, (uint32_t)nt * tstride);
-  f32x4 acc[FF_RT][FF_NT];
-  stream_share<DN_SPLIT, PACKED>(nt, ws, rt, tstride, I / 32, acc);
-  // one wavefront per unit: its accumulators are the sums
-#pragma unroll
-  for (int t = 0; t < FF_RT; ++t)
-#pragma unroll
-  for (int j = 0; j < FF_NT; ++j) {
+  for (int j = 0; j < NT; ++j) {
     const int tk = 16 * j + row;
-    if (j < nt && tk < n) {
-      const f32x4 o = acc[t][j];
-      float4 v = {gt[j] * o[0], gt[j] * o[1], gt[j] * o[2], gt[j] * o[3]};
-      *reinterpret_cast<float4 *>(pairbuf + (size_t)(p0 + tk) * d + 64 * g + 16 * t +
+    if (tk < pt.n) {
+      const f32x4 o = acc[j];
+      const float4 v = {gt[j] * o[0], gt[j] * o[1], gt[j] * o[2], gt[j] * o[3]};
+      *reinterpret_cast<float4 *>(pairbuf + (size_t)(pt.p0 + tk) * d + 16 * rtile +
                                   4 * (lane >> 4)) = v;
     }
   }
 }
+
+// The units of this workgroup's die, in order: unit m of die x is the die's
+// part m / upp (table rows die[x] .. die[x + 1] - 1), row group m % upp.
+// Returns false past the die's last unit.
+__device__ __forceinline__ bool next_unit(const int32_t *die, int m, int upp, int &k, int &rg) {
+  const int x = (int)(blockIdx.x % N_XCD);
+  k = __builtin_amdgcn_readfirstlane(die[x]) + m / upp;
+  rg = m % upp;
+  return k < __builtin_amdgcn_readfirstlane(die[x + 1]);
+}
+
+// gate/up: up to FFN_WAVES row-pair tiles per unit (hdr->rp_gu, chosen by
+// the compaction launch), the part's tiles shared through the LDS ring.
+template <bool PACKED>
+__global__ __launch_bounds__(FFN_WAVES * WAVE)
+void k_gateup_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w13r,
+                   const uint16_t *__restrict__ w13s, const FfnHdr *__restrict__ hdr,
+                   const FfnPart *__restrict__ parts, const uint16_t *__restrict__ xp,
+                   uint16_t *__restrict__ hp) {
+  __shared__ __attribute__((aligned(16))) uint8_t ring[(FFN_GU_DT + 1) * FFN_GU_PT * 1024];
+  __shared__ __attribute__((aligned(16))) uint8_t dummy[FFN_WAVES * 1024];
+  const int RP = __builtin_amdgcn_readfirstlane(hdr->rp_gu);
+  const int T = I / 16;                    // row-pair tiles per expert
+  if (RP < 1 || RP > FFN_WAVES) return;    // only for a plan not made by k_compact
+  const int upp = (T + RP - 1) / RP;
+  const int step = (int)(gridDim.x / N_XCD);
+  int k, rg;
+  for (int m = (int)(blockIdx.x / N_XCD); next_unit(hdr->die_gu, m, upp, k, rg); m += step) {
+    const PartU pt = load_part(parts + k);
+    if (pt.u < 0 || pt.u >= E + ns || pt.nt < 1 || pt.nt > FFN_GU_PT) continue;
+    const uint16_t *w13 = pt.u < E ? w13r : w13s;
+    PartU q = pt;
+    q.u = pt.u < E ? pt.u : pt.u - E;   // experts E .. E + ns - 1: the shared ones
+    const int rp0 = rg * RP, nrp = min(RP, T - rp0);
+    wg_barrier();   // every wavefront is done with the previous unit's ring
+#define BASE_GU(N) case N: gateup_unit<N, PACKED>(ring, dummy, d, I, w13, q, rp0, nrp, xp, hp); break;
+    switch (q.nt) { BASE_GU(1) BASE_GU(2) BASE_GU(3) BASE_GU(4) BASE_GU(5) default: BASE_GU(6) }
+#undef BASE_GU
+  }
+}
+static_assert(FFN_GU_PT == 6, "gate/up tile-count cases");
+
+// down: FFN_WAVES row tiles of 16 rows of d per unit; registers for two
+// workgroups per CU (four wavefronts per SIMD).
+template <bool PACKED>
+__global__ __launch_bounds__(FFN_WAVES * WAVE, FFN_DN_WPE)
+void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
+                 const uint16_t *__restrict__ w2s, const FfnHdr *__restrict__ hdr,
+                 const FfnPart *__restrict__ parts, const float *__restrict__ pair_gate,
+                 const uint16_t *__restrict__ hp, float *__restrict__ pairbuf) {
+  __shared__ __attribute__((aligned(16))) uint8_t ring[(FFN_DN_DT + 1) * FFN_DN_PT * 1024];
+  __shared__ __attribute__((aligned(16))) uint8_t dummy[FFN_WAVES * 1024];
+  const int T = d / 16;                    // row tiles per expert
+  const int upp = (T + FFN_WAVES - 1) / FFN_WAVES;
+  const int step = (int)(gridDim.x / N_XCD);
+  int k, rg;
+  for (int m = (int)(blockIdx.x / N_XCD); next_unit(hdr->die_dn, m, upp, k, rg); m += step) {
+    const PartU pt = load_part(parts + k);
+    if (pt.u < 0 || pt.u >= E + ns || pt.nt < 1 || pt.nt > FFN_DN_PT) continue;
+    const uint16_t *w2 = pt.u < E ? w2r : w2s;
+    PartU q = pt;
+    q.u = pt.u < E ? pt.u : pt.u - E;
+    const int rt0 = rg * FFN_WAVES, nrt = min(FFN_WAVES, T - rt0);
+    wg_barrier();
+#define BASE_DN(N) case N: down_unit<N, PACKED>(ring, dummy, d, I, w2, q, rt0, nrt, pair_gate, hp, pairbuf); break;
+    switch (q.nt) { BASE_DN(1) BASE_DN(2) BASE_DN(3) BASE_DN(4) BASE_DN(5) BASE_DN(6) BASE_DN(7) default: BASE_DN(8) }
+#undef BASE_DN
+  }
+}
+static_assert(FFN_DN_PT == 8, "down tile-count cases");
 
 // fp32 experts (small layers): one wavefront per (kept slot, output row).
 // The lanes split the contraction (lane l takes elements l, l + 64, ..., so
@@ -462,12 +520,12 @@ hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
                          int I, int E, int K, int budget, int ns, const void *w13,
                          const void *w13s, const int32_t *sel_ids, const int32_t *n_sel,
                          const int32_t *offsets, const int32_t *pair_tok,
-                         const UnitRec *units, const void *xp, void *H, hipStream_t st) {
+                         const FfnHdr *hdr, const FfnPart *parts, int n_cu, const void *xp,
+                         void *H, hipStream_t st) {
   if (bf16) {
-    launch_k(packed ? k_gateup_bf16<true> : k_gateup_bf16<false>,
-                       dim3(ffn_gu_blocks(B, K, budget, ns, I)), dim3(GU_SPLIT * WAVE), 0, st,
-                       d, I, E, ns, (const uint16_t *)w13, (const uint16_t *)w13s, units,
-                       (const uint16_t *)xp, (uint16_t *)H);
+    launch_k(packed ? k_gateup_bf16<true> : k_gateup_bf16<false>, dim3(ffn_gu_grid(n_cu)),
+             dim3(FFN_WAVES * WAVE), 0, st, d, I, E, ns, (const uint16_t *)w13,
+             (const uint16_t *)w13s, hdr, parts, (const uint16_t *)xp, (uint16_t *)H);
   } else {
     launch_k(k_gateup_f32, dim3(budget, (I + F32_WAVES - 1) / F32_WAVES),
                        dim3(F32_WAVES * WAVE), 0, st, (const float *)x, d, I,
@@ -481,13 +539,12 @@ hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K
                        int budget, int ns, const void *w2, const void *w2s,
                        const int32_t *sel_ids,
                        const int32_t *n_sel, const int32_t *offsets,
-                       const UnitRec *units, const float *pair_gate, const void *H,
-                       float *pairbuf, hipStream_t st) {
+                       const FfnHdr *hdr, const FfnPart *parts, int n_cu,
+                       const float *pair_gate, const void *H, float *pairbuf, hipStream_t st) {
   if (bf16) {
-    launch_k(packed ? k_down_bf16<true> : k_down_bf16<false>,
-                       dim3(ffn_dn_blocks(B, K, budget, ns, d)), dim3(DN_SPLIT * WAVE), 0, st,
-                       d, I, E, ns, (const uint16_t *)w2, (const uint16_t *)w2s, units,
-                       pair_gate, (const uint16_t *)H, pairbuf);
+    launch_k(packed ? k_down_bf16<true> : k_down_bf16<false>, dim3(ffn_dn_grid(n_cu)),
+             dim3(FFN_WAVES * WAVE), 0, st, d, I, E, ns, (const uint16_t *)w2,
+             (const uint16_t *)w2s, hdr, parts, pair_gate, (const uint16_t *)H, pairbuf);
   } else {
     launch_k(k_down_f32, dim3(budget, (d + F32_WAVES - 1) / F32_WAVES),
                        dim3(F32_WAVES * WAVE), 0, st, d, I, E,

@@ -11,7 +11,7 @@ namespace basek {
 constexpr int MAX_K = 16;     // experts per token
 constexpr int MAX_E = 256;    // experts per layer
 constexpr int MAX_B = 1024;   // tokens per batch
-constexpr int FFN_PART = 64;  // tokens of one FFN wavefront (4 MFMA tiles)
+constexpr int FFN_PART = 64;  // tokens per task of the FFN's token gather
 
 // Events attached to the next kernel launch (per host thread): when set,
 // launch_k hands them to the dispatch itself, which records `start` as the
@@ -34,11 +34,13 @@ inline void launch_k(F kernel, dim3 grid, dim3 block, uint32_t shm, hipStream_t 
   }
 }
 
+constexpr int N_XCD = 8;   // accelerator dies, one L2 each
+
 constexpr int MAX_SHARED = 8;               // shared experts per layer
 constexpr int MAX_SLOTS = MAX_E + MAX_SHARED;  // kept slots + shared slots
 
 // Upper bounds (host-known) of the FFN token tiling for a batch: 16-pair
-// tiles and FFN_PART-token parts over all kept slots and the ns shared
+// tiles and FFN_PART-token gather tasks over all kept slots and the ns shared
 // slots (B pairs each).
 inline int ffn_max_tiles(int B, int K, int budget, int ns) {
   return (B * K + 15) / 16 + budget + ns * ((B + 15) / 16);
@@ -47,28 +49,51 @@ inline int ffn_max_parts(int B, int K, int budget, int ns) {
   return (B * K + FFN_PART - 1) / FFN_PART + budget + ns * ((B + FFN_PART - 1) / FFN_PART);
 }
 
-// One FFN work unit: expert u (u >= E: shared expert u - E; -1: no unit),
-// its row group g, its pairs p0 .. p0 + n - 1 in the compacted order and
-// their first 16-pair tile.
-struct alignas(32) UnitRec {
-  int32_t u, g, p0, n, tile0, pad0, pad1, pad2;
+// The grouped bf16 FFN (see "Grouped bf16 FFN" in ffn.hip).  A part is at
+// most FFN_GU_PT (gate/up) or FFN_DN_PT (down) 16-pair tiles of one kept or
+// shared slot; a unit of work is (part, row group), one per workgroup of
+// FFN_WAVES wavefronts at a time, each wavefront owning 16-row tiles over the
+// whole contraction with weights requested FFN_GU_DW (gate/up) or FFN_DN_DW
+// (down) k-steps ahead and token fragments FFN_GU_DT or FFN_DN_DT k-steps
+// ahead.
+constexpr int FFN_WAVES = 8;
+constexpr int FFN_GU_DW = 8;
+constexpr int FFN_GU_DT = 2;
+constexpr int FFN_DN_DW = 3;
+constexpr int FFN_DN_DT = 3;
+// wavefronts per SIMD the down kernel's registers allow: three workgroups
+// per CU, so that a die's down units mostly run in one round
+constexpr int FFN_DN_WPE = 6;
+constexpr int FFN_GU_PT = 6;
+constexpr int FFN_DN_PT = 8;
+
+// A part of a slot's pairs: expert u (u >= E: shared expert u - E), its
+// first 16-pair tile in the token operand, its tile count, its first pair
+// in the compacted order and its pair count.
+struct alignas(32) FfnPart {
+  int32_t u, tile0, nt, p0, n, pad0, pad1, pad2;
+};
+// The part tables' layout and gate/up's row group (row-pair tiles per
+// unit), written by the compaction launch: the parts of die x are rows
+// die_gu[x] .. die_gu[x + 1] - 1 of the gate/up table (die_dn: the down
+// table).
+struct alignas(16) FfnHdr {
+  int32_t rp_gu, pad0;
+  int32_t die_gu[N_XCD + 1], die_dn[N_XCD + 1];
 };
 
-constexpr int N_XCD = 8;   // accelerator dies, one L2 each
 
-// Workgroups for up to `units` units: a multiple of N_XCD, so that every
-// XCD's run of units has all its workgroups.
-inline unsigned ffn_grid(long long units) {
-  return (unsigned)(((units + N_XCD - 1) / N_XCD) * N_XCD);
+// Upper bound of the parts of a launch with at most pt tiles per part: the
+// sum over slots of ceil(tiles / pt) is below tiles / pt + slots.
+inline int ffn_parts_bound(int B, int K, int budget, int ns, int pt) {
+  return ffn_max_tiles(B, K, budget, ns) / pt + budget + ns + 1;
 }
-// The FFN launches' workgroups (bf16): gate/up row groups of 32 gate + 32
-// up rows, down row groups of 64 rows of d, one unit per workgroup.
-inline unsigned ffn_gu_blocks(int B, int K, int budget, int ns, int I) {
-  return ffn_grid((long long)ffn_max_parts(B, K, budget, ns) * (I / 32));
-}
-inline unsigned ffn_dn_blocks(int B, int K, int budget, int ns, int d) {
-  return ffn_grid((long long)ffn_max_parts(B, K, budget, ns) * (d / 64));
-}
+// Workgroups of the FFN launches: a multiple of N_XCD, from the device's
+// compute units -- gate/up one per CU (its registers allow no second), down
+// three per CU (FFN_DN_WPE).
+__host__ __device__ inline unsigned ffn_cu_grid(int n_cu) { return (unsigned)(((n_cu + N_XCD - 1) / N_XCD) * N_XCD); }
+__host__ __device__ inline unsigned ffn_gu_grid(int n_cu) { return ffn_cu_grid(n_cu); }
+__host__ __device__ inline unsigned ffn_dn_grid(int n_cu) { return 3u * ffn_cu_grid(n_cu); }
 
 // rows: n_router of Wr (logits, + beta), n_pred of A (q), then the vector G
 // when given (gdot); ss: ||x||^2 when given
@@ -108,14 +133,16 @@ hipError_t launch_backfill(int B, int E, int K, int norm_topk, int flags,
 // ns shared slots follow the kept ones (expert E + i, every token, gate
 // sigmoid(gdot[t]) or 1 when gdot is null).  With x_bf16 (the layer's bf16
 // hidden states, rows of d) the same launch also writes the FFN's token
-// operand xp and its work units: units[b] for gate/up workgroup b, then
-// units[ffn_gu_blocks + b] for down workgroup b.
+// operand xp, its part tables (parts_gu, parts_dn, each of at most
+// ffn_parts_bound rows) and their header; n_cu: the device's compute units
+// (the FFN launches' sizes follow from it).
 hipError_t launch_compact(int B, int K, int E, int budget, int ns, const int32_t *exec_ids,
                           const float *exec_gates, const int32_t *slot_of,
                           const int32_t *n_sel, const float *gdot, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
                           int32_t *pair_of, const int32_t *sel_ids, const void *x_bf16, int d,
-                          int I, void *xp, UnitRec *units, hipStream_t st);
+                          int I, void *xp, FfnHdr *hdr, FfnPart *parts_gu, FfnPart *parts_dn,
+                          int n_cu, hipStream_t st);
 hipError_t launch_pack(const void *w13, const void *w2, void *w13p, void *w2p,
                        int E, int d, int I, hipStream_t st);
 // parts of expert u >= E read the shared experts' weights (w13s / w2s, u - E)
@@ -124,13 +151,14 @@ hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
                          const void *w13s,
                          const int32_t *sel_ids, const int32_t *n_sel,
                          const int32_t *offsets, const int32_t *pair_tok,
-                         const UnitRec *units, const void *xp, void *H, hipStream_t st);
+                         const FfnHdr *hdr, const FfnPart *parts, int n_cu, const void *xp,
+                         void *H, hipStream_t st);
 hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K,
                        int budget, int ns, const void *w2, const void *w2s,
                        const int32_t *sel_ids,
                        const int32_t *n_sel, const int32_t *offsets,
-                       const UnitRec *units, const float *pair_gate, const void *H,
-                       float *pairbuf, hipStream_t st);
+                       const FfnHdr *hdr, const FfnPart *parts, int n_cu,
+                       const float *pair_gate, const void *H, float *pairbuf, hipStream_t st);
 // kc: columns of pair_of (K routed + the shared experts)
 hipError_t launch_combine(bool bf16, int B, int d, int kc,
                           const int32_t *pair_of, const float *pairbuf,

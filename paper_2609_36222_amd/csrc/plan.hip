@@ -429,6 +429,81 @@ __device__ __forceinline__ void wave_scan3(const int *cnt, int n, int *off, int 
   if (lane == WAVE - 1) { off[SCAN_N] = i0; tb[SCAN_N] = i1; pb[SCAN_N] = i2; }
 }
 
+// A slot of nt tiles cut into np = ceil(nt / pt) parts of balanced size:
+// the first ex = nt % np parts have lo + 1 tiles, the others lo = nt / np.
+struct PartSplit {
+  int np, lo, ex;
+};
+__device__ __forceinline__ PartSplit part_split(int nt, int pt) {
+  if (nt <= 0) return {0, 0, 0};
+  const int np = (nt + pt - 1) / pt;   // pt is a constant: no division
+  // nt / np as a multiply-high by ceil(2^16 / np): exact while nt np < 2^16
+  // (a slot has at most MAX_B / 16 tiles)
+  const int lo = (int)(((uint32_t)nt * ((65536u + (uint32_t)np - 1u) / (uint32_t)np)) >> 16);
+  return {np, lo, nt - lo * np};
+}
+static_assert((MAX_B / 16) * (MAX_B / 16) < 65536, "part_split's quotient");
+// pre[j] = cnt[0] + ... + cnt[j - 1] (j <= SCAN_N; pre[SCAN_N]: the
+// total), by one wavefront.
+__device__ __forceinline__ void wave_scan_counts(const int *cnt, int *pre) {
+  const int lane = lane_id();
+  constexpr int Q = SCAN_Q;
+  int l[Q], s = 0;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    l[q] = cnt[lane * Q + q];
+    s += l[q];
+  }
+  int inc = s;
+#pragma unroll
+  for (int h = 1; h < WAVE; h <<= 1) {
+    const int o = __shfl_up(inc, h, WAVE);
+    if (lane >= h) inc += o;
+  }
+  int r = inc - s;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    pre[lane * Q + q] = r;
+    r += l[q];
+  }
+  if (lane == WAVE - 1) pre[SCAN_N] = inc;
+}
+
+// hr[s] = slots below s with more than one part (s <= SCAN_N; hr[SCAN_N]:
+// all of them), by one wavefront.
+__device__ __forceinline__ void wave_scan_multi(const int *tb, int nslot, int pt, int *hr) {
+  const int lane = lane_id();
+  constexpr int Q = SCAN_Q;
+  int l[Q], s = 0;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int i = lane * Q + q;
+    l[q] = (i < nslot && tb[i + 1] - tb[i] > pt) ? 1 : 0;
+    s += l[q];
+  }
+  int inc = s;
+#pragma unroll
+  for (int h = 1; h < WAVE; h <<= 1) {
+    const int o = __shfl_up(inc, h, WAVE);
+    if (lane >= h) inc += o;
+  }
+  int r = inc - s;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    hr[lane * Q + q] = r;
+    r += l[q];
+  }
+  if (lane == WAVE - 1) hr[SCAN_N] = inc;
+}
+
+// Die-major scan position of slot s: its deal position r (multi-part slots
+// first, see k_compact) goes to die r % N_XCD, as that die's slot r / N_XCD.
+__device__ __forceinline__ int slot_j(int s, const int *hr, int spd) {
+  const bool multi = hr[s + 1] > hr[s];
+  const int r = multi ? hr[s] : hr[SCAN_N] + (s - hr[s]);
+  return (r % N_XCD) * spd + r / N_XCD;
+}
+
 constexpr int CP_THREADS = 1024;
 constexpr int CP_WAVES = CP_THREADS / WAVE;
 constexpr int CP_STAGE = 4096;   // pair gates staged in LDS per pass
@@ -457,7 +532,7 @@ constexpr int CP_MAXPARTS = CP_PAIRS / FFN_PART + MAX_E + MAX_SHARED * (MAX_B / 
 // global stores are contiguous.  Then ns shared slots (slot n_sel + i runs
 // expert E + i for every token in token order, gate sigmoid(gdot[t]) =
 // 1 / (1 + exp(-s)) in fp32, or 1); offsets, the pair lists and pair_of
-// [B][K + ns] (and, with x, the FFN's operand and work units, below).
+// [B][K + ns] (and, with x, the FFN's operand and part tables, below).
 // With 16 wavefronts on one CU every per-thread instruction costs about 16
 // cycles, so the per-pair work is kept short: no division (t = q / K as a
 // multiply-high by kmul = ceil(2^32 / K), exact for q < 2^32 / K, far above
@@ -471,8 +546,8 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
                int32_t *__restrict__ offsets, int32_t *__restrict__ pair_tok,
                float *__restrict__ pair_gate, int32_t *__restrict__ pair_of,
                const int32_t *__restrict__ sel_ids, const uint16_t *__restrict__ x, int d,
-               int I, uint16_t *__restrict__ xp, UnitRec *__restrict__ units, int gu_blocks,
-               int dn_blocks) {
+               int I, uint16_t *__restrict__ xp, FfnHdr *__restrict__ hdr,
+               FfnPart *__restrict__ parts_gu, FfnPart *__restrict__ parts_dn, int n_cu) {
   // cw[w][s]: pairs of slot s in wavefront w, then their first rank in slot s
   __shared__ int cw[CP_WAVES][MAX_E];
   __shared__ int cnt[SCAN_N];
@@ -484,6 +559,9 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
   __shared__ int stage_t[CP_PAIRS];     // token of every routed position
   __shared__ float stage_g[CP_STAGE];   // gates, CP_STAGE positions per pass
   __shared__ int part_slot[CP_MAXPARTS];
+  __shared__ int np_gu[SCAN_N], np_dn[SCAN_N];          // FFN part tables (below)
+  __shared__ int pre_gu[SCAN_N + 1], pre_dn[SCAN_N + 1];
+  __shared__ int hr[SCAN_N + 1];
   const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
   const bool out = blockIdx.x == 0;     // the workgroup that writes the plan
   const int kc = K + ns;   // columns of pair_of
@@ -598,38 +676,77 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
   }
   if (!x) return;
   __syncthreads();   // part_slot complete
-  // The FFN's work units, one per workgroup of its two launches, shared out
-  // over this launch's workgroups.  Unit v of a launch with `groups` row
-  // groups is (slot s, row group g, part ts of s), ordered by slot, then
-  // group, then part (v = groups * first part of s + g * parts of s + ts),
-  // so that the units that read one row group's weights are neighbours;
-  // the list is cut into N_XCD contiguous runs and workgroup b (which the
-  // dispatcher runs on XCD b % N_XCD) takes unit local b / N_XCD of run
-  // b % N_XCD: the units that share a slot's tokens or a row group's
-  // weights mostly share an L2.
-  {
-    const int n_parts = pb[SCAN_N];
-    for (int e = blockIdx.x * CP_THREADS + tid; e < gu_blocks + dn_blocks;
-         e += gridDim.x * CP_THREADS) {
-      const bool gu = e < gu_blocks;
-      const int b = gu ? e : e - gu_blocks;
-      const int groups = gu ? I / 32 : d / 64;
-      const int nu = groups * n_parts;
-      const int per = (nu + N_XCD - 1) / N_XCD;
-      const int v = (b % N_XCD) * per + b / N_XCD;
-      UnitRec rec = {-1, 0, 0, 0, 0, 0, 0, 0};
-      if (b / N_XCD < per && v < nu) {
-        const int s = part_slot[v / groups];
-        const int np = pb[s + 1] - pb[s];
-        const int rel = v - groups * pb[s];
-        const int ts = rel % np;
-        rec.u = s < n_sel ? sel_s[s] : E + (s - n_sel);
-        rec.g = rel / np;
-        rec.p0 = off[s] + FFN_PART * ts;
-        rec.n = min(FFN_PART, cnt[s] - FFN_PART * ts);
-        rec.tile0 = tb[s] + (FFN_PART / 16) * ts;
+  // The FFN's part tables (see "Grouped bf16 FFN" in ffn.hip), one per
+  // launch.  Slot s (kept slots, then shared ones) has nt = tb[s + 1] - tb[s]
+  // tiles, cut into parts of balanced size (part_split).  Every part of a
+  // slot goes to one die in both tables (one L2 serves the expert's weights,
+  // and down finds the activations gate/up wrote there), and the dies get
+  // equal shares as far as whole slots allow: the slots with more than one
+  // gate/up part are dealt round-robin first, then the others, i.e. slot s
+  // takes deal position r = (its rank among the multi-part slots) or
+  // H + (its rank among the others) (H multi-part slots) on die r % N_XCD.
+  // A table lists the parts die by die, each die's in deal order (so the
+  // multi-part slots, the heaviest, start first): a scan of the slots' part
+  // counts in die-major order (j = x spd + r / N_XCD, spd slots per die at
+  // most) gives every slot's first row and every die's first row.
+  const int nslot = n_sel + ns;
+  const int spd = (nslot + N_XCD - 1) / N_XCD;
+  if (wv == 0) wave_scan_multi(tb, nslot, FFN_GU_PT, hr);
+  for (int j = tid; j < SCAN_N; j += CP_THREADS) np_gu[j] = np_dn[j] = 0;
+  __syncthreads();
+  for (int s = tid; s < nslot; s += CP_THREADS) {
+    const int nt = tb[s + 1] - tb[s], j = slot_j(s, hr, spd);
+    np_gu[j] = part_split(nt, FFN_GU_PT).np;
+    np_dn[j] = part_split(nt, FFN_DN_PT).np;
+  }
+  __syncthreads();
+  if (wv < 2) wave_scan_counts(wv == 0 ? np_gu : np_dn, wv == 0 ? pre_gu : pre_dn);
+  __syncthreads();
+  if (out && tid == 0) {
+    // gate/up's row group: the row-pair tiles per unit (FFN_WAVES down to
+    // FFN_WAVES / 2) that gives the fewest row-pair tiles to the busiest
+    // workgroup when every die's units are shared by its workgroups
+    const int T = I / 16;
+    const float per_die = (float)(ffn_gu_grid(n_cu) / N_XCD);
+    FfnHdr h;
+    int parts_die = 0;
+    for (int x = 0; x <= N_XCD; ++x) {
+      const int j = min(x * spd, SCAN_N);
+      h.die_gu[x] = pre_gu[j];
+      h.die_dn[x] = pre_dn[j];
+      if (x > 0) parts_die = max(parts_die, h.die_gu[x] - h.die_gu[x - 1]);
+    }
+    int best = FFN_WAVES, best_cost = 0x7FFFFFFF;
+#pragma unroll
+    for (int rp = FFN_WAVES; rp >= FFN_WAVES / 2; --rp) {
+      const int units = parts_die * ((T + rp - 1) / rp);
+      // rounds = ceil(units / per_die); exact in fp32 for these small integers
+      const int cost = (int)ceilf((float)units / per_die) * rp;
+      if (cost < best_cost) { best = rp; best_cost = cost; }
+    }
+    h.rp_gu = best;
+    h.pad0 = 0;
+    *hdr = h;
+  }
+  for (int s = blockIdx.x * CP_WAVES + wv; s < nslot; s += gridDim.x * CP_WAVES) {
+    const int u = s < n_sel ? sel_s[s] : E + (s - n_sel);
+    const int j = slot_j(s, hr, spd), nt = tb[s + 1] - tb[s];
+#pragma unroll
+    for (int tbl = 0; tbl < 2; ++tbl) {
+      const PartSplit sp = part_split(nt, tbl == 0 ? FFN_GU_PT : FFN_DN_PT);
+      const int row0 = tbl == 0 ? pre_gu[j] : pre_dn[j];
+      for (int q = lane; q < sp.np; q += WAVE) {
+        const int c = q < sp.ex ? sp.lo + 1 : sp.lo;
+        const int tf = q * sp.lo + min(q, sp.ex);   // the part's first tile in its slot
+        FfnPart rec;
+        rec.u = u;
+        rec.tile0 = tb[s] + tf;
+        rec.nt = c;
+        rec.p0 = off[s] + 16 * tf;
+        rec.n = min(16 * c, cnt[s] - 16 * tf);
+        rec.pad0 = rec.pad1 = rec.pad2 = 0;
+        (tbl == 0 ? parts_gu : parts_dn)[row0 + q] = rec;
       }
-      units[e] = rec;
     }
   }
   // the token gather: one wavefront per (part, k-step); every load of a
@@ -705,22 +822,20 @@ hipError_t launch_compact(int B, int K, int E, int budget, int ns, const int32_t
                           const int32_t *n_sel, const float *gdot, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
                           int32_t *pair_of, const int32_t *sel_ids,
-                          const void *x_bf16, int d, int I, void *xp, UnitRec *units,
-                          hipStream_t st) {
+                          const void *x_bf16, int d, int I, void *xp, FfnHdr *hdr,
+                          FfnPart *parts_gu, FfnPart *parts_dn, int n_cu, hipStream_t st) {
   const int ppt = (B * K + CP_THREADS - 1) / CP_THREADS;
   // with a gather: one wavefront per (part, k-step) at most, 256 workgroups
   // at most (one per CU: each holds the whole sort in its LDS)
   const long long tasks = (long long)ffn_max_parts(B, K, budget, ns) * (d / 32);
   const unsigned blocks =
       x_bf16 ? (unsigned)std::min<long long>(256, (tasks + CP_WAVES - 1) / CP_WAVES) : 1u;
-  const unsigned gu_blocks = x_bf16 ? ffn_gu_blocks(B, K, budget, ns, I) : 0u;
-  const unsigned dn_blocks = x_bf16 ? ffn_dn_blocks(B, K, budget, ns, d) : 0u;
   const uint64_t kmul = ((1ull << 32) + (uint64_t)K - 1) / (uint64_t)K;
 #define BASE_COMPACT(P)                                                                    \
   launch_k(k_compact<P>, dim3(blocks), dim3(CP_THREADS), 0, st, B, K, kmul, E, budget, ns, \
            exec_ids, exec_gates, slot_of, n_sel, gdot, offsets, pair_tok, pair_gate,      \
-           pair_of, sel_ids, (const uint16_t *)x_bf16, d, I, (uint16_t *)xp, units,          \
-           (int)gu_blocks, (int)dn_blocks)
+           pair_of, sel_ids, (const uint16_t *)x_bf16, d, I, (uint16_t *)xp, hdr,          \
+           parts_gu, parts_dn, n_cu)
   if (ppt <= 1) BASE_COMPACT(1);
   else if (ppt <= 2) BASE_COMPACT(2);
   else if (ppt <= 4) BASE_COMPACT(4);
