@@ -267,6 +267,34 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
                               base_plan *plan_out, void *ws, size_t ws_bytes,
                               void *stream);
 
+/* For callers that cannot allocate device memory (code under stream
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * layer as base_decode_layer, with the workspace replaced by a fixed scratch
+ * array the library holds on each GPU it runs on (BASE_NOALLOC_SCRATCH_BYTES,
+ * a static device array, kept until the process ends).  The call allocates
+ * nothing and calls no allocating routine; the caller still owns x, y and
+ * residual.  Results are bit for bit those of base_decode_layer.
+ *   Limit: a layer, batch and budget whose base_workspace_bytes exceeds
+ *          BASE_NOALLOC_SCRATCH_BYTES returns BASE_ERR_WORKSPACE (64 MiB
+ *          covers, e.g., d = 2048, E = 128, K = 8, I = 768 at B = 256 with
+ *          any budget up to E).
+ *   plan_out: pointers into the GPU's scratch array, valid until the next
+ *          call on that GPU.
+ *   Sharing: every call on one GPU uses that GPU's one array, which keeps
+ *          the last call's contents (nothing in it needs to start at zero:
+ *          every value a call reads is written by the same call first).
+ *          Calls that overlap on one GPU -- from several host threads or on
+ *          several streams without ordering between them -- race; the
+ *          caller orders them.
+ *   Errors: as base_decode_layer, checked on the host before anything is
+ *          enqueued; BASE_ERR_HIP if the scratch array's address cannot be
+ *          taken on the current device. */
+#define BASE_NOALLOC_SCRATCH_BYTES (64u << 20)
+base_status base_decode_layer_noalloc(const base_layer *L, const void *x, int32_t B,
+                                      int32_t budget, int32_t flags,
+                                      const void *residual, void *y,
+                                      base_plan *plan_out, void *stream);
+
 /* Packed expert weights (BASE_W_PACKED).  A one-time permutation, done when
  * a model is loaded; the values are unchanged.  The shared experts of a
  * packed layer are packed the same way, by a call whose L has E = n_shared

@@ -22,6 +22,7 @@ SCORE_BASE, SCORE_TOP1, SCORE_WEIGHT, SCORE_WEIGHT_SQ, SCORE_STATIC = 0, 1, 2, 3
 
 EXPORTS = ("base_workspace_bytes", "base_route", "base_predict_cost",
            "base_select", "base_moe_forward", "base_decode_layer",
+           "base_decode_layer_noalloc",
            "base_pack_experts", "base_set_stage_events", "base_status_string",
            "base_calib_stats_bytes", "base_calib_ws_bytes", "base_calib_reset",
            "base_calib_accumulate")
@@ -95,6 +96,10 @@ def load(path: str = LIB_PATH):
                                     _i32, _i32, _vp, _vp,
                                     ctypes.POINTER(base_plan), _vp,
                                     ctypes.c_size_t, _vp]
+    L.base_decode_layer_noalloc.restype = _i32
+    L.base_decode_layer_noalloc.argtypes = [ctypes.POINTER(base_layer), _vp, _i32,
+                                            _i32, _i32, _vp, _vp,
+                                            ctypes.POINTER(base_plan), _vp]
     L.base_pack_experts.restype = _i32
     L.base_pack_experts.argtypes = [ctypes.POINTER(base_layer), _vp, _vp, _vp]
     L.base_set_stage_events.restype = _i32
@@ -242,6 +247,21 @@ def base_decode_layer(desc, x, B, budget, flags, residual, y, ws, plan=None,
         ctypes.byref(plan), _ptr(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
     return plan
+
+
+def base_decode_layer_noalloc(desc, x, B, budget, flags, residual, y, plan=None,
+                              stream=None):
+    """base_decode_layer on the library's own scratch array (no workspace
+    argument, nothing allocated); returns the filled base_plan (device
+    pointers into that array)."""
+    plan = base_plan() if plan is None else plan
+    _check(load().base_decode_layer_noalloc(
+        ctypes.byref(desc), _ptr(x), B, budget, flags, _ptr(residual), _ptr(y),
+        ctypes.byref(plan), _stream(stream)))
+    return plan
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 def base_pack_experts(desc, w13_packed, w2_packed, stream=None):

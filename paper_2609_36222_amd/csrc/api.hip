@@ -182,6 +182,30 @@ int device_cus() {
   return n;
 }
 
+// Scratch of base_decode_layer_noalloc: one array of
+// BASE_NOALLOC_SCRATCH_BYTES per GPU, held by the library until the process
+// ends.  In host code `scratch` names a host-side stand-in, not device
+// memory: its device address on the current GPU comes from
+// hipGetSymbolAddress, taken once per device (with that device current) on
+// the entry point's first call there, and only that address is used.
+static __device__ __align__(256) unsigned char scratch[BASE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::atomic<void *> g_scratch_ptr[MAX_DEVICES];
+
+base_status scratch_of_current_device(void **out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) return BASE_ERR_HIP;
+  void *p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    // two threads racing here both store the same address
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return BASE_ERR_HIP;
+    g_scratch_ptr[dev].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return BASE_OK;
+}
+
 template <typename T>
 T *at(void *ws, size_t off) {
   return reinterpret_cast<T *>(static_cast<char *>(ws) + off);
@@ -422,6 +446,25 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
                        residual, y, ws, o, st, true));
   fill_plan(plan_out, ws, o, true);
   return BASE_OK;
+}
+
+base_status base_decode_layer_noalloc(const base_layer *L, const void *x, int32_t B,
+                                      int32_t budget, int32_t flags, const void *residual,
+                                      void *y, base_plan *plan_out, void *stream) {
+  // the checks base_decode_layer makes, then the size limit, all before the
+  // device is touched
+  BASE_TRY(check_layer(L, B, true, true, true));
+  if (budget < 1) return BASE_ERR_BUDGET;
+  if (flags & ~3) return BASE_ERR_FLAGS;
+  BASE_TRY(check_ptr(x, 16));
+  BASE_TRY(check_ptr(y, 16));
+  if (residual && !aligned(residual, 16)) return BASE_ERR_ALIGN;
+  const int32_t bc = budget < L->E ? budget : L->E;
+  if (layout(L, B, bc).total > (size_t)BASE_NOALLOC_SCRATCH_BYTES) return BASE_ERR_WORKSPACE;
+  void *ws = nullptr;
+  BASE_TRY(scratch_of_current_device(&ws));
+  return base_decode_layer(L, x, B, budget, flags, residual, y, plan_out, ws,
+                           (size_t)BASE_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 // ------------------------------------------------------------ calibration --

@@ -284,3 +284,23 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(bd, "_lib", None)
     with pytest.raises(ImportError, match="no CPU fallback"):
         bd.load(str(tmp_path / "libbase.so"))
+
+
+def test_noalloc_validation(lib):
+    """base_decode_layer_noalloc checks like base_decode_layer, and rejects
+    a layer whose workspace exceeds its scratch array, before it touches the
+    device (these calls return without a GPU)."""
+    def na(L, B=16, budget=4, flags=0, x=FAKE, y=FAKE, residual=None):
+        return lib.base_decode_layer_noalloc(ctypes.byref(L), x, B, budget, flags,
+                                             residual, y, None, None)
+    L = layer()
+    assert na(L, budget=0) == BUDGET
+    assert na(L, flags=8) == FLAGS
+    assert na(L, x=0) == NULL
+    assert na(L, y=FAKE + 4) == ALIGN
+    assert na(L, residual=FAKE + 8) == ALIGN
+    assert na(layer(pred_b=0)) == NULL
+    assert na(L, B=2048) == SHAPE
+    big = layer(E=256, K=16)
+    assert lib.base_workspace_bytes(ctypes.byref(big), 1024, 256) > bd.NOALLOC_SCRATCH_BYTES
+    assert na(big, B=1024, budget=256) == WS
