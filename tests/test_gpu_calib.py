@@ -136,3 +136,73 @@ def test_calibration_fit(gu, case):
         scale = max(1e-6, float(np.max(np.abs(f["a"]))))
         assert np.max(np.abs(pa[u] - f["a"])) <= 1e-4 * scale, u
         assert abs(pb[u] - f["b"]) <= 1e-4 * max(1.0, abs(f["b"])), u
+
+
+def test_calibration_qwen3_shape(gu):
+    """The Qwen3-shaped layer (d=2048, E=128, top-8, I=768, bf16), 768
+    calibration tokens in 3 batches of 256 (App. A): head, sum z_bar and
+    sum z_bar y of every expert in full; the fp32 Gram matrices (2048 x 2048
+    each) and the fit's lambda, a and b on sampled experts (the most and
+    least used, and two others)."""
+    from paper_2609_36222_amd import binding as bd
+    inp = W.layer_inputs("qwen3_b64")
+    sh = inp["shape"]
+    assert (sh.d, sh.E, sh.K, sh.I) == (2048, 128, 8, 768)
+    z = W.calibration_tokens(sh, n=768)
+    batches = [z[i:i + 256] for i in range(0, 768, 256)]
+    print("calibration statistics qwen3: 768 tokens", flush=True)
+    gl, stats = run_gpu_stats(gu, inp, batches)
+    head, sz, q, G = read_stats(stats, sh.E, sh.d)
+    # the oracle's statistics, the Gram only for the sampled experts
+    ex = method.Experts(inp["w13"], inp["w2"], True)
+    n = np.zeros(sh.E, np.int64)
+    sy, syy = np.zeros(sh.E), np.zeros(sh.E)
+    szr, qr = np.zeros((sh.E, sh.d)), np.zeros((sh.E, sh.d))
+    rows = {u: [] for u in range(sh.E)}
+    for zb_tok in batches:
+        _, ids, _ = carith.route(zb_tok, inp["w_router"], inp["b_router"], sh.K)
+        z64 = zb_tok.astype(np.float64)
+        zbar = z64 / np.linalg.norm(z64, axis=1, keepdims=True)
+        for u in np.unique(ids):
+            tt = np.nonzero((ids == u).any(axis=1))[0]
+            out = ex.forward(int(u), z64[tt])
+            y = np.log(np.sum(out ** 2, axis=1) + calib.EPS)
+            n[u] += len(tt)
+            sy[u] += y.sum()
+            syy[u] += y @ y
+            szr[u] += zbar[tt].sum(axis=0)
+            qr[u] += zbar[tt].T @ y
+            rows[int(u)].append(zbar[tt])
+    ytol = 2e-3
+    for u in range(sh.E):
+        assert int(head[u, 0]) == n[u], u
+        if n[u] == 0:
+            continue
+        assert abs(head[u, 1] - sy[u]) <= ytol * n[u], u
+        assert abs(head[u, 2] - syy[u]) <= 3 * ytol * n[u] * (1 + abs(sy[u]) / n[u]), u
+        assert np.max(np.abs(sz[u] - szr[u])) <= 1e-12 * n[u] + 1e-12, u
+        assert np.max(np.abs(q[u] - qr[u])) <= ytol * n[u], u
+    used = [u for u in range(sh.E) if n[u] > 0]
+    sample = sorted({int(max(used, key=lambda u: n[u])), int(min(used, key=lambda u: n[u])),
+                     used[len(used) // 3], used[2 * len(used) // 3]})
+    for u in sample:
+        Zu = np.concatenate(rows[u])
+        Gr = (Zu.T @ Zu)
+        scale = max(1.0, float(np.max(np.abs(Gr))))
+        assert np.max(np.abs(G[u] - Gr)) <= 1e-5 * scale, u
+    # the fit on the device against the oracle's ridge on the same statistics
+    pa = torch.empty(sh.E, sh.d, dtype=torch.float32, device="cuda")
+    pb = torch.empty(sh.E, dtype=torch.float32, device="cuda")
+    lam = torch.empty(sh.E, dtype=torch.float32, device="cuda")
+    bd.calib_fit(gl.desc, stats, calib.LAMBDAS, pa, pb, lam)
+    pa, pb, lam = pa.cpu().numpy(), pb.cpu().numpy(), lam.cpu().numpy()
+    for u in sample:
+        st = calib.ExpertStats(sh.d)
+        st.n = int(round(head[u, 0]))
+        st.sy, st.syy = float(head[u, 1]), float(head[u, 2])
+        st.sz, st.q, st.G = sz[u].copy(), q[u].copy(), G[u].copy()
+        f = calib.ridge_fit(st)
+        assert lam[u] == np.float32(f["lam"]), u
+        a_scale = max(1e-6, float(np.max(np.abs(f["a"]))))
+        assert np.max(np.abs(pa[u] - f["a"])) <= 1e-4 * a_scale, u
+        assert abs(pb[u] - f["b"]) <= 1e-4 * max(1.0, abs(f["b"])), u
