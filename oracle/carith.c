@@ -133,6 +133,9 @@ void orc_route(const float *x, int B, int d, const float *Wr,
                const float *beta, int E, int K, int norm_topk,
                float *logits, int32_t *ids, float *w)
 {
+    /* tokens are independent: the loop may run on several host threads
+       (OpenMP) with results identical to one thread */
+#pragma omp parallel for schedule(static)
     for (int t = 0; t < B; ++t) {
         const float *xt = x + (int64_t)t * d;
         float *lt = logits + (int64_t)t * E;
@@ -184,6 +187,7 @@ void orc_predict(const float *x, int B, int d, const float *A,
                  const float *b, int K, const int32_t *ids, const float *w,
                  float *cost, float *inv_norm)
 {
+#pragma omp parallel for schedule(static)
     for (int t = 0; t < B; ++t) {
         const float *xt = x + (int64_t)t * d;
         float ss = orc_cdot(xt, xt, d);

@@ -29,7 +29,7 @@ def build(force: bool = False) -> str:
             os.path.getmtime(_LIB) < os.path.getmtime(_SRC)):
         tmp = _LIB + ".tmp%d" % os.getpid()
         subprocess.check_call([
-            "gcc", "-O2", "-std=c99", "-fPIC", "-shared",
+            "gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-fopenmp",
             "-ffp-contract=off", "-fno-fast-math", "-frounding-math",
             _SRC, "-o", tmp, "-lm"])
         os.replace(tmp, _LIB)

@@ -80,43 +80,66 @@ def silu(a):
     return a / (1.0 + np.exp(-a))
 
 
-def expert_forward64(z, w13_u, w2_u, round_h_bf16=False):
+def expert_forward64(z, w13_u, w2_u, round_h_bf16=False, dtype=np.float64):
     """E_u(z) = W_d (silu(W_g z) * (W_u z)) for rows z [n, d], fp64.
 
     w13_u [2I, d] (gate rows then up rows), w2_u [d, I], given as fp32
     arrays holding the stored values.  round_h_bf16 rounds the SwiGLU
     activation to bf16 before the down projection, the precision at which a
-    bf16 serving stack feeds it to the second matrix product."""
-    z = np.asarray(z, np.float64)
+    bf16 serving stack feeds it to the second matrix product.  dtype: the
+    arithmetic (fp64, the definition every check uses; fp32 only for the
+    timed CPU baseline of the benchmark)."""
+    z = np.asarray(z, dtype)
     I = w2_u.shape[1]
-    gu = z @ np.asarray(w13_u, np.float64).T
+    gu = z @ np.asarray(w13_u, dtype).T
     h = silu(gu[:, :I]) * gu[:, I:]
     if round_h_bf16:
-        h = bf16_round(h.astype(np.float32)).astype(np.float64)
-    return h @ np.asarray(w2_u, np.float64).T
+        h = bf16_round(h.astype(np.float32)).astype(dtype)
+    return h @ np.asarray(w2_u, dtype).T
 
 
 class Experts:
-    """Expert weights as fp32 values (bf16 bit patterns widened exactly)."""
+    """Expert weights as fp32 values (bf16 bit patterns widened exactly).
 
-    def __init__(self, w13, w2, bf16):
+    dtype: the FFN arithmetic (fp64 for every check; see widened())."""
+
+    def __init__(self, w13, w2, bf16, dtype=np.float64):
         self.bf16 = bf16
         self._w13, self._w2 = w13, w2
+        self._widened = False
+        self.dtype = dtype
         self.E = w13.shape[0]
         self.I = w2.shape[2]
         self.d = w2.shape[1]
 
-    def w13(self, u):
-        a = self._w13[u]
+    def widened(self, dtype):
+        """The same experts with the FFN computed in dtype on weights widened
+        to dtype once, on an expert's first use, and kept (the benchmark's CPU
+        baseline: fp32 BLAS on weights converted before its timed region)."""
+        out = Experts(self._w13, self._w2, self.bf16, dtype)
+        out._widened = {}
+        return out
+
+    def _weights(self, u, which):
+        if self._widened is not False:
+            key = (u, which)
+            if key not in self._widened:
+                a = (self._w13 if which == 0 else self._w2)[u]
+                a = bf16_to_f32(a) if self.bf16 else np.asarray(a, np.float32)
+                self._widened[key] = np.ascontiguousarray(a, self.dtype)
+            return self._widened[key]
+        a = (self._w13 if which == 0 else self._w2)[u]
         return bf16_to_f32(a) if self.bf16 else np.asarray(a, np.float32)
 
+    def w13(self, u):
+        return self._weights(u, 0)
+
     def w2(self, u):
-        a = self._w2[u]
-        return bf16_to_f32(a) if self.bf16 else np.asarray(a, np.float32)
+        return self._weights(u, 1)
 
     def forward(self, u, z, round_h_bf16=None):
         rh = self.bf16 if round_h_bf16 is None else round_h_bf16
-        return expert_forward64(z, self.w13(u), self.w2(u), rh)
+        return expert_forward64(z, self.w13(u), self.w2(u), rh, self.dtype)
 
 
 def expert_outputs(experts, x, ids, round_h_bf16=False):
