@@ -351,9 +351,9 @@ base_status base_calib_accumulate(const base_layer *L, const void *z, int32_t B,
  * always) records its pair back to back.
  * Stages: 0 scores (router logits, predictor dot products, norms), 1 tail
  * (top-K, router weights, predicted costs), 2 aggregation + selection,
- * 3 backfill + gates, 4 compaction and the token gather (one kernel),
- * 5 (no kernel: the gather is in stage 4), 6 FFN gate/up, 7 FFN down,
- * 8 combine.  base_route runs stages 0 and 1,
+ * 3 backfill + gates, 4 compaction and the FFN's part tables, 5 (no
+ * kernel: FFN gate/up gathers its own token rows), 6 FFN gate/up, 7 FFN
+ * down, 8 combine.  base_route runs stages 0 and 1,
  * base_select stage 2, base_moe_forward 3 to 8 (base_predict_cost runs its
  * own kernel, untimed); base_decode_layer runs all of them except that one
  * kernel makes the selection and the backfill: stage 2 times it and stage 3

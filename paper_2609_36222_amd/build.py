@@ -22,7 +22,7 @@ OUT_DIR = os.path.join(HERE, "_lib")
 LIB = os.path.join(OUT_DIR, "libbase.so")
 PROBE_LIB = os.path.join(OUT_DIR, "libbase_probe.so")   # bench's streaming-read probe
 CALIB_LIB = os.path.join(OUT_DIR, "libbase_calib.so")   # predictor fit (links rocSOLVER)
-SOURCES = ["api.hip", "scores.hip", "route_predict.hip", "plan.hip", "ffn.hip",
+SOURCES = ["api.hip", "scores.hip", "plan.hip", "ffn.hip",
            "pack.hip", "calib.hip"]
 ARCH = os.environ.get("BASE_OFFLOAD_ARCH", "gfx950")
 

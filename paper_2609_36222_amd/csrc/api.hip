@@ -91,9 +91,9 @@ base_status check_ptr(const void *p, size_t a) {
 
 // Workspace layout: every array starts on a 256-byte boundary.
 struct Layout {
-  size_t logits, q, ss, gdot, topk_ids, topk_w, cost, scores, counts, sel_ids, n_sel,
+  size_t logits, gdot, topk_ids, topk_w, cost, scores, counts, sel_ids, n_sel,
       slot_of, exec_ids, exec_gates, offsets, pair_tok, pair_gate, pair_of,
-      hdr, parts_gu, parts_dn, xp, H, pairbuf, total;
+      hdr, parts_gu, parts_dn, tokoff, H, pairbuf, total;
 };
 
 size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -110,8 +110,6 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
   const int ns = L->n_shared;
   const size_t P = BK + (size_t)ns * B;   // routed pairs + shared pairs
   o.logits = take((size_t)B * L->E * 4);
-  o.q = take((size_t)B * L->E * 4);
-  o.ss = take((size_t)B * 4);
   o.gdot = take((size_t)B * 4);
   o.topk_ids = take(BK * 4);
   o.topk_w = take(BK * 4);
@@ -129,16 +127,17 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
   o.pair_of = take((size_t)B * (L->K + ns) * 4);
   // the FFN's part tables and their header (bf16)
   const bool bf = L->dtype == BASE_BF16;
-  o.hdr = take(bf ? sizeof(FfnHdr) : 0);
-  o.parts_gu = take(bf ? (size_t)ffn_parts_bound(B, L->K, bc, ns, FFN_GU_PT) * sizeof(FfnPart) : 0);
-  o.parts_dn = take(bf ? (size_t)ffn_parts_bound(B, L->K, bc, ns, FFN_DN_PT) * sizeof(FfnPart) : 0);
+  // (one copy per die: the FFN's workgroups read their die's copy)
+  const size_t cp = bf ? N_XCD : 0;
+  o.hdr = take(cp * sizeof(FfnHdr));
+  o.parts_gu = take(cp * ffn_parts_bound(B, L->K, bc, ns, FFN_GU_PT) * sizeof(FfnPart));
+  o.parts_dn = take(cp * ffn_parts_bound(B, L->K, bc, ns, FFN_DN_PT) * sizeof(FfnPart));
+  o.tokoff = take(cp * ffn_parts_bound(B, L->K, bc, ns, FFN_GU_PT) * FFN_GU_TOK * 4);
   if (L->dtype == BASE_BF16) {
-    // fragment-ordered tokens and SwiGLU activations (16-pair tiles)
+    // fragment-ordered SwiGLU activations (16-pair tiles)
     const size_t tiles = (size_t)ffn_max_tiles(B, L->K, bc, ns);
-    o.xp = take(tiles * 16 * (size_t)L->d * 2);
     o.H = take(tiles * 16 * (size_t)L->I * 2);
   } else {
-    o.xp = 0;
     o.H = take(BK * L->I * 4);
   }
   o.pairbuf = take(P * L->d * 4);
@@ -236,21 +235,20 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
   const int n_cu = device_cus();
   FfnHdr *hdr = at<FfnHdr>(ws, o.hdr);
   FfnPart *parts_gu = at<FfnPart>(ws, o.parts_gu), *parts_dn = at<FfnPart>(ws, o.parts_dn);
-  // the same launch gathers the FFN's token operand and lists its parts
-  // (bf16)
+  uint32_t *tokoff = at<uint32_t>(ws, o.tokoff);
+  // the same launch lists the FFN's parts and gate/up's token rows (bf16)
   HIP_TRY(launch_compact(B, L->K, L->E, bc, ns, exec_ids, exec_gates, slot_of, n_sel,
                          shared_gate(L) ? at<float>(ws, o.gdot) : nullptr, offsets,
-                         pair_tok, pair_gate, pair_of, sel_ids, bf16 ? x : nullptr, L->d,
-                         L->I, bf16 ? at<void>(ws, o.xp) : nullptr, hdr, parts_gu, parts_dn,
-                         n_cu, st));
+                         pair_tok, pair_gate, pair_of, sel_ids, bf16, L->d, L->I, tokoff,
+                         hdr, parts_gu, parts_dn, n_cu, st));
   stage_end(st);
-  stage(5);   // no launch of its own: the gather is part of stage 4
+  stage(5);   // no launch of its own: gate/up gathers its tokens itself
   stage_end(st);
   stage(6);
   const bool packed = L->w_layout == BASE_W_PACKED;
   HIP_TRY(launch_gateup(bf16, packed, x, B, L->d, L->I, L->E, L->K, bc, ns, L->w13,
                         L->w13_shared, sel_ids, n_sel, offsets, pair_tok, hdr, parts_gu, n_cu,
-                        at<void>(ws, o.xp), at<void>(ws, o.H), st));
+                        tokoff, at<void>(ws, o.H), st));
   stage_end(st);
   stage(7);
   HIP_TRY(launch_down(bf16, packed, B, L->d, L->I, L->E, L->K, bc, ns, L->w2,
@@ -315,11 +313,11 @@ base_status base_route(const base_layer *L, const void *x, int32_t B,
   hipStream_t st = (hipStream_t)stream;
   const bool bf16 = L->dtype == BASE_BF16;
   stage(0);
-  HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
-                        nullptr, 0, nullptr, logits, nullptr, nullptr, nullptr, st));
+  HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E, nullptr, logits,
+                        nullptr, st));
   stage_end(st);
   stage(1);
-  HIP_TRY(launch_tail(B, L->E, L->K, L->norm_topk, logits, nullptr, nullptr,
+  HIP_TRY(launch_tail(bf16, B, L->E, L->K, L->d, L->norm_topk, logits, nullptr, nullptr,
                       nullptr, topk_ids, topk_w, nullptr, 1, BASE_SCORE_BASE, st));
   stage_end(st);
   return BASE_OK;
@@ -333,15 +331,12 @@ base_status base_predict_cost(const base_layer *L, const void *x, int32_t B,
   BASE_TRY(check_ptr(topk_ids, 4));
   BASE_TRY(check_ptr(topk_w, 4));
   BASE_TRY(check_ptr(cost, 4));
-  if (L->score_rule == BASE_SCORE_BASE)
-    HIP_TRY(launch_predict(L->dtype == BASE_BF16, x, B, L->d, L->E, L->K,
-                           topk_ids, topk_w, L->pred_a, L->pred_b, cost,
-                           (hipStream_t)stream));
-  else   // the other rules' scores need only the routes (and pred_b)
-    HIP_TRY(launch_tail(B, L->E, L->K, L->norm_topk, nullptr, nullptr, nullptr,
-                        L->pred_b, const_cast<int32_t *>(topk_ids),
-                        const_cast<float *>(topk_w), cost, 2, L->score_rule,
-                        (hipStream_t)stream));
+  // the method's rule computes the predictor's dot products of the routed
+  // pairs; the other rules' scores need only the routes (and pred_b)
+  HIP_TRY(launch_tail(L->dtype == BASE_BF16, B, L->E, L->K, L->d, L->norm_topk, nullptr, x,
+                      L->pred_a, L->pred_b, const_cast<int32_t *>(topk_ids),
+                      const_cast<float *>(topk_w), cost, 2, L->score_rule,
+                      (hipStream_t)stream));
   return BASE_OK;
 }
 
@@ -389,9 +384,8 @@ base_status base_moe_forward(const base_layer *L, const void *x, int32_t B,
   BASE_TRY(check_ws(L, B, bc, ws, ws_bytes));
   const Layout o = layout(L, B, bc);
   if (shared_gate(L))   // the shared experts' gate: its own dot-product launch
-    HIP_TRY(launch_scores(L->dtype == BASE_BF16, x, B, L->d, nullptr, nullptr, 0, nullptr, 0,
-                          shared_gate(L), nullptr, nullptr, at<float>(ws, o.gdot), nullptr,
-                          (hipStream_t)stream));
+    HIP_TRY(launch_scores(L->dtype == BASE_BF16, x, B, L->d, nullptr, nullptr, 0,
+                          shared_gate(L), nullptr, at<float>(ws, o.gdot), (hipStream_t)stream));
   BASE_TRY(run_forward(L, x, B, logits, topk_ids, sel_ids, n_sel,
                        slot_of_expert, bc, flags, residual, y, ws, o,
                        (hipStream_t)stream));
@@ -422,18 +416,13 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
   int32_t *sel = at<int32_t>(ws, o.sel_ids);
   int32_t *nsel = at<int32_t>(ws, o.n_sel);
   int32_t *slot = at<int32_t>(ws, o.slot_of);
-  float *q = at<float>(ws, o.q);
-  float *ss = at<float>(ws, o.ss);
-  // the predictor's dot products and norms only for the method's own rule
-  const bool pred = L->score_rule == BASE_SCORE_BASE;
   stage(0);
-  HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E,
-                        pred ? L->pred_a : nullptr, pred ? L->E : 0, shared_gate(L), logits,
-                        pred ? q : nullptr, at<float>(ws, o.gdot), pred ? ss : nullptr, st));
+  HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E, shared_gate(L),
+                        logits, at<float>(ws, o.gdot), st));
   stage_end(st);
-  stage(1);
-  HIP_TRY(launch_tail(B, L->E, L->K, L->norm_topk, logits, q, ss, L->pred_b,
-                      ids, w, cost, 3, L->score_rule, st));
+  stage(1);   // top-K, weights and (the method's rule) the routed pairs' predictor
+  HIP_TRY(launch_tail(bf16, B, L->E, L->K, L->d, L->norm_topk, logits, x, L->pred_a,
+                      L->pred_b, ids, w, cost, 3, L->score_rule, st));
   stage_end(st);
   stage(2);   // selection and backfill in one launch
   HIP_TRY(launch_select_backfill(B, L->K, L->E, ids, cost, bc,
@@ -516,10 +505,10 @@ base_status base_calib_accumulate(const base_layer *L, const void *z, int32_t B,
   int32_t *sel = at<int32_t>(ws, o.sel_ids);
   int32_t *nsel = at<int32_t>(ws, o.n_sel);
   int32_t *slot = at<int32_t>(ws, o.slot_of);
-  HIP_TRY(launch_scores(bf16, z, B, C.d, C.w_router, C.b_router, C.E, nullptr, 0, nullptr,
-                        logits, nullptr, nullptr, nullptr, st));
-  HIP_TRY(launch_tail(B, C.E, C.K, C.norm_topk, logits, nullptr, nullptr, nullptr, ids, w,
-                      nullptr, 1, BASE_SCORE_BASE, st));
+  HIP_TRY(launch_scores(bf16, z, B, C.d, C.w_router, C.b_router, C.E, nullptr, logits,
+                        nullptr, st));
+  HIP_TRY(launch_tail(bf16, B, C.E, C.K, C.d, C.norm_topk, logits, nullptr, nullptr, nullptr,
+                      ids, w, nullptr, 1, BASE_SCORE_BASE, st));
   // the budget E keeps the whole batch union (any positive scores do)
   HIP_TRY(launch_select(B, C.K, C.E, ids, w, bc, false, at<float>(ws, o.scores),
                         at<int32_t>(ws, o.counts), sel, nsel, slot, st));
@@ -535,11 +524,11 @@ base_status base_calib_accumulate(const base_layer *L, const void *z, int32_t B,
   HIP_TRY(launch_compact(B, C.K, C.E, bc, 0, at<int32_t>(ws, o.exec_ids),
                          at<float>(ws, o.exec_gates), slot, nsel, nullptr, offsets, pair_tok,
                          at<float>(ws, o.pair_gate), at<int32_t>(ws, o.pair_of), sel,
-                         bf16 ? z : nullptr, C.d, C.I, bf16 ? at<void>(ws, o.xp) : nullptr,
-                         hdr, parts_gu, parts_dn, n_cu, st));
+                         bf16, C.d, C.I, at<uint32_t>(ws, o.tokoff), hdr, parts_gu, parts_dn,
+                         n_cu, st));
   const bool packed = C.w_layout == BASE_W_PACKED;
   HIP_TRY(launch_gateup(bf16, packed, z, B, C.d, C.I, C.E, C.K, bc, 0, C.w13, nullptr, sel,
-                        nsel, offsets, pair_tok, hdr, parts_gu, n_cu, at<void>(ws, o.xp),
+                        nsel, offsets, pair_tok, hdr, parts_gu, n_cu, at<uint32_t>(ws, o.tokoff),
                         at<void>(ws, o.H), st));
   HIP_TRY(launch_down(bf16, packed, B, C.d, C.I, C.E, C.K, bc, 0, C.w2, nullptr, sel, nsel,
                       offsets, hdr, parts_dn, n_cu, at<float>(ws, o.pair_gate),

@@ -61,13 +61,36 @@ __device__ __forceinline__ void load4(const uint16_t *p, float v[4]) {
 }
 
 // ---------------------------------------------------------- wave sums ---
+// The value of lane j ^ H in lane j: quad permutations (DPP) for H = 1, 2,
+// an LDS-free swizzle inside 32-lane halves for H = 4, 8, 16, a permute
+// across the halves for H = 32.
+template <int H>
+__device__ __forceinline__ float xor_lane(float v) {
+  static_assert(H == 1 || H == 2 || H == 4 || H == 8 || H == 16 || H == 32, "lane distance");
+  const int i = __float_as_int(v);
+  int r;
+  if constexpr (H == 1)
+    r = __builtin_amdgcn_update_dpp(0, i, 0xB1, 0xF, 0xF, false);   // quad_perm [1, 0, 3, 2]
+  else if constexpr (H == 2)
+    r = __builtin_amdgcn_update_dpp(0, i, 0x4E, 0xF, 0xF, false);   // quad_perm [2, 3, 0, 1]
+  else if constexpr (H < 32)
+    r = __builtin_amdgcn_ds_swizzle(i, (H << 10) | 0x1F);          // bit mode: lane ^ H
+  else
+    r = __shfl_xor(i, 32, WAVE);
+  return __int_as_float(r);
+}
+
 // Butterfly over the 64 lanes.  At step h lane j adds the value of lane
 // j^h; since fp32 addition is commutative this is, value for value, the
 // halving tree "s[j] = s[j] + s[j+h] for j < h" (h = 32 .. 1), and every
 // lane ends with the tree's s[0].
 __device__ __forceinline__ float wave_tree_sum(float v) {
-#pragma unroll
-  for (int h = 32; h >= 1; h >>= 1) v = v + __shfl_xor(v, h, WAVE);
+  v = v + xor_lane<32>(v);
+  v = v + xor_lane<16>(v);
+  v = v + xor_lane<8>(v);
+  v = v + xor_lane<4>(v);
+  v = v + xor_lane<2>(v);
+  v = v + xor_lane<1>(v);
   return v;
 }
 

@@ -87,16 +87,18 @@ __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "mem
 // their resource (zero, no memory access) and skip the MFMAs, but still take
 // their share of the token loads.
 //
-// Token operands in fragment order: the pairs of slot s occupy consecutive
-// 16-pair tiles (its i-th tile holds its pairs 16 i .. 16 i + 15, padding
-// rows zero); a tile is ksteps fragments of 1 KiB, fragment (tile, k-step) =
-// 64 lanes x 8 elements, lane l holding pair 16 i' + l % 16, elements
-// 32 k-step + 8 (l / 16) .. +7 -- the MFMA B-operand layout.
-//   xp: the pairs' hidden states (contraction d), written by k_compact with
-//       its padding rows zeroed
-//   hp: the SwiGLU activations (contraction I), written by k_gateup_bf16;
-//       its padding rows are never written (they meet only the discarded
-//       output columns of padding pairs)
+// Token operands: the pairs of slot s occupy consecutive 16-pair tiles (its
+// i-th tile holds its pairs 16 i .. 16 i + 15); the fragment of (tile,
+// k-step) is 64 lanes x 8 elements, lane l holding pair 16 i' + l % 16,
+// elements 32 k-step + 8 (l / 16) .. +7 -- the MFMA B-operand layout.
+//   gate/up (contraction d): gathered from the hidden states x by a buffer
+//       load per lane into the LDS ring, 64 contiguous bytes of a token row
+//       per 16 lanes (x stays in L2: every kept expert's pairs read it);
+//       padding rows read zero
+//   hp: the SwiGLU activations (contraction I), written by k_gateup_bf16 in
+//       fragment order (1 KiB per fragment, tile-major); its padding rows are
+//       never written (they meet only the discarded output columns of
+//       padding pairs)
 
 // The weight operand of one wavefront: one 16-row tile (two for gate/up:
 // the gate rows and their up rows).
@@ -129,19 +131,34 @@ __device__ __forceinline__ PartU load_part(const FfnPart *p) {
 
 // One unit of gate/up: wavefront w owns row-pair tile r = rp0 + w (gate rows
 // 16 r .. 16 r + 15 and their up rows I + 16 r ..), if w < nrp.  NT: the
-// part's tile count.  Writes H = bf16(silu(g) * u) in fragment order: column
+// part's tile count.  The loop advances two k-steps at a time (a step: 64
+// contraction elements, one 128-byte line of every token row).  The token
+// fragments come straight from the hidden states (resource rx over x):
+// wavefront w < NT loads tile w's pairs 0..7 (half 0) and 8..15 (half 1), one
+// line each per step, lane l taking row l / 8 of its half and 16-byte
+// segment (l % 8) ^ (l / 8) of the line (tv0, tv1: that row's byte offset
+// in x plus 16 times the segment; past the part's pairs at least
+// FFN_TOK_PAD, beyond rx: zero).  Lane l's bytes land at 16 l of the half's
+// 1 KiB in the ring, so the fragment of k-step e (0, 1) of the step, lane m
+// (pair n = m % 16, elements 8 (m / 16) ..), is read at half n / 8, position
+// 8 (n % 8) + ((4 e + m / 16) ^ (n % 8)): the swizzle keeps the eight lanes
+// of a read pass on distinct bank groups, and every token line is fetched
+// whole by one load.  Writes H = bf16(silu(g) * u) in fragment order: column
 // i = 16 r + 4 (l / 16) + q of pair tk sits in fragment (tile of tk, k-step
 // r / 2), lane tk % 16 + 16 (2 (r % 2) + (l / 16) / 2), element
 // 4 ((l / 16) % 2) + q.
 template <int NT, bool PACKED>
 __device__ __forceinline__ void gateup_unit(uint8_t *ring, uint8_t *dummy, int d, int I,
                                             const uint16_t *__restrict__ w13, const PartU &pt,
-                                            int rp0, int nrp, const uint16_t *__restrict__ xp,
-                                            uint16_t *__restrict__ hp) {
+                                            int rp0, int nrp, rsrc_t rx, uint32_t tv0,
+                                            uint32_t tv1, uint16_t *__restrict__ hp) {
   constexpr int W = FFN_WAVES, DW = FFN_GU_DW, DT = FFN_GU_DT;
-  constexpr int NTK = (NT + W - 1) / W;   // token loads per wavefront per k-step
+  constexpr int SLOT = NT * 2048;       // one step's token lines in the ring
+  constexpr int LPS = 6;                // loads per step and wavefront
+  static_assert(NT <= W, "one token tile per wavefront");
+  static_assert(DW % 2 == 0 && DW / 2 > DT, "weights requested before the step's tokens");
   const int w = wave_id_u(), lane = lane_id();
-  const int KS = d / 32;
+  const int KS = d / 32, NS = KS / 2;
   const bool active = w < nrp;
   const int r = rp0 + (active ? w : 0);
   TileSrc ws;
@@ -160,27 +177,29 @@ __device__ __forceinline__ void gateup_unit(uint8_t *ring, uint8_t *dummy, int d
     ws.v0 = ws.v1 = (uint32_t)(lane & 15) * (uint32_t)(d * 2) + (uint32_t)(lane >> 4) * 16u;
     ws.kstride = 64;
   }
-  const uint32_t tbytes = (uint32_t)KS * 1024u;
-  const rsrc_t rt = make_rsrc(xp + (size_t)pt.tile0 * (tbytes / 2), (uint32_t)pt.nt * tbytes);
-  const uint32_t vl = lane * 16;
-  auto tok_load = [&](int ks) {
-    uint8_t *slot = ring + (ks % (DT + 1)) * (NT * 1024);
-#pragma unroll
-    for (int q = 0; q < NTK; ++q) {
-      const int j = w + W * q;
-      if (j < NT)
-        load_lds(rt, slot + j * 1024, vl,
-                 ks < KS ? (uint32_t)j * tbytes + (uint32_t)ks * 1024u : OOB);
-      else
-        load_lds(rt, dummy + w * 1024, vl, OOB);
+  // the step offset goes into the lane offset, so that the range check
+  // alone keeps every load inside x
+  auto tok_load = [&](int st) {
+    uint8_t *slot = ring + (st % (DT + 1)) * SLOT;
+    const uint32_t o = (uint32_t)st * 128u;
+    if (w < NT) {
+      load_lds(rx, slot + w * 2048, st < NS ? tv0 + o : FFN_TOK_PAD, 0);
+      load_lds(rx, slot + w * 2048 + 1024, st < NS ? tv1 + o : FFN_TOK_PAD, 0);
+    } else {
+      load_lds(rx, dummy + w * 1024, FFN_TOK_PAD, 0);
+      load_lds(rx, dummy + w * 1024, FFN_TOK_PAD, 0);
     }
   };
+  // this lane's fragment positions in a step's tile (k-step e = 0, 1)
+  const int n = lane & 15, n8 = n & 7;
+  const int rb0 = (n >> 3) * 1024 + (8 * n8 + ((lane >> 4) ^ n8)) * 16;
+  const int rb1 = (n >> 3) * 1024 + (8 * n8 + ((4 + (lane >> 4)) ^ n8)) * 16;
   f32x4 ag[NT], au[NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j) { ag[j] = f32x4{0, 0, 0, 0}; au[j] = f32x4{0, 0, 0, 0}; }
-  // the first token loads before the first weight loads: the wait of
-  // k-step ks below allows (DT - 1) * (2 + NTK) younger loads, and for the
-  // first k-steps the prologue's weight loads are among them
+  // the first token loads before the first weight loads: the wait of step
+  // st below allows (DT - 1) * LPS younger loads, and for the first steps
+  // the prologue's weight loads are among them
 #pragma unroll
   for (int p = 0; p < DT; ++p) tok_load(p);
   bf16x8 wg[DW], wu[DW];
@@ -191,30 +210,37 @@ __device__ __forceinline__ void gateup_unit(uint8_t *ring, uint8_t *dummy, int d
   }
   for (int k0 = 0; k0 < KS; k0 += DW) {
 #pragma unroll
-    for (int p = 0; p < DW; ++p) {
-      const int ks = k0 + p;
-      // this wavefront's loads of k-step ks are done: at most the loads of
-      // the DT - 1 later iterations are in flight
-      wait_vm<(DT - 1) * (2 + NTK)>();
+    for (int p = 0; p < DW; p += 2) {
+      const int ks = k0 + p, st = ks / 2;
+      // this wavefront's loads of step st are done: at most the loads of
+      // the DT - 1 later steps are in flight
+      wait_vm<(DT - 1) * LPS>();
       wg_barrier();
       __builtin_amdgcn_sched_barrier(0);
       if (active) {
-        const uint8_t *sb = ring + (ks % (DT + 1)) * (NT * 1024) + lane * 16;
-        bf16x8 xc = *reinterpret_cast<const bf16x8 *>(sb);
+        const uint8_t *sb = ring + (st % (DT + 1)) * SLOT;
 #pragma unroll
-        for (int j = 0; j < NT; ++j) {
-          bf16x8 xn = xc;
-          if (j + 1 < NT) xn = *reinterpret_cast<const bf16x8 *>(sb + (j + 1) * 1024);
-          ag[j] = mfma16(wg[p], xc, ag[j]);
-          au[j] = mfma16(wu[p], xc, au[j]);
-          __builtin_amdgcn_sched_barrier(0);
-          xc = xn;
+        for (int e = 0; e < 2; ++e) {
+          const uint8_t *se = sb + (e == 0 ? rb0 : rb1);
+          bf16x8 xc = *reinterpret_cast<const bf16x8 *>(se);
+#pragma unroll
+          for (int j = 0; j < NT; ++j) {
+            bf16x8 xn = xc;
+            if (j + 1 < NT) xn = *reinterpret_cast<const bf16x8 *>(se + (j + 1) * 2048);
+            ag[j] = mfma16(wg[p + e], xc, ag[j]);
+            au[j] = mfma16(wu[p + e], xc, au[j]);
+            __builtin_amdgcn_sched_barrier(0);
+            xc = xn;
+          }
         }
       }
       __builtin_amdgcn_sched_barrier(0);
-      wg[p] = bload(ws.r0, ws.v0, ksoff(ws, ks + DW, KS));
-      wu[p] = bload(ws.r1, ws.v1, ksoff(ws, ks + DW, KS));
-      tok_load(ks + DT);
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        wg[p + e] = bload(ws.r0, ws.v0, ksoff(ws, ks + e + DW, KS));
+        wu[p + e] = bload(ws.r1, ws.v1, ksoff(ws, ks + e + DW, KS));
+      }
+      tok_load(st + DT);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
@@ -354,17 +380,31 @@ template <bool PACKED>
 __global__ __launch_bounds__(FFN_WAVES * WAVE)
 void k_gateup_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w13r,
                    const uint16_t *__restrict__ w13s, const FfnHdr *__restrict__ hdr,
-                   const FfnPart *__restrict__ parts, const uint16_t *__restrict__ xp,
+                   const FfnPart *__restrict__ parts, int pstride,
+                   const uint16_t *__restrict__ x, int B, const uint32_t *__restrict__ tokoff,
                    uint16_t *__restrict__ hp) {
-  __shared__ __attribute__((aligned(16))) uint8_t ring[(FFN_GU_DT + 1) * FFN_GU_PT * 1024];
+  __shared__ __attribute__((aligned(16))) uint8_t ring[(FFN_GU_DT + 1) * FFN_GU_PT * 2048];
   __shared__ __attribute__((aligned(16))) uint8_t dummy[FFN_WAVES * 1024];
+  // this die's copy of the tables (written by the compaction workgroup
+  // that ran on the same die)
+  const int die = (int)(blockIdx.x % N_XCD);
+  hdr += die;
+  parts += (size_t)die * pstride;
+  tokoff += (size_t)die * pstride * FFN_GU_TOK;
   const int RP = __builtin_amdgcn_readfirstlane(hdr->rp_gu);
   const int T = I / 16;                    // row-pair tiles per expert
   if (RP < 1 || RP > FFN_WAVES) return;    // only for a plan not made by k_compact
   const int upp = (T + RP - 1) / RP;
   const int step = (int)(gridDim.x / N_XCD);
+  const rsrc_t rx = make_rsrc(x, (uint32_t)B * (uint32_t)d * 2u);
+  const int w = wave_id_u(), lane = lane_id();
   int k, rg;
   for (int m = (int)(blockIdx.x / N_XCD); next_unit(hdr->die_gu, m, upp, k, rg); m += step) {
+    // the part and this wavefront's token rows (row l / 8 of each half of
+    // its tile), loaded together
+    const uint32_t *tr = tokoff + (size_t)k * FFN_GU_TOK + 16 * w + (lane >> 3);
+    const uint32_t tk0 = w < FFN_GU_PT ? tr[0] : FFN_TOK_PAD;
+    const uint32_t tk1 = w < FFN_GU_PT ? tr[8] : FFN_TOK_PAD;
     const PartU pt = load_part(parts + k);
     if (pt.u < 0 || pt.u >= E + ns || pt.nt < 1 || pt.nt > FFN_GU_PT) continue;
     const uint16_t *w13 = pt.u < E ? w13r : w13s;
@@ -372,7 +412,11 @@ void k_gateup_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w13
     q.u = pt.u < E ? pt.u : pt.u - E;   // experts E .. E + ns - 1: the shared ones
     const int rp0 = rg * RP, nrp = min(RP, T - rp0);
     wg_barrier();   // every wavefront is done with the previous unit's ring
-#define BASE_GU(N) case N: gateup_unit<N, PACKED>(ring, dummy, d, I, w13, q, rp0, nrp, xp, hp); break;
+    // entries past the part's pairs are not written: those lanes read zero
+    const uint32_t seg = 16u * (uint32_t)((lane & 7) ^ (lane >> 3));
+    const uint32_t tv0 = 16 * w + (lane >> 3) < q.n ? tk0 + seg : FFN_TOK_PAD;
+    const uint32_t tv1 = 16 * w + 8 + (lane >> 3) < q.n ? tk1 + seg : FFN_TOK_PAD;
+#define BASE_GU(N) case N: gateup_unit<N, PACKED>(ring, dummy, d, I, w13, q, rp0, nrp, rx, tv0, tv1, hp); break;
     switch (q.nt) { BASE_GU(1) BASE_GU(2) BASE_GU(3) BASE_GU(4) BASE_GU(5) default: BASE_GU(6) }
 #undef BASE_GU
   }
@@ -385,10 +429,14 @@ template <bool PACKED>
 __global__ __launch_bounds__(FFN_WAVES * WAVE, FFN_DN_WPE)
 void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
                  const uint16_t *__restrict__ w2s, const FfnHdr *__restrict__ hdr,
-                 const FfnPart *__restrict__ parts, const float *__restrict__ pair_gate,
-                 const uint16_t *__restrict__ hp, float *__restrict__ pairbuf) {
+                 const FfnPart *__restrict__ parts, int pstride,
+                 const float *__restrict__ pair_gate, const uint16_t *__restrict__ hp,
+                 float *__restrict__ pairbuf) {
   __shared__ __attribute__((aligned(16))) uint8_t ring[(FFN_DN_DT + 1) * FFN_DN_PT * 1024];
   __shared__ __attribute__((aligned(16))) uint8_t dummy[FFN_WAVES * 1024];
+  const int die = (int)(blockIdx.x % N_XCD);   // this die's copy of the tables
+  hdr += die;
+  parts += (size_t)die * pstride;
   const int T = d / 16;                    // row tiles per expert
   const int upp = (T + FFN_WAVES - 1) / FFN_WAVES;
   const int step = (int)(gridDim.x / N_XCD);
@@ -520,12 +568,13 @@ hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
                          int I, int E, int K, int budget, int ns, const void *w13,
                          const void *w13s, const int32_t *sel_ids, const int32_t *n_sel,
                          const int32_t *offsets, const int32_t *pair_tok,
-                         const FfnHdr *hdr, const FfnPart *parts, int n_cu, const void *xp,
-                         void *H, hipStream_t st) {
+                         const FfnHdr *hdr, const FfnPart *parts, int n_cu,
+                         const uint32_t *tokoff, void *H, hipStream_t st) {
   if (bf16) {
     launch_k(packed ? k_gateup_bf16<true> : k_gateup_bf16<false>, dim3(ffn_gu_grid(n_cu)),
              dim3(FFN_WAVES * WAVE), 0, st, d, I, E, ns, (const uint16_t *)w13,
-             (const uint16_t *)w13s, hdr, parts, (const uint16_t *)xp, (uint16_t *)H);
+             (const uint16_t *)w13s, hdr, parts, ffn_parts_bound(B, K, budget, ns, FFN_GU_PT),
+             (const uint16_t *)x, B, tokoff, (uint16_t *)H);
   } else {
     launch_k(k_gateup_f32, dim3(budget, (I + F32_WAVES - 1) / F32_WAVES),
                        dim3(F32_WAVES * WAVE), 0, st, (const float *)x, d, I,
@@ -544,7 +593,8 @@ hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K
   if (bf16) {
     launch_k(packed ? k_down_bf16<true> : k_down_bf16<false>, dim3(ffn_dn_grid(n_cu)),
              dim3(FFN_WAVES * WAVE), 0, st, d, I, E, ns, (const uint16_t *)w2,
-             (const uint16_t *)w2s, hdr, parts, pair_gate, (const uint16_t *)H, pairbuf);
+             (const uint16_t *)w2s, hdr, parts, ffn_parts_bound(B, K, budget, ns, FFN_DN_PT),
+             pair_gate, (const uint16_t *)H, pairbuf);
   } else {
     launch_k(k_down_f32, dim3(budget, (d + F32_WAVES - 1) / F32_WAVES),
                        dim3(F32_WAVES * WAVE), 0, st, d, I, E,

@@ -11,7 +11,6 @@ namespace basek {
 constexpr int MAX_K = 16;     // experts per token
 constexpr int MAX_E = 256;    // experts per layer
 constexpr int MAX_B = 1024;   // tokens per batch
-constexpr int FFN_PART = 64;  // tokens per task of the FFN's token gather
 
 // Events attached to the next kernel launch (per host thread): when set,
 // launch_k hands them to the dispatch itself, which records `start` as the
@@ -36,17 +35,30 @@ inline void launch_k(F kernel, dim3 grid, dim3 block, uint32_t shm, hipStream_t 
 
 constexpr int N_XCD = 8;   // accelerator dies, one L2 each
 
+// Token groups on dies.  The scoring launches keep a group of TOK_GROUP
+// consecutive tokens on one die, g on die g % N_XCD, so that a token's
+// logits are read where they were written (in that die's L2).  Workgroup b
+// of such a launch runs on die b % N_XCD; with `per` workgroups per group it
+// takes group g = b % N_XCD + N_XCD * (q / per) and share q % per of it (q =
+// b / N_XCD).  The launch has xcd_grid(groups, per) workgroups; those past
+// the last group have nothing to do.
+constexpr int TOK_GROUP = 16;
+__host__ __device__ inline int xcd_grid(int groups, int per) {
+  return N_XCD * ((groups + N_XCD - 1) / N_XCD) * per;
+}
+__device__ inline void xcd_group(int b, int per, int &g, int &share) {
+  const int q = b / N_XCD;
+  g = b % N_XCD + N_XCD * (q / per);
+  share = q % per;
+}
+
 constexpr int MAX_SHARED = 8;               // shared experts per layer
 constexpr int MAX_SLOTS = MAX_E + MAX_SHARED;  // kept slots + shared slots
 
-// Upper bounds (host-known) of the FFN token tiling for a batch: 16-pair
-// tiles and FFN_PART-token gather tasks over all kept slots and the ns shared
-// slots (B pairs each).
+// Upper bound (host-known) of the FFN's 16-pair tiles for a batch over all
+// kept slots and the ns shared slots (B pairs each).
 inline int ffn_max_tiles(int B, int K, int budget, int ns) {
   return (B * K + 15) / 16 + budget + ns * ((B + 15) / 16);
-}
-inline int ffn_max_parts(int B, int K, int budget, int ns) {
-  return (B * K + FFN_PART - 1) / FFN_PART + budget + ns * ((B + FFN_PART - 1) / FFN_PART);
 }
 
 // The grouped bf16 FFN (see "Grouped bf16 FFN" in ffn.hip).  A part is at
@@ -66,6 +78,14 @@ constexpr int FFN_DN_DT = 3;
 constexpr int FFN_DN_WPE = 6;
 constexpr int FFN_GU_PT = 6;
 constexpr int FFN_DN_PT = 8;
+// gate/up reads its token rows straight from the hidden states: row i of
+// part k of the gate/up table is the byte offset of its token's row,
+// tokoff[k * FFN_GU_TOK + i] = t * d * 2 (FFN_TOK_PAD past the part's pairs:
+// a buffer load there returns zero)
+constexpr int FFN_GU_TOK = FFN_GU_PT * 16;
+constexpr uint32_t FFN_TOK_PAD = 0x80000000u;
+static_assert(FFN_GU_PT <= FFN_WAVES, "one token tile per gate/up wavefront");
+static_assert((size_t)MAX_B * 16384 * 2 < FFN_TOK_PAD, "token row offsets below the pad mark");
 
 // A part of a slot's pairs: expert u (u >= E: shared expert u - E), its
 // first 16-pair tile in the token operand, its tile count, its first pair
@@ -95,25 +115,20 @@ __host__ __device__ inline unsigned ffn_cu_grid(int n_cu) { return (unsigned)(((
 __host__ __device__ inline unsigned ffn_gu_grid(int n_cu) { return ffn_cu_grid(n_cu); }
 __host__ __device__ inline unsigned ffn_dn_grid(int n_cu) { return 3u * ffn_cu_grid(n_cu); }
 
-// rows: n_router of Wr (logits, + beta), n_pred of A (q), then the vector G
-// when given (gdot); ss: ||x||^2 when given
+// rows: n_router of Wr (logits, + beta), then the vector G when given (gdot)
 hipError_t launch_scores(bool bf16, const void *x, int B, int d, const float *Wr,
-                         const float *beta, int n_router, const float *A,
-                         int n_pred, const float *G, float *logits, float *q,
-                         float *gdot, float *ss, hipStream_t st);
+                         const float *beta, int n_router, const float *G, float *logits,
+                         float *gdot, hipStream_t st);
 // Selection rules (the values of BASE_SCORE_* in base.h): the per-pair
 // score k_tail writes as the cost
 constexpr int SCORE_BASE = 0, SCORE_TOP1 = 1, SCORE_WEIGHT = 2, SCORE_WEIGHT_SQ = 3,
               SCORE_STATIC = 4;
 // mode bit 0: top-K + weights from logits; bit 1: per-pair scores of `rule`
-// (SCORE_BASE: from q / ss)
-hipError_t launch_tail(int B, int E, int K, int norm_topk, const float *logits,
-                       const float *q, const float *ss, const float *bp,
+// (SCORE_BASE: the predictor a_u . x / ||x|| from x (rows of d) and A)
+hipError_t launch_tail(bool bf16, int B, int E, int K, int d, int norm_topk,
+                       const float *logits, const void *x, const float *A, const float *bp,
                        int32_t *ids, float *w, float *cost, int mode, int rule,
                        hipStream_t st);
-hipError_t launch_predict(bool bf16, const void *x, int B, int d, int E, int K,
-                          const int32_t *ids, const float *w, const float *A,
-                          const float *bp, float *cost, hipStream_t st);
 // binary: rank by (score > 0) instead of the score (the top-1-union rule)
 hipError_t launch_select(int B, int K, int E, const int32_t *ids,
                          const float *cost, int budget, bool binary, float *scores,
@@ -131,18 +146,18 @@ hipError_t launch_backfill(int B, int E, int K, int norm_topk, int flags,
                            int32_t *exec_ids, float *exec_gates,
                            hipStream_t st);
 // ns shared slots follow the kept ones (expert E + i, every token, gate
-// sigmoid(gdot[t]) or 1 when gdot is null).  With x_bf16 (the layer's bf16
-// hidden states, rows of d) the same launch also writes the FFN's token
-// operand xp, its part tables (parts_gu, parts_dn, each of at most
-// ffn_parts_bound rows) and their header; n_cu: the device's compute units
-// (the FFN launches' sizes follow from it).
+// sigmoid(gdot[t]) or 1 when gdot is null).  With `tables` (bf16 layers)
+// the same launch also writes the FFN's part tables (parts_gu, parts_dn,
+// each of at most ffn_parts_bound rows), their header and gate/up's token
+// row offsets (tokoff, FFN_GU_TOK per gate/up part; d: the hidden size);
+// n_cu: the device's compute units (the FFN launches' sizes follow from it).
 hipError_t launch_compact(int B, int K, int E, int budget, int ns, const int32_t *exec_ids,
                           const float *exec_gates, const int32_t *slot_of,
                           const int32_t *n_sel, const float *gdot, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
-                          int32_t *pair_of, const int32_t *sel_ids, const void *x_bf16, int d,
-                          int I, void *xp, FfnHdr *hdr, FfnPart *parts_gu, FfnPart *parts_dn,
-                          int n_cu, hipStream_t st);
+                          int32_t *pair_of, const int32_t *sel_ids, bool tables, int d,
+                          int I, uint32_t *tokoff, FfnHdr *hdr, FfnPart *parts_gu,
+                          FfnPart *parts_dn, int n_cu, hipStream_t st);
 hipError_t launch_pack(const void *w13, const void *w2, void *w13p, void *w2p,
                        int E, int d, int I, hipStream_t st);
 // parts of expert u >= E read the shared experts' weights (w13s / w2s, u - E)
@@ -151,8 +166,8 @@ hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
                          const void *w13s,
                          const int32_t *sel_ids, const int32_t *n_sel,
                          const int32_t *offsets, const int32_t *pair_tok,
-                         const FfnHdr *hdr, const FfnPart *parts, int n_cu, const void *xp,
-                         void *H, hipStream_t st);
+                         const FfnHdr *hdr, const FfnPart *parts, int n_cu,
+                         const uint32_t *tokoff, void *H, hipStream_t st);
 hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K,
                        int budget, int ns, const void *w2, const void *w2s,
                        const int32_t *sel_ids,

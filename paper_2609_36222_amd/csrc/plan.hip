@@ -214,6 +214,7 @@ void k_select(int B, int K, int E, const int32_t *__restrict__ ids,
 constexpr int BF_WAVES = 4;
 constexpr int SB_WAVES = SEL_THREADS / WAVE;   // wavefronts of k_select_backfill
 constexpr int SB_TOK = 2;                      // its tokens per workgroup (wavefronts 0 ..)
+static_assert(TOK_GROUP % SB_TOK == 0, "a token group in whole workgroups");
 
 // Per-wavefront LDS of the backfill
 template <int W>
@@ -366,8 +367,13 @@ void k_select_backfill(int B, int K, int E, const int32_t *__restrict__ ids,
   // the backfill's own loads first (its token's logits row and routes), so
   // that they are in flight while the selection runs
   const int lane = lane_id(), wv = wave_id();
+  int tg, tq;
+  xcd_group(blockIdx.x, TOK_GROUP / SB_TOK, tg, tq);
+  if (tg * TOK_GROUP >= B) return;
   const bool active = wv < SB_TOK;
-  const int t = blockIdx.x * SB_TOK + wv, tc = min(t, B - 1);
+  // the tokens of group tg sit on die tg % N_XCD, where their logits were
+  // written
+  const int t = tg * TOK_GROUP + tq * SB_TOK + wv, tc = min(t, B - 1);
   float lv[MAX_E / WAVE];
 #pragma unroll
   for (int i = 0; i < MAX_E / WAVE; ++i) {
@@ -392,41 +398,38 @@ void k_select_backfill(int B, int K, int E, const int32_t *__restrict__ ids,
                           lrow[active ? wv : 0], r_k, slot_s, n_sel, exec_ids, exec_gates);
 }
 
-// Exclusive prefixes over slots s < n of cnt[s] (pairs), ceil(cnt[s] / 16)
-// (16-pair tiles) and ceil(cnt[s] / FFN_PART) (FFN parts), by one
-// wavefront in one pass (SCAN_Q slots per lane); index SCAN_N receives each
-// total.
+// Exclusive prefixes over slots s < n of cnt[s] (pairs) and ceil(cnt[s] /
+// 16) (16-pair tiles), by one wavefront in one pass (SCAN_Q slots per
+// lane); index SCAN_N receives each total.
 constexpr int SCAN_Q = (MAX_SLOTS + WAVE - 1) / WAVE;
 constexpr int SCAN_N = SCAN_Q * WAVE;
-__device__ __forceinline__ void wave_scan3(const int *cnt, int n, int *off, int *tb, int *pb) {
+__device__ __forceinline__ void wave_scan2(const int *cnt, int n, int *off, int *tb) {
   const int lane = lane_id();
   constexpr int Q = SCAN_Q;
-  int l0[Q], l1[Q], l2[Q];
-  int s0 = 0, s1 = 0, s2 = 0;
+  int l0[Q], l1[Q];
+  int s0 = 0, s1 = 0;
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
     const int s = lane * Q + q;
     const int c = (s < n) ? cnt[s] : 0;
     l0[q] = c;
     l1[q] = (c + 15) / 16;
-    l2[q] = (c + FFN_PART - 1) / FFN_PART;
-    s0 += l0[q]; s1 += l1[q]; s2 += l2[q];
+    s0 += l0[q]; s1 += l1[q];
   }
-  int i0 = s0, i1 = s1, i2 = s2;
+  int i0 = s0, i1 = s1;
 #pragma unroll
   for (int h = 1; h < WAVE; h <<= 1) {
-    const int o0 = __shfl_up(i0, h, WAVE), o1 = __shfl_up(i1, h, WAVE),
-              o2 = __shfl_up(i2, h, WAVE);
-    if (lane >= h) { i0 += o0; i1 += o1; i2 += o2; }
+    const int o0 = __shfl_up(i0, h, WAVE), o1 = __shfl_up(i1, h, WAVE);
+    if (lane >= h) { i0 += o0; i1 += o1; }
   }
-  int r0 = i0 - s0, r1 = i1 - s1, r2 = i2 - s2;
+  int r0 = i0 - s0, r1 = i1 - s1;
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
     const int s = lane * Q + q;
-    off[s] = r0; tb[s] = r1; pb[s] = r2;
-    r0 += l0[q]; r1 += l1[q]; r2 += l2[q];
+    off[s] = r0; tb[s] = r1;
+    r0 += l0[q]; r1 += l1[q];
   }
-  if (lane == WAVE - 1) { off[SCAN_N] = i0; tb[SCAN_N] = i1; pb[SCAN_N] = i2; }
+  if (lane == WAVE - 1) { off[SCAN_N] = i0; tb[SCAN_N] = i1; }
 }
 
 // A slot of nt tiles cut into np = ceil(nt / pt) parts of balanced size:
@@ -469,16 +472,17 @@ __device__ __forceinline__ void wave_scan_counts(const int *cnt, int *pre) {
   if (lane == WAVE - 1) pre[SCAN_N] = inc;
 }
 
-// hr[s] = slots below s with more than one part (s <= SCAN_N; hr[SCAN_N]:
-// all of them), by one wavefront.
-__device__ __forceinline__ void wave_scan_multi(const int *tb, int nslot, int pt, int *hr) {
+// hr[s] = slots below s with more than one part, i.e. more than pt 16-pair
+// tiles (s <= SCAN_N; hr[SCAN_N]: all of them), from the slots' pair counts,
+// by one wavefront.
+__device__ __forceinline__ void wave_scan_multi(const int *cnt, int nslot, int pt, int *hr) {
   const int lane = lane_id();
   constexpr int Q = SCAN_Q;
   int l[Q], s = 0;
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
     const int i = lane * Q + q;
-    l[q] = (i < nslot && tb[i + 1] - tb[i] > pt) ? 1 : 0;
+    l[q] = (i < nslot && cnt[i] > 16 * pt) ? 1 : 0;
     s += l[q];
   }
   int inc = s;
@@ -508,18 +512,13 @@ constexpr int CP_THREADS = 1024;
 constexpr int CP_WAVES = CP_THREADS / WAVE;
 constexpr int CP_STAGE = 4096;   // pair gates staged in LDS per pass
 constexpr int CP_PAIRS = MAX_B * MAX_K;   // routed pairs at most
-constexpr int CP_MAXPARTS = CP_PAIRS / FFN_PART + MAX_E + MAX_SHARED * (MAX_B / FFN_PART);
 
-// A stable counting sort of the executed pairs by kept slot, then the FFN's
-// token operand.  Every workgroup of the launch makes the whole sort in its
-// own LDS (the same arithmetic, so the same result everywhere) and
-// workgroup 0 alone writes the plan; then all of them share the token
-// gather: for every (part, k-step) the part's hidden-state rows are copied
-// from x into xp in the FFN's fragment order (tile-major 1 KiB fragments:
-// fragment (tile, k-step) holds lane l = pair 16 tile' + l % 16 of the part's
-// tile, elements 32 k-step + 8 (l / 16) .. + 7; padding rows zeroed), with
-// streaming stores.  With x null (fp32 layers) there is no gather and one
-// workgroup.
+// A stable counting sort of the executed pairs by kept slot and (bf16
+// layers) the FFN's part tables.  With tables there is one workgroup per
+// die, each making the whole sort (the same arithmetic, so the same result
+// everywhere) and writing its die's copy of the tables, which the FFN's
+// workgroups on that die read from their own L2; workgroup 0 alone writes
+// the plan.  Without tables, one workgroup.
 // The routed pairs are taken in flat order q = t K + j, so sorting by (slot,
 // q) is sorting by (slot, token, rank).  Wavefront w owns the pairs w 64 PPT
 // + r 64 + lane (r = 0 .. PPT - 1, PPT pairs per thread, PPT * CP_THREADS >=
@@ -532,11 +531,30 @@ constexpr int CP_MAXPARTS = CP_PAIRS / FFN_PART + MAX_E + MAX_SHARED * (MAX_B / 
 // global stores are contiguous.  Then ns shared slots (slot n_sel + i runs
 // expert E + i for every token in token order, gate sigmoid(gdot[t]) =
 // 1 / (1 + exp(-s)) in fp32, or 1); offsets, the pair lists and pair_of
-// [B][K + ns] (and, with x, the FFN's operand and part tables, below).
+// [B][K + ns].
 // With 16 wavefronts on one CU every per-thread instruction costs about 16
 // cycles, so the per-pair work is kept short: no division (t = q / K as a
 // multiply-high by kmul = ceil(2^32 / K), exact for q < 2^32 / K, far above
 // B K), and every global load is issued before the first wait.
+//
+// The FFN's part tables (see "Grouped bf16 FFN" in ffn.hip), gate/up's and
+// down's.  Slot s (kept slots, then shared ones) has nt = tb[s + 1] - tb[s]
+// tiles, cut into parts of balanced size (part_split).  Every part of a
+// slot goes to one die in both tables (one L2 serves the expert's weights,
+// and down finds the activations gate/up wrote there), and the dies get
+// equal shares as far as whole slots allow: the slots with more than one
+// gate/up part are dealt round-robin first, then the others, i.e. slot s
+// takes deal position r = (its rank among the multi-part slots) or
+// H + (its rank among the others) (H multi-part slots) on die r % N_XCD.
+// A table lists the parts die by die, each die's in deal order (so the
+// multi-part slots, the heaviest, start first): a scan of the slots' part
+// counts in die-major order (j = x spd + r / N_XCD, spd slots per die at
+// most) gives every slot's first row and every die's first row.  Gate/up's
+// token rows: entry i of part row k is the byte offset in x of the row of
+// the part's pair i (tokoff[k * FFN_GU_TOK + i], written for its pairs
+// only; gate/up reads no entry at or past the part's pair count).
+// Die x's copy: hdr[x], rows x pstride_gu .. of parts_gu and tokoff (times
+// FFN_GU_TOK), rows x pstride_dn .. of parts_dn.
 template <int PPT>
 __global__ __launch_bounds__(CP_THREADS)
 void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
@@ -545,21 +563,20 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
                const int32_t *__restrict__ n_sel_p, const float *__restrict__ gdot,
                int32_t *__restrict__ offsets, int32_t *__restrict__ pair_tok,
                float *__restrict__ pair_gate, int32_t *__restrict__ pair_of,
-               const int32_t *__restrict__ sel_ids, const uint16_t *__restrict__ x, int d,
-               int I, uint16_t *__restrict__ xp, FfnHdr *__restrict__ hdr,
-               FfnPart *__restrict__ parts_gu, FfnPart *__restrict__ parts_dn, int n_cu) {
+               const int32_t *__restrict__ sel_ids, int tables, int d, int I,
+               uint32_t *__restrict__ tokoff, FfnHdr *__restrict__ hdr,
+               FfnPart *__restrict__ parts_gu, FfnPart *__restrict__ parts_dn,
+               int pstride_gu, int pstride_dn, int n_cu) {
   // cw[w][s]: pairs of slot s in wavefront w, then their first rank in slot s
   __shared__ int cw[CP_WAVES][MAX_E];
   __shared__ int cnt[SCAN_N];
   __shared__ int off[SCAN_N + 1];
   __shared__ int tb[SCAN_N + 1];
-  __shared__ int pb[SCAN_N + 1];
   __shared__ int sel_s[MAX_E];
   __shared__ int slot_s[MAX_E];
   __shared__ int stage_t[CP_PAIRS];     // token of every routed position
   __shared__ float stage_g[CP_STAGE];   // gates, CP_STAGE positions per pass
-  __shared__ int part_slot[CP_MAXPARTS];
-  __shared__ int np_gu[SCAN_N], np_dn[SCAN_N];          // FFN part tables (below)
+  __shared__ int np_gu[SCAN_N], np_dn[SCAN_N];          // the part tables' layout
   __shared__ int pre_gu[SCAN_N + 1], pre_dn[SCAN_N + 1];
   __shared__ int hr[SCAN_N + 1];
   const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
@@ -626,14 +643,37 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
   }
   if (tid >= n_sel && tid < n_sel + ns) cnt[tid] = B;
   __syncthreads();
-  if (tid < WAVE) wave_scan3(cnt, n_sel + ns, off, tb, pb);
+  const int nslot = n_sel + ns;
+  const int spd = (nslot + N_XCD - 1) / N_XCD;
+  // the slots' prefixes, and the tables' layout (die-major part counts)
+  if (wv == 0) wave_scan2(cnt, nslot, off, tb);
+  if (tables) {
+    if (wv == 1) wave_scan_multi(cnt, nslot, FFN_GU_PT, hr);
+    for (int j = tid - 2 * WAVE; j >= 0 && j < SCAN_N; j += CP_THREADS - 2 * WAVE)
+      np_gu[j] = np_dn[j] = 0;
+  }
   __syncthreads();
-  // the slot of every 64-token part
-  for (int s = wv; s < n_sel + ns; s += CP_WAVES)
-    for (int i = lane; i < pb[s + 1] - pb[s]; i += WAVE) part_slot[pb[s] + i] = s;
+  if (tables) {
+    for (int s = tid; s < nslot; s += CP_THREADS) {
+      const int nt = tb[s + 1] - tb[s], j = slot_j(s, hr, spd);
+      np_gu[j] = part_split(nt, FFN_GU_PT).np;
+      np_dn[j] = part_split(nt, FFN_DN_PT).np;
+    }
+  }
   const int routed = off[n_sel];   // pairs of the kept slots
   if (out && tid <= budget) offsets[tid] = (tid < n_sel) ? off[tid] : routed;
   if (out && tid < ns) offsets[budget + 1 + tid] = off[n_sel + tid + 1];
+  uint32_t *tko = tokoff + (size_t)blockIdx.x * pstride_gu * FFN_GU_TOK;
+  // gate/up's token row of pair pr of slot s (token t): its part row and
+  // entry
+  auto put_tok = [&](int s, int pr, int t) {
+    const PartSplit sp = part_split(tb[s + 1] - tb[s], FFN_GU_PT);
+    const int ti = pr >> 4, big = sp.ex * (sp.lo + 1);
+    const int q = ti < big ? ti / (sp.lo + 1) : sp.ex + (ti - big) / sp.lo;
+    const int tf = q * sp.lo + min(q, sp.ex);
+    const int row = pre_gu[slot_j(s, hr, spd)] + q;
+    tko[(size_t)row * FFN_GU_TOK + (pr - 16 * tf)] = (uint32_t)t * (uint32_t)d * 2u;
+  };
   // positions, pair_of, every routed position's token and the first pass
   // of gates
 #pragma unroll
@@ -648,140 +688,98 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
     }
     if (out && q < nq) pair_of[(size_t)t * kc + (q - t * K)] = p_r[r];
   }
-  __syncthreads();
-  if (out) {
-    for (int i = tid; i < routed; i += CP_THREADS) pair_tok[i] = stage_t[i];
-    // the gates, CP_STAGE positions per pass
-    for (int c0 = 0; c0 < routed; c0 += CP_STAGE) {
-      if (c0 > 0) {
-#pragma unroll
-        for (int r = 0; r < PPT; ++r) {
-          const int i = p_r[r] - c0;
-          if (s_r[r] >= 0 && i >= 0 && i < CP_STAGE) stage_g[i] = g_r[r];
-        }
-        __syncthreads();
+  if (tables) {
+    __syncthreads();   // np complete
+    if (wv < 2) wave_scan_counts(wv == 0 ? np_gu : np_dn, wv == 0 ? pre_gu : pre_dn);
+    __syncthreads();
+    if (wv == 0) {
+      // the header: every die's first rows, and gate/up's row group: the
+      // row-pair tiles per unit (FFN_WAVES down to FFN_WAVES / 2) that gives
+      // the fewest row-pair tiles to the busiest workgroup when every die's
+      // units are shared by its workgroups
+      int dg = 0, dd = 0;
+      if (lane <= N_XCD) {
+        const int j = min(lane * spd, SCAN_N);
+        dg = pre_gu[j];
+        dd = pre_dn[j];
       }
-      const int n = min(CP_STAGE, routed - c0);
-      for (int i = tid; i < n; i += CP_THREADS) pair_gate[c0 + i] = stage_g[i];
+      const int dprev = __shfl(dg, max(lane - 1, 0), WAVE);
+      int pd = (lane >= 1 && lane <= N_XCD) ? dg - dprev : 0;
+#pragma unroll
+      for (int h = 1; h < 16; h <<= 1) pd = max(pd, __shfl_xor(pd, h, WAVE));
+      const int T = I / 16;
+      const float per_die = (float)(ffn_gu_grid(n_cu) / N_XCD);
+      int best = FFN_WAVES, best_cost = 0x7FFFFFFF;
+#pragma unroll
+      for (int rp = FFN_WAVES; rp >= FFN_WAVES / 2; --rp) {
+        const int units = pd * ((T + rp - 1) / rp);
+        // rounds = ceil(units / per_die); exact in fp32 for these small integers
+        const int cost = (int)ceilf((float)units / per_die) * rp;
+        if (cost < best_cost) { best = rp; best_cost = cost; }
+      }
+      FfnHdr *hx = hdr + blockIdx.x;
+      if (lane <= N_XCD) {
+        hx->die_gu[lane] = dg;
+        hx->die_dn[lane] = dd;
+      }
+      if (lane == 0) {
+        hx->rp_gu = best;
+        hx->pad0 = 0;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < PPT; ++r)
+      if (s_r[r] >= 0) put_tok(s_r[r], p_r[r] - off[s_r[r]], (int)(((uint64_t)(uint32_t)(q0 + r * WAVE) * kmul) >> 32));
+    if (tid < B)
+      for (int i = 0; i < ns; ++i) put_tok(n_sel + i, tid, tid);
+    // the part records of this die's copy, one thread per slot
+    FfnPart *pg = parts_gu + (size_t)blockIdx.x * pstride_gu;
+    FfnPart *pdn = parts_dn + (size_t)blockIdx.x * pstride_dn;
+    for (int s = tid; s < nslot; s += CP_THREADS) {
+      const int u = s < n_sel ? sel_s[s] : E + (s - n_sel);
+      const int j = slot_j(s, hr, spd), nt = tb[s + 1] - tb[s];
+#pragma unroll
+      for (int tbl = 0; tbl < 2; ++tbl) {
+        const PartSplit sp = part_split(nt, tbl == 0 ? FFN_GU_PT : FFN_DN_PT);
+        FfnPart *dst = (tbl == 0 ? pg : pdn) + (tbl == 0 ? pre_gu[j] : pre_dn[j]);
+        for (int q = 0; q < sp.np; ++q) {
+          const int c = q < sp.ex ? sp.lo + 1 : sp.lo;
+          const int tf = q * sp.lo + min(q, sp.ex);   // the part's first tile in its slot
+          FfnPart rec;
+          rec.u = u;
+          rec.tile0 = tb[s] + tf;
+          rec.nt = c;
+          rec.p0 = off[s] + 16 * tf;
+          rec.n = min(16 * c, cnt[s] - 16 * tf);
+          rec.pad0 = rec.pad1 = rec.pad2 = 0;
+          dst[q] = rec;
+        }
+      }
+    }
+  }
+  if (!out) return;
+  __syncthreads();
+  for (int i = tid; i < routed; i += CP_THREADS) pair_tok[i] = stage_t[i];
+  // the gates, CP_STAGE positions per pass
+  for (int c0 = 0; c0 < routed; c0 += CP_STAGE) {
+    if (c0 > 0) {
+#pragma unroll
+      for (int r = 0; r < PPT; ++r) {
+        const int i = p_r[r] - c0;
+        if (s_r[r] >= 0 && i >= 0 && i < CP_STAGE) stage_g[i] = g_r[r];
+      }
       __syncthreads();
     }
-    if (tid < B) {
-      for (int i = 0; i < ns; ++i) {
-        const int p = off[n_sel + i] + tid;
-        pair_tok[p] = tid;
-        pair_gate[p] = gs;
-        pair_of[(size_t)tid * kc + K + i] = p;
-      }
-    }
+    const int n = min(CP_STAGE, routed - c0);
+    for (int i = tid; i < n; i += CP_THREADS) pair_gate[c0 + i] = stage_g[i];
+    __syncthreads();
   }
-  if (!x) return;
-  __syncthreads();   // part_slot complete
-  // The FFN's part tables (see "Grouped bf16 FFN" in ffn.hip), one per
-  // launch.  Slot s (kept slots, then shared ones) has nt = tb[s + 1] - tb[s]
-  // tiles, cut into parts of balanced size (part_split).  Every part of a
-  // slot goes to one die in both tables (one L2 serves the expert's weights,
-  // and down finds the activations gate/up wrote there), and the dies get
-  // equal shares as far as whole slots allow: the slots with more than one
-  // gate/up part are dealt round-robin first, then the others, i.e. slot s
-  // takes deal position r = (its rank among the multi-part slots) or
-  // H + (its rank among the others) (H multi-part slots) on die r % N_XCD.
-  // A table lists the parts die by die, each die's in deal order (so the
-  // multi-part slots, the heaviest, start first): a scan of the slots' part
-  // counts in die-major order (j = x spd + r / N_XCD, spd slots per die at
-  // most) gives every slot's first row and every die's first row.
-  const int nslot = n_sel + ns;
-  const int spd = (nslot + N_XCD - 1) / N_XCD;
-  if (wv == 0) wave_scan_multi(tb, nslot, FFN_GU_PT, hr);
-  for (int j = tid; j < SCAN_N; j += CP_THREADS) np_gu[j] = np_dn[j] = 0;
-  __syncthreads();
-  for (int s = tid; s < nslot; s += CP_THREADS) {
-    const int nt = tb[s + 1] - tb[s], j = slot_j(s, hr, spd);
-    np_gu[j] = part_split(nt, FFN_GU_PT).np;
-    np_dn[j] = part_split(nt, FFN_DN_PT).np;
-  }
-  __syncthreads();
-  if (wv < 2) wave_scan_counts(wv == 0 ? np_gu : np_dn, wv == 0 ? pre_gu : pre_dn);
-  __syncthreads();
-  if (out && tid == 0) {
-    // gate/up's row group: the row-pair tiles per unit (FFN_WAVES down to
-    // FFN_WAVES / 2) that gives the fewest row-pair tiles to the busiest
-    // workgroup when every die's units are shared by its workgroups
-    const int T = I / 16;
-    const float per_die = (float)(ffn_gu_grid(n_cu) / N_XCD);
-    FfnHdr h;
-    int parts_die = 0;
-    for (int x = 0; x <= N_XCD; ++x) {
-      const int j = min(x * spd, SCAN_N);
-      h.die_gu[x] = pre_gu[j];
-      h.die_dn[x] = pre_dn[j];
-      if (x > 0) parts_die = max(parts_die, h.die_gu[x] - h.die_gu[x - 1]);
-    }
-    int best = FFN_WAVES, best_cost = 0x7FFFFFFF;
-#pragma unroll
-    for (int rp = FFN_WAVES; rp >= FFN_WAVES / 2; --rp) {
-      const int units = parts_die * ((T + rp - 1) / rp);
-      // rounds = ceil(units / per_die); exact in fp32 for these small integers
-      const int cost = (int)ceilf((float)units / per_die) * rp;
-      if (cost < best_cost) { best = rp; best_cost = cost; }
-    }
-    h.rp_gu = best;
-    h.pad0 = 0;
-    *hdr = h;
-  }
-  for (int s = blockIdx.x * CP_WAVES + wv; s < nslot; s += gridDim.x * CP_WAVES) {
-    const int u = s < n_sel ? sel_s[s] : E + (s - n_sel);
-    const int j = slot_j(s, hr, spd), nt = tb[s + 1] - tb[s];
-#pragma unroll
-    for (int tbl = 0; tbl < 2; ++tbl) {
-      const PartSplit sp = part_split(nt, tbl == 0 ? FFN_GU_PT : FFN_DN_PT);
-      const int row0 = tbl == 0 ? pre_gu[j] : pre_dn[j];
-      for (int q = lane; q < sp.np; q += WAVE) {
-        const int c = q < sp.ex ? sp.lo + 1 : sp.lo;
-        const int tf = q * sp.lo + min(q, sp.ex);   // the part's first tile in its slot
-        FfnPart rec;
-        rec.u = u;
-        rec.tile0 = tb[s] + tf;
-        rec.nt = c;
-        rec.p0 = off[s] + 16 * tf;
-        rec.n = min(16 * c, cnt[s] - 16 * tf);
-        rec.pad0 = rec.pad1 = rec.pad2 = 0;
-        (tbl == 0 ? parts_gu : parts_dn)[row0 + q] = rec;
-      }
-    }
-  }
-  // the token gather: one wavefront per (part, k-step); every load of a
-  // task is issued before its first use
-  constexpr int NJ = FFN_PART / 16;
-  const int ksteps = d / 32;
-  const int tasks = pb[SCAN_N] * ksteps;
-  for (int v = blockIdx.x * CP_WAVES + wv; v < tasks; v += gridDim.x * CP_WAVES) {
-    const int q = v / ksteps, ks = v - q * ksteps;
-    const int s = part_slot[q];
-    const int pr = FFN_PART * (q - pb[s]);   // the part's first pair within its slot
-    const int p0 = off[s] + pr, n = min(FFN_PART, cnt[s] - pr);
-    const int tile0 = tb[s] + (FFN_PART / 16) * (q - pb[s]);
-    int tok[NJ];
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int k = min(16 * j + (lane & 15), n - 1);
-      tok[j] = s < n_sel ? stage_t[p0 + k] : pr + k;   // a shared slot lists every token
-    }
-    u32x4 v4[NJ];
-#pragma unroll
-    for (int j = 0; j < NJ; ++j)
-      v4[j] = *reinterpret_cast<const u32x4 *>(x + (size_t)tok[j] * d + 32 * ks + 8 * (lane >> 4));
-    // streaming stores: the fragments are read once, by the FFN's launch;
-    // stores left dirty in L2 would be written back when this launch ends,
-    // which the next launch waits for
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      if (16 * j < n) {
-        const bool pad = 16 * j + (lane & 15) >= n;
-        const u32x4 z = {0u, 0u, 0u, 0u};
-        __builtin_nontemporal_store(
-            pad ? z : v4[j],
-            reinterpret_cast<u32x4 *>(xp + (((size_t)(tile0 + j) * ksteps + ks) * WAVE + lane) * 8));
-      }
+  if (tid < B) {
+    for (int i = 0; i < ns; ++i) {
+      const int p = off[n_sel + i] + tid;
+      pair_tok[p] = tid;
+      pair_gate[p] = gs;
+      pair_of[(size_t)tid * kc + K + i] = p;
     }
   }
 }
@@ -800,7 +798,8 @@ hipError_t launch_select_backfill(int B, int K, int E, const int32_t *ids, const
                                   const float *logits, float *scores, int32_t *counts,
                                   int32_t *sel_ids, int32_t *n_sel, int32_t *slot_of,
                                   int32_t *exec_ids, float *exec_gates, hipStream_t st) {
-  launch_k(k_select_backfill, dim3((B + SB_TOK - 1) / SB_TOK), dim3(SEL_THREADS), 0, st,
+  launch_k(k_select_backfill, dim3(xcd_grid((B + TOK_GROUP - 1) / TOK_GROUP, TOK_GROUP / SB_TOK)),
+           dim3(SEL_THREADS), 0, st,
            B, K, E, ids, cost, budget, (int)binary, norm_topk, flags, logits, scores, counts,
            sel_ids, n_sel, slot_of, exec_ids, exec_gates);
   return hipGetLastError();
@@ -821,21 +820,19 @@ hipError_t launch_compact(int B, int K, int E, int budget, int ns, const int32_t
                           const float *exec_gates, const int32_t *slot_of,
                           const int32_t *n_sel, const float *gdot, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
-                          int32_t *pair_of, const int32_t *sel_ids,
-                          const void *x_bf16, int d, int I, void *xp, FfnHdr *hdr,
-                          FfnPart *parts_gu, FfnPart *parts_dn, int n_cu, hipStream_t st) {
+                          int32_t *pair_of, const int32_t *sel_ids, bool tables, int d,
+                          int I, uint32_t *tokoff, FfnHdr *hdr, FfnPart *parts_gu,
+                          FfnPart *parts_dn, int n_cu, hipStream_t st) {
   const int ppt = (B * K + CP_THREADS - 1) / CP_THREADS;
-  // with a gather: one wavefront per (part, k-step) at most, 256 workgroups
-  // at most (one per CU: each holds the whole sort in its LDS)
-  const long long tasks = (long long)ffn_max_parts(B, K, budget, ns) * (d / 32);
-  const unsigned blocks =
-      x_bf16 ? (unsigned)std::min<long long>(256, (tasks + CP_WAVES - 1) / CP_WAVES) : 1u;
   const uint64_t kmul = ((1ull << 32) + (uint64_t)K - 1) / (uint64_t)K;
+  const int sg = ffn_parts_bound(B, K, budget, ns, FFN_GU_PT);
+  const int sd = ffn_parts_bound(B, K, budget, ns, FFN_DN_PT);
+  const unsigned blocks = tables ? N_XCD : 1u;   // one copy of the tables per die
 #define BASE_COMPACT(P)                                                                    \
   launch_k(k_compact<P>, dim3(blocks), dim3(CP_THREADS), 0, st, B, K, kmul, E, budget, ns, \
            exec_ids, exec_gates, slot_of, n_sel, gdot, offsets, pair_tok, pair_gate,      \
-           pair_of, sel_ids, (const uint16_t *)x_bf16, d, I, (uint16_t *)xp, hdr,          \
-           parts_gu, parts_dn, n_cu)
+           pair_of, sel_ids, (int)tables, d, I, tokoff, hdr, parts_gu, parts_dn, sg, sd,  \
+           n_cu)
   if (ppt <= 1) BASE_COMPACT(1);
   else if (ppt <= 2) BASE_COMPACT(2);
   else if (ppt <= 4) BASE_COMPACT(4);
