@@ -71,8 +71,8 @@ inline int ffn_max_tiles(int B, int K, int budget, int ns) {
 constexpr int FFN_WAVES = 8;
 constexpr int FFN_GU_DW = 8;
 constexpr int FFN_GU_DT = 2;
-constexpr int FFN_DN_DW = 3;
-constexpr int FFN_DN_DT = 3;
+constexpr int FFN_DN_DW = 2;
+constexpr int FFN_DN_DT = 2;
 // wavefronts per SIMD the down kernel's registers allow: three workgroups
 // per CU, so that a die's down units mostly run in one round
 constexpr int FFN_DN_WPE = 6;

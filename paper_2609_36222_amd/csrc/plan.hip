@@ -32,7 +32,7 @@ struct SelLds {
   float CS[SEL_THREADS];
   float D[MAX_E];
   int cnt[MAX_E];
-  uint64_t key[MAX_E];
+  __attribute__((aligned(16))) uint64_t key[MAX_E];
   int rnk[MAX_E];
   int n_union;
 };
@@ -80,11 +80,13 @@ __device__ __forceinline__ int select_body(SelLds &S, int B, int K, int E, int b
     }
     __syncthreads();
     if (tid < nb * E) {
-      float v[WAVE];
+      // the tree's first level as the row is read (positions q, q + 32)
+      float v[WAVE / 2];
 #pragma unroll
-      for (int q = 0; q < WAVE; ++q) v[q] = S.V[tid * SEL_PAD + q];
+      for (int q = 0; q < WAVE / 2; ++q)
+        v[q] = S.V[tid * SEL_PAD + q] + S.V[tid * SEL_PAD + q + WAVE / 2];
 #pragma unroll
-      for (int h = WAVE / 2; h >= 1; h >>= 1)
+      for (int h = WAVE / 4; h >= 1; h >>= 1)
 #pragma unroll
         for (int q = 0; q < h; ++q) v[q] = v[q] + v[q + h];
       S.CS[tid] = v[0];
@@ -96,25 +98,44 @@ __device__ __forceinline__ int select_body(SelLds &S, int B, int K, int E, int b
     __syncthreads();
   }
 
-  for (int u = tid; u < ((E + WAVE - 1) & ~(WAVE - 1)); u += SEL_THREADS) {
+  // E2: the power of two >= E (at least a wavefront); keys past E are 0
+  int E2 = WAVE;
+  while (E2 < E) E2 <<= 1;
+  for (int u = tid; u < E2; u += SEL_THREADS) {
     const bool in = u < E && S.cnt[u] > 0;
-    if (u < E) {
-      const float kv = binary ? (S.D[u] > 0.0f ? 1.0f : 0.0f) : S.D[u];
-      S.key[u] = in ? rank_key(kv, u) : 0;   // 0: ranks after every expert
-    }
+    float kv = 0.0f;
+    if (u < E) kv = binary ? (S.D[u] > 0.0f ? 1.0f : 0.0f) : S.D[u];
+    S.key[u] = in ? rank_key(kv, u) : 0;   // 0: ranks after every expert
     const uint64_t m = __ballot(in);
     if (lane == 0 && m) atomicAdd(&S.n_union, (int)__popcll(m));
   }
   __syncthreads();
   const int n_sel = min(budget, S.n_union);
   {
-    // tpe consecutive threads per expert, each over a share of the keys
-    const int tpe = E <= 64 ? 16 : E <= 128 ? 8 : 4;
+    // tpe consecutive threads per expert, thread `part` over the key pairs
+    // part, part + tpe, ... (16 bytes each: the tpe threads of an expert
+    // read consecutive bytes, distinct banks); the keys past E are 0 and
+    // never count
+    const int tpe = SEL_THREADS / E2, npair = E2 / (2 * tpe);
     const int u = tid / tpe, part = tid % tpe;
     int r = 0;
     if (u < E && S.cnt[u] > 0) {
       const uint64_t ku = S.key[u];
-      for (int v = part; v < E; v += tpe) r += S.key[v] > ku;
+      // up to 8 pairs per step, their LDS reads issued together
+      for (int i0 = 0; i0 < npair; i0 += 8) {
+        u32x4 o[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (i0 + q < npair)
+            o[q] = *reinterpret_cast<const u32x4 *>(&S.key[2 * (part + tpe * (i0 + q))]);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          if (i0 + q < npair) {
+            r += (((uint64_t)o[q].y << 32 | o[q].x) > ku);
+            r += (((uint64_t)o[q].w << 32 | o[q].z) > ku);
+          }
+        }
+      }
     }
     for (int h = 1; h < tpe; h <<= 1) r += __shfl_xor(r, h, WAVE);
     if (u < E && part == 0) S.rnk[u] = r;
@@ -219,7 +240,7 @@ static_assert(TOK_GROUP % SB_TOK == 0, "a token group in whole workgroups");
 // Per-wavefront LDS of the backfill
 template <int W>
 struct BfLds {
-  uint64_t kk[W][MAX_E];
+  __attribute__((aligned(16))) uint64_t kk[W][MAX_E];
   int ke[W][MAX_E];
   int xs[W][MAX_K];
   float num_s[W][MAX_K];
@@ -282,17 +303,24 @@ __device__ __forceinline__ void backfill_body(BfLds<W> &S, bool active, int t, i
         n_kept += __popcll(m);
       }
       if (lane == 0) S.nx_s[wv] = min(min(K, n_sel), n_kept);
-      if (n_kept & 1) { if (lane == 0) S.kk[wv][n_kept] = 0; }
+      // keys 0 (ranked after every expert) up to a multiple of 16
+      if (n_kept + lane < ((n_kept + 15) & ~15)) S.kk[wv][n_kept + lane] = 0;
     }
     __syncthreads();
     const int kp = min(K, n_sel);
     for (int s = lane; s < n_kept; s += WAVE) {
       const uint64_t ks = S.kk[wv][s];
       int r = 0;
-      for (int f = 0; f < n_kept; f += 2) {
-        const u32x4 o = *reinterpret_cast<const u32x4 *>(&S.kk[wv][f]);
-        r += (((uint64_t)o.y << 32 | o.x) > ks);
-        r += (((uint64_t)o.w << 32 | o.z) > ks);
+      // 16 keys per step, their LDS reads issued together
+      for (int f = 0; f < n_kept; f += 16) {
+        u32x4 o[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) o[q] = *reinterpret_cast<const u32x4 *>(&S.kk[wv][f + 2 * q]);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          r += (((uint64_t)o[q].y << 32 | o[q].x) > ks);
+          r += (((uint64_t)o[q].w << 32 | o[q].z) > ks);
+        }
       }
       if (r < kp) S.xs[wv][r] = S.ke[wv][s];
     }
@@ -446,6 +474,7 @@ __device__ __forceinline__ PartSplit part_split(int nt, int pt) {
   return {np, lo, nt - lo * np};
 }
 static_assert((MAX_B / 16) * (MAX_B / 16) < 65536, "part_split's quotient");
+static_assert((MAX_B / 16) * (FFN_GU_PT + 1) < 65536, "put_tok's quotients");
 // pre[j] = cnt[0] + ... + cnt[j - 1] (j <= SCAN_N; pre[SCAN_N]: the
 // total), by one wavefront.
 __device__ __forceinline__ void wave_scan_counts(const int *cnt, int *pre) {
@@ -579,6 +608,9 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
   __shared__ int np_gu[SCAN_N], np_dn[SCAN_N];          // the part tables' layout
   __shared__ int pre_gu[SCAN_N + 1], pre_dn[SCAN_N + 1];
   __shared__ int hr[SCAN_N + 1];
+  __shared__ int sj_s[SCAN_N];           // slot -> its die-major scan position j
+  __shared__ uint32_t sp_s[SCAN_N];      // slot -> its gate/up part split, packed
+  __shared__ uint32_t rc_s[2][SCAN_N];   // slot -> ceil(2^16 / (lo + 1)), ceil(2^16 / lo)
   const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
   const bool out = blockIdx.x == 0;     // the workgroup that writes the plan
   const int kc = K + ns;   // columns of pair_of
@@ -656,8 +688,14 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
   if (tables) {
     for (int s = tid; s < nslot; s += CP_THREADS) {
       const int nt = tb[s + 1] - tb[s], j = slot_j(s, hr, spd);
-      np_gu[j] = part_split(nt, FFN_GU_PT).np;
+      const PartSplit sg = part_split(nt, FFN_GU_PT);
+      np_gu[j] = sg.np;
       np_dn[j] = part_split(nt, FFN_DN_PT).np;
+      sj_s[s] = j;
+      // lo (<= FFN_GU_PT) and ex (< np <= MAX_B / 16) for put_tok
+      sp_s[s] = (uint32_t)sg.lo | ((uint32_t)sg.ex << 8);
+      rc_s[0][s] = (65536u + (uint32_t)sg.lo) / (uint32_t)(sg.lo + 1);
+      rc_s[1][s] = (65536u + (uint32_t)sg.lo - 1u) / (uint32_t)max(sg.lo, 1);
     }
   }
   const int routed = off[n_sel];   // pairs of the kept slots
@@ -665,13 +703,18 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
   if (out && tid < ns) offsets[budget + 1 + tid] = off[n_sel + tid + 1];
   uint32_t *tko = tokoff + (size_t)blockIdx.x * pstride_gu * FFN_GU_TOK;
   // gate/up's token row of pair pr of slot s (token t): its part row and
-  // entry
+  // entry.  The part of tile ti: the first ex parts have lo + 1 tiles, the
+  // others lo; the quotients as multiply-highs by ceil(2^16 / divisor),
+  // exact for ti < 2^16 / FFN_GU_PT (a slot has at most MAX_B / 16 tiles).
   auto put_tok = [&](int s, int pr, int t) {
-    const PartSplit sp = part_split(tb[s + 1] - tb[s], FFN_GU_PT);
-    const int ti = pr >> 4, big = sp.ex * (sp.lo + 1);
-    const int q = ti < big ? ti / (sp.lo + 1) : sp.ex + (ti - big) / sp.lo;
-    const int tf = q * sp.lo + min(q, sp.ex);
-    const int row = pre_gu[slot_j(s, hr, spd)] + q;
+    const uint32_t pk = sp_s[s];
+    const int lo = (int)(pk & 0xFFu), ex = (int)(pk >> 8);
+    const int ti = pr >> 4, big = ex * (lo + 1);
+    const uint32_t a = (uint32_t)(ti < big ? ti : ti - big);
+    const int qq = (int)((a * rc_s[ti < big ? 0 : 1][s]) >> 16);
+    const int q = ti < big ? qq : ex + qq;
+    const int tf = q * lo + min(q, ex);
+    const int row = pre_gu[sj_s[s]] + q;
     tko[(size_t)row * FFN_GU_TOK + (pr - 16 * tf)] = (uint32_t)t * (uint32_t)d * 2u;
   };
   // positions, pair_of, every routed position's token and the first pass
