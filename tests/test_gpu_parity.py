@@ -123,6 +123,8 @@ def run_case(gu, inp, budget, flags=0, norm_topk=1, with_residual=False,
     y_staged = gu.to_np_f32(y)
     if check_y:
         err = np.max(np.abs(y_staged.astype(np.float64) - ref["y"]))
+        _flush(f"y max-abs error {err:.3e} (bar {Y_TOL[sh.bf16]:.0e}, "
+               f"max |y| {np.max(np.abs(ref['y'])):.3e})")
         assert err <= Y_TOL[sh.bf16], err
     # fused layer: bit-identical to the staged calls
     ws2 = gl.workspace(B, budget)
