@@ -93,7 +93,7 @@ base_status check_ptr(const void *p, size_t a) {
 struct Layout {
   size_t logits, gdot, topk_ids, topk_w, cost, scores, counts, sel_ids, n_sel,
       slot_of, exec_ids, exec_gates, offsets, pair_tok, pair_gate, pair_of,
-      hdr, parts_gu, parts_dn, tokoff, H, pairbuf, total;
+      hdr, units_gu, units_dn, tokoff, H, pairbuf, total;
 };
 
 size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -127,12 +127,13 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
   o.pair_of = take((size_t)B * (L->K + ns) * 4);
   // the FFN's part tables and their header (bf16)
   const bool bf = L->dtype == BASE_BF16;
-  // (one copy per die: the FFN's workgroups read their die's copy)
-  const size_t cp = bf ? N_XCD : 0;
-  o.hdr = take(cp * sizeof(FfnHdr));
-  o.parts_gu = take(cp * ffn_parts_bound(B, L->K, bc, ns, FFN_GU_PT) * sizeof(FfnPart));
-  o.parts_dn = take(cp * ffn_parts_bound(B, L->K, bc, ns, FFN_DN_PT) * sizeof(FfnPart));
-  o.tokoff = take(cp * ffn_parts_bound(B, L->K, bc, ns, FFN_GU_PT) * FFN_GU_TOK * 4);
+  // (one header per die; every die's run of units written on that die)
+  const size_t ug = bf ? (size_t)ffn_units_bound_gu(B, L->K, bc, ns, L->I) : 0;
+  const size_t ud = bf ? (size_t)ffn_units_bound_dn(B, L->K, bc, ns, L->d) : 0;
+  o.hdr = take(bf ? N_XCD * sizeof(FfnHdr) : 0);
+  o.units_gu = take(ug * sizeof(FfnUnit));
+  o.units_dn = take(ud * sizeof(FfnUnit));
+  o.tokoff = take(ug * FFN_GU_TOK * 4);
   if (L->dtype == BASE_BF16) {
     // fragment-ordered SwiGLU activations (16-pair tiles)
     const size_t tiles = (size_t)ffn_max_tiles(B, L->K, bc, ns);
@@ -234,25 +235,25 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
   const int ns = L->n_shared;
   const int n_cu = device_cus();
   FfnHdr *hdr = at<FfnHdr>(ws, o.hdr);
-  FfnPart *parts_gu = at<FfnPart>(ws, o.parts_gu), *parts_dn = at<FfnPart>(ws, o.parts_dn);
+  FfnUnit *units_gu = at<FfnUnit>(ws, o.units_gu), *units_dn = at<FfnUnit>(ws, o.units_dn);
   uint32_t *tokoff = at<uint32_t>(ws, o.tokoff);
   // the same launch lists the FFN's parts and gate/up's token rows (bf16)
   HIP_TRY(launch_compact(B, L->K, L->E, bc, ns, exec_ids, exec_gates, slot_of, n_sel,
                          shared_gate(L) ? at<float>(ws, o.gdot) : nullptr, offsets,
                          pair_tok, pair_gate, pair_of, sel_ids, bf16, L->d, L->I, tokoff,
-                         hdr, parts_gu, parts_dn, n_cu, st));
+                         hdr, units_gu, units_dn, n_cu, st));
   stage_end(st);
   stage(5);   // no launch of its own: gate/up gathers its tokens itself
   stage_end(st);
   stage(6);
   const bool packed = L->w_layout == BASE_W_PACKED;
   HIP_TRY(launch_gateup(bf16, packed, x, B, L->d, L->I, L->E, L->K, bc, ns, L->w13,
-                        L->w13_shared, sel_ids, n_sel, offsets, pair_tok, hdr, parts_gu, n_cu,
+                        L->w13_shared, sel_ids, n_sel, offsets, pair_tok, hdr, units_gu, n_cu,
                         tokoff, at<void>(ws, o.H), st));
   stage_end(st);
   stage(7);
   HIP_TRY(launch_down(bf16, packed, B, L->d, L->I, L->E, L->K, bc, ns, L->w2,
-                      L->w2_shared, sel_ids, n_sel, offsets, hdr, parts_dn, n_cu, pair_gate,
+                      L->w2_shared, sel_ids, n_sel, offsets, hdr, units_dn, n_cu, pair_gate,
                       at<void>(ws, o.H), at<float>(ws, o.pairbuf), st));
   stage_end(st);
   stage(8);
@@ -520,18 +521,18 @@ base_status base_calib_accumulate(const base_layer *L, const void *z, int32_t B,
   int32_t *pair_tok = at<int32_t>(ws, o.pair_tok);
   const int n_cu = device_cus();
   FfnHdr *hdr = at<FfnHdr>(ws, o.hdr);
-  FfnPart *parts_gu = at<FfnPart>(ws, o.parts_gu), *parts_dn = at<FfnPart>(ws, o.parts_dn);
+  FfnUnit *units_gu = at<FfnUnit>(ws, o.units_gu), *units_dn = at<FfnUnit>(ws, o.units_dn);
   HIP_TRY(launch_compact(B, C.K, C.E, bc, 0, at<int32_t>(ws, o.exec_ids),
                          at<float>(ws, o.exec_gates), slot, nsel, nullptr, offsets, pair_tok,
                          at<float>(ws, o.pair_gate), at<int32_t>(ws, o.pair_of), sel,
-                         bf16, C.d, C.I, at<uint32_t>(ws, o.tokoff), hdr, parts_gu, parts_dn,
+                         bf16, C.d, C.I, at<uint32_t>(ws, o.tokoff), hdr, units_gu, units_dn,
                          n_cu, st));
   const bool packed = C.w_layout == BASE_W_PACKED;
   HIP_TRY(launch_gateup(bf16, packed, z, B, C.d, C.I, C.E, C.K, bc, 0, C.w13, nullptr, sel,
-                        nsel, offsets, pair_tok, hdr, parts_gu, n_cu, at<uint32_t>(ws, o.tokoff),
+                        nsel, offsets, pair_tok, hdr, units_gu, n_cu, at<uint32_t>(ws, o.tokoff),
                         at<void>(ws, o.H), st));
   HIP_TRY(launch_down(bf16, packed, B, C.d, C.I, C.E, C.K, bc, 0, C.w2, nullptr, sel, nsel,
-                      offsets, hdr, parts_dn, n_cu, at<float>(ws, o.pair_gate),
+                      offsets, hdr, units_dn, n_cu, at<float>(ws, o.pair_gate),
                       at<void>(ws, o.H), at<float>(ws, o.pairbuf), st));
   double *inv = at<double>(ws, o.total);
   double *y = at<double>(ws, o.total + up256((size_t)B * 8));

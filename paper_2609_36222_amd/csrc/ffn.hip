@@ -64,14 +64,15 @@ __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "mem
 // Grouped bf16 FFN (K3, K4).  Work is cut by the compaction launch into
 // parts: a kept (or shared) slot's pairs, as 16-pair tiles, split into parts
 // of at most FFN_GU_PT (gate/up) or FFN_DN_PT (down) tiles of balanced size.
-// Every slot is dealt to one die (an expert's weights are read through one
-// L2, and down finds there the activations gate/up wrote), the slots with
-// several parts first, and each die's parts are consecutive rows of the
-// launch's part table (FfnPart, written by k_compact).  A unit is (part, row
-// group); the units of die x are taken by the workgroups that run on die x
-// (workgroup b runs on die b % N_XCD), workgroup b taking units b / N_XCD,
-// b / N_XCD + gridDim.x / N_XCD, ... of its die, so the heaviest parts start
-// first.
+// A unit is (part, row group).  The launch's units are numbered slot by slot
+// and, within a slot, row group by row group, and cut into one run of equal
+// length per die (FfnUnit records and per-die headers, written by
+// k_compact): a row group's weights are read through one L2 by all the parts
+// that need them, and every die has the same number of units, whether the
+// kept slots are many or few.  The units of die x are taken by the
+// workgroups that run on die x (workgroup b runs on die b % N_XCD),
+// workgroup b taking units b / N_XCD, b / N_XCD + gridDim.x / N_XCD, ... of
+// its die's run.
 //
 // Inside a unit every wavefront owns its rows over the whole contraction (so
 // it finishes its outputs alone, in one fixed order: k ascending), and the
@@ -120,13 +121,22 @@ __device__ __forceinline__ uint32_t ksoff(const TileSrc &s, int ks, int KS) {
 // that the addresses derived from it stay in scalar registers (a buffer
 // resource held in vector registers would turn each load into a loop).
 struct PartU {
-  int u, tile0, nt, p0, n;
+  int u, tile0, nt, p0, n, rg;
 };
-__device__ __forceinline__ PartU load_part(const FfnPart *p) {
-  const FfnPart r = *p;
+__device__ __forceinline__ PartU load_unit(const FfnUnit *p) {
+  const FfnUnit r = *p;
   return {__builtin_amdgcn_readfirstlane(r.u), __builtin_amdgcn_readfirstlane(r.tile0),
           __builtin_amdgcn_readfirstlane(r.nt), __builtin_amdgcn_readfirstlane(r.p0),
-          __builtin_amdgcn_readfirstlane(r.n)};
+          __builtin_amdgcn_readfirstlane(r.n), __builtin_amdgcn_readfirstlane(r.rg)};
+}
+// This workgroup's die's run of a unit table, [u0, u1), and its first unit
+// and stride (workgroup b runs on die b % N_XCD).
+struct Run {
+  int k0, k1, step;
+};
+__device__ __forceinline__ Run die_run(const int32_t &u0, const int32_t &u1) {
+  return {__builtin_amdgcn_readfirstlane(u0) + (int)(blockIdx.x / N_XCD),
+          __builtin_amdgcn_readfirstlane(u1), (int)(gridDim.x / N_XCD)};
 }
 
 // One unit of gate/up: wavefront w owns row-pair tile r = rp0 + w (gate rows
@@ -266,13 +276,13 @@ __device__ __forceinline__ void gateup_unit(uint8_t *ring, uint8_t *dummy, int d
 // One unit of down: wavefront w owns row tile rt = rt0 + w (rows 16 rt ..
 // 16 rt + 15 of W_d), if w < nrt; the tokens are the part's SwiGLU
 // activations.  pairbuf[p][c] = gate_p * (H[p] . W_d[c]).
-template <int NT, bool PACKED>
+template <int NT, bool PACKED, int DW>
 __device__ __forceinline__ void down_unit(uint8_t *ring, uint8_t *dummy, int d, int I,
                                           const uint16_t *__restrict__ w2, const PartU &pt,
                                           int rt0, int nrt, const float *__restrict__ pair_gate,
                                           const uint16_t *__restrict__ hp,
                                           float *__restrict__ pairbuf) {
-  constexpr int W = FFN_WAVES, DW = FFN_DN_DW, DT = FFN_DN_DT;
+  constexpr int W = FFN_WAVES, DT = FFN_DN_DT;
   constexpr int NTK = (NT + W - 1) / W;
   const int w = wave_id_u(), lane = lane_id();
   const int KS = I / 32;
@@ -364,53 +374,38 @@ __device__ __forceinline__ void down_unit(uint8_t *ring, uint8_t *dummy, int d, 
   }
 }
 
-// The units of this workgroup's die, in order: unit m of die x is the die's
-// part m / upp (table rows die[x] .. die[x + 1] - 1), row group m % upp.
-// Returns false past the die's last unit.
-__device__ __forceinline__ bool next_unit(const int32_t *die, int m, int upp, int &k, int &rg) {
-  const int x = (int)(blockIdx.x % N_XCD);
-  k = __builtin_amdgcn_readfirstlane(die[x]) + m / upp;
-  rg = m % upp;
-  return k < __builtin_amdgcn_readfirstlane(die[x + 1]);
-}
-
 // gate/up: up to FFN_WAVES row-pair tiles per unit (hdr->rp_gu, chosen by
 // the compaction launch), the part's tiles shared through the LDS ring.
 template <bool PACKED>
 __global__ __launch_bounds__(FFN_WAVES * WAVE)
 void k_gateup_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w13r,
                    const uint16_t *__restrict__ w13s, const FfnHdr *__restrict__ hdr,
-                   const FfnPart *__restrict__ parts, int pstride,
-                   const uint16_t *__restrict__ x, int B, const uint32_t *__restrict__ tokoff,
-                   uint16_t *__restrict__ hp) {
+                   const FfnUnit *__restrict__ units, const uint16_t *__restrict__ x, int B,
+                   const uint32_t *__restrict__ tokoff, uint16_t *__restrict__ hp) {
   __shared__ __attribute__((aligned(16))) uint8_t ring[(FFN_GU_DT + 1) * FFN_GU_PT * 2048];
   __shared__ __attribute__((aligned(16))) uint8_t dummy[FFN_WAVES * 1024];
-  // this die's copy of the tables (written by the compaction workgroup
-  // that ran on the same die)
-  const int die = (int)(blockIdx.x % N_XCD);
-  hdr += die;
-  parts += (size_t)die * pstride;
-  tokoff += (size_t)die * pstride * FFN_GU_TOK;
+  // this die's header and run (written by the compaction workgroup that
+  // ran on the same die)
+  hdr += blockIdx.x % N_XCD;
   const int RP = __builtin_amdgcn_readfirstlane(hdr->rp_gu);
   const int T = I / 16;                    // row-pair tiles per expert
   if (RP < 1 || RP > FFN_WAVES) return;    // only for a plan not made by k_compact
-  const int upp = (T + RP - 1) / RP;
-  const int step = (int)(gridDim.x / N_XCD);
+  const Run run = die_run(hdr->gu0, hdr->gu1);
   const rsrc_t rx = make_rsrc(x, (uint32_t)B * (uint32_t)d * 2u);
   const int w = wave_id_u(), lane = lane_id();
-  int k, rg;
-  for (int m = (int)(blockIdx.x / N_XCD); next_unit(hdr->die_gu, m, upp, k, rg); m += step) {
-    // the part and this wavefront's token rows (row l / 8 of each half of
+  for (int k = run.k0; k < run.k1; k += run.step) {
+    // the unit and this wavefront's token rows (row l / 8 of each half of
     // its tile), loaded together
     const uint32_t *tr = tokoff + (size_t)k * FFN_GU_TOK + 16 * w + (lane >> 3);
     const uint32_t tk0 = w < FFN_GU_PT ? tr[0] : FFN_TOK_PAD;
     const uint32_t tk1 = w < FFN_GU_PT ? tr[8] : FFN_TOK_PAD;
-    const PartU pt = load_part(parts + k);
+    const PartU pt = load_unit(units + k);
     if (pt.u < 0 || pt.u >= E + ns || pt.nt < 1 || pt.nt > FFN_GU_PT) continue;
     const uint16_t *w13 = pt.u < E ? w13r : w13s;
     PartU q = pt;
     q.u = pt.u < E ? pt.u : pt.u - E;   // experts E .. E + ns - 1: the shared ones
-    const int rp0 = rg * RP, nrp = min(RP, T - rp0);
+    const int rp0 = pt.rg * RP, nrp = min(RP, T - rp0);
+    if (nrp < 1) continue;
     wg_barrier();   // every wavefront is done with the previous unit's ring
     // entries past the part's pairs are not written: those lanes read zero
     const uint32_t seg = 16u * (uint32_t)((lane & 7) ^ (lane >> 3));
@@ -423,33 +418,31 @@ void k_gateup_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w13
 }
 static_assert(FFN_GU_PT == 6, "gate/up tile-count cases");
 
-// down: FFN_WAVES row tiles of 16 rows of d per unit; registers for two
-// workgroups per CU (four wavefronts per SIMD).
-template <bool PACKED>
-__global__ __launch_bounds__(FFN_WAVES * WAVE, FFN_DN_WPE)
+// down: FFN_WAVES row tiles of 16 rows of d per unit, DW k-steps of weights
+// in flight; registers for WPE wavefronts per SIMD (FFN_DN_WPE / FFN_DN_DW
+// for the usual short contractions, FFN_DN_WPE_LONG / FFN_DN_DW_LONG for
+// long ones, whose few units each stream many k-steps).
+template <bool PACKED, int DW, int WPE>
+__global__ __launch_bounds__(FFN_WAVES * WAVE, WPE)
 void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
                  const uint16_t *__restrict__ w2s, const FfnHdr *__restrict__ hdr,
-                 const FfnPart *__restrict__ parts, int pstride,
-                 const float *__restrict__ pair_gate, const uint16_t *__restrict__ hp,
-                 float *__restrict__ pairbuf) {
+                 const FfnUnit *__restrict__ units, const float *__restrict__ pair_gate,
+                 const uint16_t *__restrict__ hp, float *__restrict__ pairbuf) {
   __shared__ __attribute__((aligned(16))) uint8_t ring[(FFN_DN_DT + 1) * FFN_DN_PT * 1024];
   __shared__ __attribute__((aligned(16))) uint8_t dummy[FFN_WAVES * 1024];
-  const int die = (int)(blockIdx.x % N_XCD);   // this die's copy of the tables
-  hdr += die;
-  parts += (size_t)die * pstride;
-  const int T = d / 16;                    // row tiles per expert
-  const int upp = (T + FFN_WAVES - 1) / FFN_WAVES;
-  const int step = (int)(gridDim.x / N_XCD);
-  int k, rg;
-  for (int m = (int)(blockIdx.x / N_XCD); next_unit(hdr->die_dn, m, upp, k, rg); m += step) {
-    const PartU pt = load_part(parts + k);
+  hdr += blockIdx.x % N_XCD;   // this die's header and run
+  const int T = d / 16;          // row tiles per expert
+  const Run run = die_run(hdr->dn0, hdr->dn1);
+  for (int k = run.k0; k < run.k1; k += run.step) {
+    const PartU pt = load_unit(units + k);
     if (pt.u < 0 || pt.u >= E + ns || pt.nt < 1 || pt.nt > FFN_DN_PT) continue;
     const uint16_t *w2 = pt.u < E ? w2r : w2s;
     PartU q = pt;
     q.u = pt.u < E ? pt.u : pt.u - E;
-    const int rt0 = rg * FFN_WAVES, nrt = min(FFN_WAVES, T - rt0);
+    const int rt0 = pt.rg * FFN_WAVES, nrt = min(FFN_WAVES, T - rt0);
+    if (nrt < 1) continue;
     wg_barrier();
-#define BASE_DN(N) case N: down_unit<N, PACKED>(ring, dummy, d, I, w2, q, rt0, nrt, pair_gate, hp, pairbuf); break;
+#define BASE_DN(N) case N: down_unit<N, PACKED, DW>(ring, dummy, d, I, w2, q, rt0, nrt, pair_gate, hp, pairbuf); break;
     switch (q.nt) { BASE_DN(1) BASE_DN(2) BASE_DN(3) BASE_DN(4) BASE_DN(5) BASE_DN(6) BASE_DN(7) default: BASE_DN(8) }
 #undef BASE_DN
   }
@@ -568,13 +561,12 @@ hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
                          int I, int E, int K, int budget, int ns, const void *w13,
                          const void *w13s, const int32_t *sel_ids, const int32_t *n_sel,
                          const int32_t *offsets, const int32_t *pair_tok,
-                         const FfnHdr *hdr, const FfnPart *parts, int n_cu,
+                         const FfnHdr *hdr, const FfnUnit *units, int n_cu,
                          const uint32_t *tokoff, void *H, hipStream_t st) {
   if (bf16) {
     launch_k(packed ? k_gateup_bf16<true> : k_gateup_bf16<false>, dim3(ffn_gu_grid(n_cu)),
              dim3(FFN_WAVES * WAVE), 0, st, d, I, E, ns, (const uint16_t *)w13,
-             (const uint16_t *)w13s, hdr, parts, ffn_parts_bound(B, K, budget, ns, FFN_GU_PT),
-             (const uint16_t *)x, B, tokoff, (uint16_t *)H);
+             (const uint16_t *)w13s, hdr, units, (const uint16_t *)x, B, tokoff, (uint16_t *)H);
   } else {
     launch_k(k_gateup_f32, dim3(budget, (I + F32_WAVES - 1) / F32_WAVES),
                        dim3(F32_WAVES * WAVE), 0, st, (const float *)x, d, I,
@@ -588,13 +580,18 @@ hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K
                        int budget, int ns, const void *w2, const void *w2s,
                        const int32_t *sel_ids,
                        const int32_t *n_sel, const int32_t *offsets,
-                       const FfnHdr *hdr, const FfnPart *parts, int n_cu,
+                       const FfnHdr *hdr, const FfnUnit *units, int n_cu,
                        const float *pair_gate, const void *H, float *pairbuf, hipStream_t st) {
   if (bf16) {
-    launch_k(packed ? k_down_bf16<true> : k_down_bf16<false>, dim3(ffn_dn_grid(n_cu)),
-             dim3(FFN_WAVES * WAVE), 0, st, d, I, E, ns, (const uint16_t *)w2,
-             (const uint16_t *)w2s, hdr, parts, ffn_parts_bound(B, K, budget, ns, FFN_DN_PT),
-             pair_gate, (const uint16_t *)H, pairbuf);
+    const bool lng = ffn_dn_long(I);
+    const auto kern =
+        lng ? (packed ? k_down_bf16<true, FFN_DN_DW_LONG, FFN_DN_WPE_LONG>
+                      : k_down_bf16<false, FFN_DN_DW_LONG, FFN_DN_WPE_LONG>)
+            : (packed ? k_down_bf16<true, FFN_DN_DW, FFN_DN_WPE>
+                      : k_down_bf16<false, FFN_DN_DW, FFN_DN_WPE>);
+    launch_k(kern, dim3(ffn_dn_grid(n_cu, I)), dim3(FFN_WAVES * WAVE), 0, st, d, I, E, ns,
+             (const uint16_t *)w2,
+             (const uint16_t *)w2s, hdr, units, pair_gate, (const uint16_t *)H, pairbuf);
   } else {
     launch_k(k_down_f32, dim3(budget, (d + F32_WAVES - 1) / F32_WAVES),
                        dim3(F32_WAVES * WAVE), 0, st, d, I, E,

@@ -66,8 +66,8 @@ inline int ffn_max_tiles(int B, int K, int budget, int ns) {
 // shared slot; a unit of work is (part, row group), one per workgroup of
 // FFN_WAVES wavefronts at a time, each wavefront owning 16-row tiles over the
 // whole contraction with weights requested FFN_GU_DW (gate/up) or FFN_DN_DW
-// (down) k-steps ahead and token fragments FFN_GU_DT or FFN_DN_DT k-steps
-// ahead.
+// (down) k-steps ahead and token fragments FFN_GU_DT steps (two k-steps each)
+// or FFN_DN_DT k-steps ahead.
 constexpr int FFN_WAVES = 8;
 constexpr int FFN_GU_DW = 8;
 constexpr int FFN_GU_DT = 2;
@@ -76,44 +76,59 @@ constexpr int FFN_DN_DT = 2;
 // wavefronts per SIMD the down kernel's registers allow: three workgroups
 // per CU, so that a die's down units mostly run in one round
 constexpr int FFN_DN_WPE = 6;
+// down with a long contraction (more than FFN_DN_LONG_KS k-steps of I): few
+// units that each stream many k-steps, so more weights in flight per
+// wavefront and one workgroup per CU
+constexpr int FFN_DN_LONG_KS = 64;
+constexpr int FFN_DN_DW_LONG = 8;
+constexpr int FFN_DN_WPE_LONG = 2;
+__host__ __device__ inline bool ffn_dn_long(int I) { return I / 32 > FFN_DN_LONG_KS; }
 constexpr int FFN_GU_PT = 6;
 constexpr int FFN_DN_PT = 8;
-// gate/up reads its token rows straight from the hidden states: row i of
-// part k of the gate/up table is the byte offset of its token's row,
-// tokoff[k * FFN_GU_TOK + i] = t * d * 2 (FFN_TOK_PAD past the part's pairs:
-// a buffer load there returns zero)
+// gate/up reads its token rows straight from the hidden states: entry i of
+// gate/up unit k's row is the byte offset of the row of its part's pair i,
+// tokoff[k * FFN_GU_TOK + i] = t * d * 2 (written for the part's pairs only)
 constexpr int FFN_GU_TOK = FFN_GU_PT * 16;
-constexpr uint32_t FFN_TOK_PAD = 0x80000000u;
+constexpr uint32_t FFN_TOK_PAD = 0x80000000u;   // past every x: a buffer load returns zero
 static_assert(FFN_GU_PT <= FFN_WAVES, "one token tile per gate/up wavefront");
 static_assert((size_t)MAX_B * 16384 * 2 < FFN_TOK_PAD, "token row offsets below the pad mark");
 
-// A part of a slot's pairs: expert u (u >= E: shared expert u - E), its
-// first 16-pair tile in the token operand, its tile count, its first pair
-// in the compacted order and its pair count.
-struct alignas(32) FfnPart {
-  int32_t u, tile0, nt, p0, n, pad0, pad1, pad2;
+// A unit: expert u (u >= E: shared expert u - E), the part's first 16-pair
+// tile, its tile count, its first pair in the compacted order and its pair
+// count, and the unit's row group (gate/up: hdr.rp_gu row-pair tiles;
+// down: FFN_WAVES row tiles).
+struct alignas(32) FfnUnit {
+  int32_t u, tile0, nt, p0, n, rg, pad0, pad1;
 };
-// The part tables' layout and gate/up's row group (row-pair tiles per
-// unit), written by the compaction launch: the parts of die x are rows
-// die_gu[x] .. die_gu[x + 1] - 1 of the gate/up table (die_dn: the down
-// table).
-struct alignas(16) FfnHdr {
-  int32_t rp_gu, pad0;
-  int32_t die_gu[N_XCD + 1], die_dn[N_XCD + 1];
+// Die x's header, written by the compaction workgroup that ran on die x:
+// gate/up's row group and die x's runs of units, [gu0, gu1) of the gate/up
+// table and [dn0, dn1) of the down table.
+struct alignas(32) FfnHdr {
+  int32_t rp_gu, gu0, gu1, dn0, dn1, pad0, pad1, pad2;
 };
-
 
 // Upper bound of the parts of a launch with at most pt tiles per part: the
 // sum over slots of ceil(tiles / pt) is below tiles / pt + slots.
 inline int ffn_parts_bound(int B, int K, int budget, int ns, int pt) {
   return ffn_max_tiles(B, K, budget, ns) / pt + budget + ns + 1;
 }
+// Upper bounds of the units: every part times its row groups (gate/up: at
+// least FFN_WAVES / 2 row-pair tiles per group; down: FFN_WAVES row tiles).
+inline int ffn_units_bound_gu(int B, int K, int budget, int ns, int I) {
+  return ffn_parts_bound(B, K, budget, ns, FFN_GU_PT) * ((I / 16 + FFN_WAVES / 2 - 1) / (FFN_WAVES / 2));
+}
+inline int ffn_units_bound_dn(int B, int K, int budget, int ns, int d) {
+  return ffn_parts_bound(B, K, budget, ns, FFN_DN_PT) * ((d / 16 + FFN_WAVES - 1) / FFN_WAVES);
+}
 // Workgroups of the FFN launches: a multiple of N_XCD, from the device's
 // compute units -- gate/up one per CU (its registers allow no second), down
-// three per CU (FFN_DN_WPE).
+// FFN_DN_WPE / 2 (or FFN_DN_WPE_LONG / 2) per CU: a workgroup of FFN_WAVES
+// wavefronts puts two on each SIMD.
 __host__ __device__ inline unsigned ffn_cu_grid(int n_cu) { return (unsigned)(((n_cu + N_XCD - 1) / N_XCD) * N_XCD); }
 __host__ __device__ inline unsigned ffn_gu_grid(int n_cu) { return ffn_cu_grid(n_cu); }
-__host__ __device__ inline unsigned ffn_dn_grid(int n_cu) { return 3u * ffn_cu_grid(n_cu); }
+__host__ __device__ inline unsigned ffn_dn_grid(int n_cu, int I) {
+  return (unsigned)((ffn_dn_long(I) ? FFN_DN_WPE_LONG : FFN_DN_WPE) / 2) * ffn_cu_grid(n_cu);
+}
 
 // rows: n_router of Wr (logits, + beta), then the vector G when given (gdot)
 hipError_t launch_scores(bool bf16, const void *x, int B, int d, const float *Wr,
@@ -147,17 +162,18 @@ hipError_t launch_backfill(int B, int E, int K, int norm_topk, int flags,
                            hipStream_t st);
 // ns shared slots follow the kept ones (expert E + i, every token, gate
 // sigmoid(gdot[t]) or 1 when gdot is null).  With `tables` (bf16 layers)
-// the same launch also writes the FFN's part tables (parts_gu, parts_dn,
-// each of at most ffn_parts_bound rows), their header and gate/up's token
-// row offsets (tokoff, FFN_GU_TOK per gate/up part; d: the hidden size);
-// n_cu: the device's compute units (the FFN launches' sizes follow from it).
+// the same launch also writes the FFN's unit tables (units_gu, units_dn, of
+// at most ffn_units_bound_gu / _dn rows), the per-die headers and gate/up's
+// token row offsets (tokoff, FFN_GU_TOK per gate/up unit; d: the hidden
+// size); n_cu: the device's compute units (the FFN launches' sizes follow
+// from it).
 hipError_t launch_compact(int B, int K, int E, int budget, int ns, const int32_t *exec_ids,
                           const float *exec_gates, const int32_t *slot_of,
                           const int32_t *n_sel, const float *gdot, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
                           int32_t *pair_of, const int32_t *sel_ids, bool tables, int d,
-                          int I, uint32_t *tokoff, FfnHdr *hdr, FfnPart *parts_gu,
-                          FfnPart *parts_dn, int n_cu, hipStream_t st);
+                          int I, uint32_t *tokoff, FfnHdr *hdr, FfnUnit *units_gu,
+                          FfnUnit *units_dn, int n_cu, hipStream_t st);
 hipError_t launch_pack(const void *w13, const void *w2, void *w13p, void *w2p,
                        int E, int d, int I, hipStream_t st);
 // parts of expert u >= E read the shared experts' weights (w13s / w2s, u - E)
@@ -166,13 +182,13 @@ hipError_t launch_gateup(bool bf16, bool packed, const void *x, int B, int d,
                          const void *w13s,
                          const int32_t *sel_ids, const int32_t *n_sel,
                          const int32_t *offsets, const int32_t *pair_tok,
-                         const FfnHdr *hdr, const FfnPart *parts, int n_cu,
+                         const FfnHdr *hdr, const FfnUnit *units, int n_cu,
                          const uint32_t *tokoff, void *H, hipStream_t st);
 hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K,
                        int budget, int ns, const void *w2, const void *w2s,
                        const int32_t *sel_ids,
                        const int32_t *n_sel, const int32_t *offsets,
-                       const FfnHdr *hdr, const FfnPart *parts, int n_cu,
+                       const FfnHdr *hdr, const FfnUnit *units, int n_cu,
                        const float *pair_gate, const void *H, float *pairbuf, hipStream_t st);
 // kc: columns of pair_of (K routed + the shared experts)
 hipError_t launch_combine(bool bf16, int B, int d, int kc,

@@ -460,6 +460,33 @@ __device__ __forceinline__ void wave_scan2(const int *cnt, int n, int *off, int 
   if (lane == WAVE - 1) { off[SCAN_N] = i0; tb[SCAN_N] = i1; }
 }
 
+// hr[s] = slots below s with more than pt 16-pair tiles (s <= SCAN_N;
+// hr[SCAN_N]: all of them), from the slots' pair counts, by one wavefront.
+__device__ __forceinline__ void wave_scan_multi(const int *cnt, int nslot, int pt, int *hr) {
+  const int lane = lane_id();
+  constexpr int Q = SCAN_Q;
+  int l[Q], s = 0;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int i = lane * Q + q;
+    l[q] = (i < nslot && cnt[i] > 16 * pt) ? 1 : 0;
+    s += l[q];
+  }
+  int inc = s;
+#pragma unroll
+  for (int h = 1; h < WAVE; h <<= 1) {
+    const int o = __shfl_up(inc, h, WAVE);
+    if (lane >= h) inc += o;
+  }
+  int r = inc - s;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    hr[lane * Q + q] = r;
+    r += l[q];
+  }
+  if (lane == WAVE - 1) hr[SCAN_N] = inc;
+}
+
 // A slot of nt tiles cut into np = ceil(nt / pt) parts of balanced size:
 // the first ex = nt % np parts have lo + 1 tiles, the others lo = nt / np.
 struct PartSplit {
@@ -501,42 +528,6 @@ __device__ __forceinline__ void wave_scan_counts(const int *cnt, int *pre) {
   if (lane == WAVE - 1) pre[SCAN_N] = inc;
 }
 
-// hr[s] = slots below s with more than one part, i.e. more than pt 16-pair
-// tiles (s <= SCAN_N; hr[SCAN_N]: all of them), from the slots' pair counts,
-// by one wavefront.
-__device__ __forceinline__ void wave_scan_multi(const int *cnt, int nslot, int pt, int *hr) {
-  const int lane = lane_id();
-  constexpr int Q = SCAN_Q;
-  int l[Q], s = 0;
-#pragma unroll
-  for (int q = 0; q < Q; ++q) {
-    const int i = lane * Q + q;
-    l[q] = (i < nslot && cnt[i] > 16 * pt) ? 1 : 0;
-    s += l[q];
-  }
-  int inc = s;
-#pragma unroll
-  for (int h = 1; h < WAVE; h <<= 1) {
-    const int o = __shfl_up(inc, h, WAVE);
-    if (lane >= h) inc += o;
-  }
-  int r = inc - s;
-#pragma unroll
-  for (int q = 0; q < Q; ++q) {
-    hr[lane * Q + q] = r;
-    r += l[q];
-  }
-  if (lane == WAVE - 1) hr[SCAN_N] = inc;
-}
-
-// Die-major scan position of slot s: its deal position r (multi-part slots
-// first, see k_compact) goes to die r % N_XCD, as that die's slot r / N_XCD.
-__device__ __forceinline__ int slot_j(int s, const int *hr, int spd) {
-  const bool multi = hr[s + 1] > hr[s];
-  const int r = multi ? hr[s] : hr[SCAN_N] + (s - hr[s]);
-  return (r % N_XCD) * spd + r / N_XCD;
-}
-
 constexpr int CP_THREADS = 1024;
 constexpr int CP_WAVES = CP_THREADS / WAVE;
 constexpr int CP_STAGE = 4096;   // pair gates staged in LDS per pass
@@ -545,9 +536,9 @@ constexpr int CP_PAIRS = MAX_B * MAX_K;   // routed pairs at most
 // A stable counting sort of the executed pairs by kept slot and (bf16
 // layers) the FFN's part tables.  With tables there is one workgroup per
 // die, each making the whole sort (the same arithmetic, so the same result
-// everywhere) and writing its die's copy of the tables, which the FFN's
-// workgroups on that die read from their own L2; workgroup 0 alone writes
-// the plan.  Without tables, one workgroup.
+// everywhere) and writing its die's header, units and token rows, which the
+// FFN's workgroups on that die then read from their own L2; workgroup 0
+// alone writes the plan.  Without tables, one workgroup.
 // The routed pairs are taken in flat order q = t K + j, so sorting by (slot,
 // q) is sorting by (slot, token, rank).  Wavefront w owns the pairs w 64 PPT
 // + r 64 + lane (r = 0 .. PPT - 1, PPT pairs per thread, PPT * CP_THREADS >=
@@ -566,24 +557,32 @@ constexpr int CP_PAIRS = MAX_B * MAX_K;   // routed pairs at most
 // multiply-high by kmul = ceil(2^32 / K), exact for q < 2^32 / K, far above
 // B K), and every global load is issued before the first wait.
 //
-// The FFN's part tables (see "Grouped bf16 FFN" in ffn.hip), gate/up's and
+// The FFN's unit tables (see "Grouped bf16 FFN" in ffn.hip), gate/up's and
 // down's.  Slot s (kept slots, then shared ones) has nt = tb[s + 1] - tb[s]
-// tiles, cut into parts of balanced size (part_split).  Every part of a
-// slot goes to one die in both tables (one L2 serves the expert's weights,
-// and down finds the activations gate/up wrote there), and the dies get
-// equal shares as far as whole slots allow: the slots with more than one
-// gate/up part are dealt round-robin first, then the others, i.e. slot s
-// takes deal position r = (its rank among the multi-part slots) or
-// H + (its rank among the others) (H multi-part slots) on die r % N_XCD.
-// A table lists the parts die by die, each die's in deal order (so the
-// multi-part slots, the heaviest, start first): a scan of the slots' part
-// counts in die-major order (j = x spd + r / N_XCD, spd slots per die at
-// most) gives every slot's first row and every die's first row.  Gate/up's
-// token rows: entry i of part row k is the byte offset in x of the row of
-// the part's pair i (tokoff[k * FFN_GU_TOK + i], written for its pairs
-// only; gate/up reads no entry at or past the part's pair count).
-// Die x's copy: hdr[x], rows x pstride_gu .. of parts_gu and tokoff (times
-// FFN_GU_TOK), rows x pstride_dn .. of parts_dn.
+// tiles, cut into parts of balanced size (part_split); a unit is (part, row
+// group).  The units are numbered slot by slot, and within a slot row group
+// by row group (all of the slot's parts for one row group together, so that
+// they read those weight rows through one L2), and the numbering is cut
+// into N_XCD runs, die x taking run x.  With at least four slots per die
+// the slots are dealt to the dies whole, round-robin, the slots with more
+// than one gate/up part first, and numbered die by die, a slot's units part
+// by part (a part's row groups together): every slot's units then fall on
+// one die in both tables (down finds gate/up's activations in that die's
+// L2) and the dies get equal shares as far as whole slots allow.  With
+// fewer slots they are numbered in slot order, a slot's units row group by
+// row group (all its parts for one row group together), and each table is
+// cut into runs of equal numbers of units at row-group boundaries (down at
+// the same fraction of the same slot's row groups): a slot's row groups then
+// spread over several dies, so that every die has its share of the work.
+// A unit's time is mostly its weight stream, so units are what is shared
+// out.  Workgroup x
+// of the launch writes die x's header, die x's units and gate/up's token
+// rows of those units (entry i of unit k's row: the byte offset in x of the
+// row of the part's pair i, tokoff[k * FFN_GU_TOK + i], for the part's
+// pairs only; gate/up reads no entry at or past the part's pair count).
+// Gate/up's row group (row-pair tiles per unit, FFN_WAVES down to
+// FFN_WAVES / 2) is the one that gives the fewest row-pair tiles to the
+// busiest workgroup when every die's units are shared by its workgroups.
 template <int PPT>
 __global__ __launch_bounds__(CP_THREADS)
 void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
@@ -594,8 +593,7 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
                float *__restrict__ pair_gate, int32_t *__restrict__ pair_of,
                const int32_t *__restrict__ sel_ids, int tables, int d, int I,
                uint32_t *__restrict__ tokoff, FfnHdr *__restrict__ hdr,
-               FfnPart *__restrict__ parts_gu, FfnPart *__restrict__ parts_dn,
-               int pstride_gu, int pstride_dn, int n_cu) {
+               FfnUnit *__restrict__ units_gu, FfnUnit *__restrict__ units_dn, int n_cu) {
   // cw[w][s]: pairs of slot s in wavefront w, then their first rank in slot s
   __shared__ int cw[CP_WAVES][MAX_E];
   __shared__ int cnt[SCAN_N];
@@ -605,11 +603,14 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
   __shared__ int slot_s[MAX_E];
   __shared__ int stage_t[CP_PAIRS];     // token of every routed position
   __shared__ float stage_g[CP_STAGE];   // gates, CP_STAGE positions per pass
-  __shared__ int np_gu[SCAN_N], np_dn[SCAN_N];          // the part tables' layout
+  // the tables' order: slot s at position pos_s[s] (slot_at: the inverse);
+  // parts per position and their prefixes
+  __shared__ int pos_s[SCAN_N], slot_at[SCAN_N];
+  __shared__ int np_gu[SCAN_N], np_dn[SCAN_N];
   __shared__ int pre_gu[SCAN_N + 1], pre_dn[SCAN_N + 1];
   __shared__ int hr[SCAN_N + 1];
-  __shared__ int sj_s[SCAN_N];           // slot -> its die-major scan position j
   __shared__ uint32_t sp_s[SCAN_N];      // slot -> its gate/up part split, packed
+  __shared__ int cut_s[3][N_XCD + 1];    // die y's first gate/up unit, down unit, slot
   __shared__ uint32_t rc_s[2][SCAN_N];   // slot -> ceil(2^16 / (lo + 1)), ceil(2^16 / lo)
   const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
   const bool out = blockIdx.x == 0;     // the workgroup that writes the plan
@@ -676,23 +677,33 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
   if (tid >= n_sel && tid < n_sel + ns) cnt[tid] = B;
   __syncthreads();
   const int nslot = n_sel + ns;
-  const int spd = (nslot + N_XCD - 1) / N_XCD;
-  // the slots' prefixes, and the tables' layout (die-major part counts)
+  const bool whole = nslot >= 4 * N_XCD;   // slots dealt to the dies whole
   if (wv == 0) wave_scan2(cnt, nslot, off, tb);
   if (tables) {
-    if (wv == 1) wave_scan_multi(cnt, nslot, FFN_GU_PT, hr);
+    if (wv == 1 && whole) wave_scan_multi(cnt, nslot, FFN_GU_PT, hr);
     for (int j = tid - 2 * WAVE; j >= 0 && j < SCAN_N; j += CP_THREADS - 2 * WAVE)
       np_gu[j] = np_dn[j] = 0;
   }
   __syncthreads();
   if (tables) {
+    // each slot's position, parts and gate/up split (packed for put_tok)
     for (int s = tid; s < nslot; s += CP_THREADS) {
-      const int nt = tb[s + 1] - tb[s], j = slot_j(s, hr, spd);
+      int j = s;
+      if (whole) {
+        // deal position r (multi-part slots first) to die r % N_XCD, as its
+        // slot r / N_XCD; die y holds ceil((nslot - y) / N_XCD) slots
+        const bool multi = hr[s + 1] > hr[s];
+        const int r = multi ? hr[s] : hr[SCAN_N] + (s - hr[s]), y = r % N_XCD;
+        j = r / N_XCD;
+        for (int z = 0; z < y; ++z) j += (nslot - z + N_XCD - 1) / N_XCD;
+      }
+      const int nt = tb[s + 1] - tb[s];
       const PartSplit sg = part_split(nt, FFN_GU_PT);
+      pos_s[s] = j;
+      slot_at[j] = s;
       np_gu[j] = sg.np;
       np_dn[j] = part_split(nt, FFN_DN_PT).np;
-      sj_s[s] = j;
-      // lo (<= FFN_GU_PT) and ex (< np <= MAX_B / 16) for put_tok
+      // lo (<= FFN_GU_PT) and ex (< np <= MAX_B / 16)
       sp_s[s] = (uint32_t)sg.lo | ((uint32_t)sg.ex << 8);
       rc_s[0][s] = (65536u + (uint32_t)sg.lo) / (uint32_t)(sg.lo + 1);
       rc_s[1][s] = (65536u + (uint32_t)sg.lo - 1u) / (uint32_t)max(sg.lo, 1);
@@ -701,22 +712,6 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
   const int routed = off[n_sel];   // pairs of the kept slots
   if (out && tid <= budget) offsets[tid] = (tid < n_sel) ? off[tid] : routed;
   if (out && tid < ns) offsets[budget + 1 + tid] = off[n_sel + tid + 1];
-  uint32_t *tko = tokoff + (size_t)blockIdx.x * pstride_gu * FFN_GU_TOK;
-  // gate/up's token row of pair pr of slot s (token t): its part row and
-  // entry.  The part of tile ti: the first ex parts have lo + 1 tiles, the
-  // others lo; the quotients as multiply-highs by ceil(2^16 / divisor),
-  // exact for ti < 2^16 / FFN_GU_PT (a slot has at most MAX_B / 16 tiles).
-  auto put_tok = [&](int s, int pr, int t) {
-    const uint32_t pk = sp_s[s];
-    const int lo = (int)(pk & 0xFFu), ex = (int)(pk >> 8);
-    const int ti = pr >> 4, big = ex * (lo + 1);
-    const uint32_t a = (uint32_t)(ti < big ? ti : ti - big);
-    const int qq = (int)((a * rc_s[ti < big ? 0 : 1][s]) >> 16);
-    const int q = ti < big ? qq : ex + qq;
-    const int tf = q * lo + min(q, ex);
-    const int row = pre_gu[sj_s[s]] + q;
-    tko[(size_t)row * FFN_GU_TOK + (pr - 16 * tf)] = (uint32_t)t * (uint32_t)d * 2u;
-  };
   // positions, pair_of, every routed position's token and the first pass
   // of gates
 #pragma unroll
@@ -732,73 +727,134 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
     if (out && q < nq) pair_of[(size_t)t * kc + (q - t * K)] = p_r[r];
   }
   if (tables) {
-    __syncthreads();   // np complete
+    __syncthreads();   // the positions' part counts complete
     if (wv < 2) wave_scan_counts(wv == 0 ? np_gu : np_dn, wv == 0 ? pre_gu : pre_dn);
     __syncthreads();
-    if (wv == 0) {
-      // the header: every die's first rows, and gate/up's row group: the
-      // row-pair tiles per unit (FFN_WAVES down to FFN_WAVES / 2) that gives
-      // the fewest row-pair tiles to the busiest workgroup when every die's
-      // units are shared by its workgroups
-      int dg = 0, dd = 0;
-      if (lane <= N_XCD) {
-        const int j = min(lane * spd, SCAN_N);
-        dg = pre_gu[j];
-        dd = pre_dn[j];
-      }
-      const int dprev = __shfl(dg, max(lane - 1, 0), WAVE);
-      int pd = (lane >= 1 && lane <= N_XCD) ? dg - dprev : 0;
-#pragma unroll
-      for (int h = 1; h < 16; h <<= 1) pd = max(pd, __shfl_xor(pd, h, WAVE));
-      const int T = I / 16;
-      const float per_die = (float)(ffn_gu_grid(n_cu) / N_XCD);
-      int best = FFN_WAVES, best_cost = 0x7FFFFFFF;
-#pragma unroll
-      for (int rp = FFN_WAVES; rp >= FFN_WAVES / 2; --rp) {
-        const int units = pd * ((T + rp - 1) / rp);
-        // rounds = ceil(units / per_die); exact in fp32 for these small integers
-        const int cost = (int)ceilf((float)units / per_die) * rp;
-        if (cost < best_cost) { best = rp; best_cost = cost; }
-      }
-      FfnHdr *hx = hdr + blockIdx.x;
-      if (lane <= N_XCD) {
-        hx->die_gu[lane] = dg;
-        hx->die_dn[lane] = dd;
-      }
-      if (lane == 0) {
-        hx->rp_gu = best;
-        hx->pad0 = 0;
+    // every thread derives the same row group and runs
+    const int x = blockIdx.x;
+    const int T = I / 16, Pg = pre_gu[SCAN_N], Pd = pre_dn[SCAN_N];
+    const float per_die = (float)(ffn_gu_grid(n_cu) / N_XCD);
+    // parts on the busiest die: dealt slots, or an even share
+    int pmax = (Pg + N_XCD - 1) / N_XCD;
+    if (whole) {
+      pmax = 0;
+      for (int y = 0, j = 0; y < N_XCD; ++y) {
+        const int jn = j + (nslot - y + N_XCD - 1) / N_XCD;
+        pmax = max(pmax, pre_gu[jn] - pre_gu[j]);
+        j = jn;
       }
     }
-#pragma unroll
-    for (int r = 0; r < PPT; ++r)
-      if (s_r[r] >= 0) put_tok(s_r[r], p_r[r] - off[s_r[r]], (int)(((uint64_t)(uint32_t)(q0 + r * WAVE) * kmul) >> 32));
-    if (tid < B)
-      for (int i = 0; i < ns; ++i) put_tok(n_sel + i, tid, tid);
-    // the part records of this die's copy, one thread per slot
-    FfnPart *pg = parts_gu + (size_t)blockIdx.x * pstride_gu;
-    FfnPart *pdn = parts_dn + (size_t)blockIdx.x * pstride_dn;
-    for (int s = tid; s < nslot; s += CP_THREADS) {
-      const int u = s < n_sel ? sel_s[s] : E + (s - n_sel);
-      const int j = slot_j(s, hr, spd), nt = tb[s + 1] - tb[s];
-#pragma unroll
-      for (int tbl = 0; tbl < 2; ++tbl) {
-        const PartSplit sp = part_split(nt, tbl == 0 ? FFN_GU_PT : FFN_DN_PT);
-        FfnPart *dst = (tbl == 0 ? pg : pdn) + (tbl == 0 ? pre_gu[j] : pre_dn[j]);
-        for (int q = 0; q < sp.np; ++q) {
-          const int c = q < sp.ex ? sp.lo + 1 : sp.lo;
-          const int tf = q * sp.lo + min(q, sp.ex);   // the part's first tile in its slot
-          FfnPart rec;
-          rec.u = u;
-          rec.tile0 = tb[s] + tf;
-          rec.nt = c;
-          rec.p0 = off[s] + 16 * tf;
-          rec.n = min(16 * c, cnt[s] - 16 * tf);
-          rec.pad0 = rec.pad1 = rec.pad2 = 0;
-          dst[q] = rec;
+    int rp = FFN_WAVES, best_cost = 0x7FFFFFFF;
+    for (int c = FFN_WAVES; c >= FFN_WAVES / 2; --c) {
+      const int units = pmax * ((T + c - 1) / c);
+      // rounds = ceil(units / per_die); exact in fp32 for these small integers
+      const int cost = (int)ceilf((float)units / per_die) * c;
+      if (cost < best_cost) { rp = c; best_cost = cost; }
+    }
+    const int ug = (T + rp - 1) / rp, ud = (d / 16 + FFN_WAVES - 1) / FFN_WAVES;
+    // die y's first unit in both tables and first position.  Whole slots:
+    // the first position of die y.  Otherwise, from the target gate/up unit
+    // Pg ug y / N_XCD at position j: the start of its row group r of ug, and
+    // in down of row group r ud / ug at j (one pass: the thread of the
+    // position holding a target writes its cut).
+    int g0, g1, d0, d1, s0, s1;   // this die's runs; their positions lie in [s0, s1]
+    if (whole) {
+      // every thread finds its own die's first positions
+      int j0 = 0;
+      for (int z = 0; z < x; ++z) j0 += (nslot - z + N_XCD - 1) / N_XCD;
+      const int j1 = j0 + (nslot - x + N_XCD - 1) / N_XCD;
+      g0 = pre_gu[j0] * ug; g1 = pre_gu[j1] * ug;
+      d0 = pre_dn[j0] * ud; d1 = pre_dn[j1] * ud;
+      s0 = min(j0, nslot - 1); s1 = min(j1, nslot - 1);
+    } else {
+      for (int j = tid; j < nslot; j += CP_THREADS) {
+        const int a = pre_gu[j] * ug, b = pre_gu[j + 1] * ug;
+        for (int y = 1; y < N_XCD; ++y) {
+          const int i = Pg * ug * y / N_XCD;
+          if (i >= a && i < b) {
+            const int r = (i - a) / np_gu[j];
+            cut_s[0][y] = a + r * np_gu[j];
+            cut_s[1][y] = pre_dn[j] * ud + (r * ud / ug) * np_dn[j];
+            cut_s[2][y] = j;
+          }
         }
       }
+      if (tid == 0) {
+        for (int y = 0; y < N_XCD && Pg == 0; ++y)   // no units: no position holds a cut
+          cut_s[0][y] = cut_s[1][y] = cut_s[2][y] = 0;
+        cut_s[0][0] = cut_s[1][0] = cut_s[2][0] = 0;
+        cut_s[0][N_XCD] = Pg * ug;
+        cut_s[1][N_XCD] = Pd * ud;
+        cut_s[2][N_XCD] = max(nslot - 1, 0);
+      }
+      __syncthreads();
+      g0 = cut_s[0][x]; g1 = cut_s[0][x + 1];
+      d0 = cut_s[1][x]; d1 = cut_s[1][x + 1];
+      s0 = cut_s[2][x]; s1 = cut_s[2][x + 1];
     }
+    if (tid == 0) {
+      FfnHdr h;
+      h.rp_gu = rp;
+      h.gu0 = g0; h.gu1 = g1; h.dn0 = d0; h.dn1 = d1;
+      h.pad0 = h.pad1 = h.pad2 = 0;
+      hdr[x] = h;
+    }
+    // unit i: its position (the first j with pre[j + 1] * upp > i) and
+    // slot, then row group and part
+    auto put_unit = [&](int i, int upp, const int *pre, const int *np, int pt, FfnUnit *dst) {
+      int lo = s0, hi = s1;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (pre[mid + 1] * upp > i) hi = mid; else lo = mid + 1;
+      }
+      const int j = lo, s = slot_at[j], r = i - pre[j] * upp;
+      const int rg = whole ? r % upp : r / np[j], q = whole ? r / upp : r % np[j];
+      const PartSplit sp = part_split(tb[s + 1] - tb[s], pt);
+      const int c = q < sp.ex ? sp.lo + 1 : sp.lo;
+      const int tf = q * sp.lo + min(q, sp.ex);   // the part's first tile in its slot
+      FfnUnit rec;
+      rec.u = s < n_sel ? sel_s[s] : E + (s - n_sel);
+      rec.tile0 = tb[s] + tf;
+      rec.nt = c;
+      rec.p0 = off[s] + 16 * tf;
+      rec.n = min(16 * c, cnt[s] - 16 * tf);
+      rec.rg = rg;
+      rec.pad0 = rec.pad1 = 0;
+      dst[i] = rec;
+    };
+    for (int i = g0 + tid; i < g1; i += CP_THREADS) put_unit(i, ug, pre_gu, np_gu, FFN_GU_PT, units_gu);
+    for (int i = d0 + tid; i < d1; i += CP_THREADS) put_unit(i, ud, pre_dn, np_dn, FFN_DN_PT, units_dn);
+    // gate/up's token row of pair pr of slot s (token t), in every unit of
+    // its part in [g0, g1).  The
+    // part of tile ti: the first ex parts have lo + 1 tiles, the others lo;
+    // the quotients as multiply-highs by ceil(2^16 / divisor), exact for
+    // ti < 2^16 / (FFN_GU_PT + 1) (a slot has at most MAX_B / 16 tiles).
+    auto put_tok = [&](int s, int pr, int t) {
+      const int j = pos_s[s];
+      if (pre_gu[j + 1] * ug <= g0 || pre_gu[j] * ug >= g1) return;   // not on this die
+      const uint32_t pk = sp_s[s];
+      const int lo = (int)(pk & 0xFFu), ex = (int)(pk >> 8);
+      const int ti = pr >> 4, big = ex * (lo + 1);
+      const uint32_t a = (uint32_t)(ti < big ? ti : ti - big);
+      const int qq = (int)((a * rc_s[ti < big ? 0 : 1][s]) >> 16);
+      const int q = ti < big ? qq : ex + qq;
+      const int tf = q * lo + min(q, ex);
+      // the part's units, base + rg n (n = 1 when numbered part by part),
+      // in [g0, g1)
+      const int n = whole ? 1 : np_gu[j];
+      const int base = pre_gu[j] * ug + (whole ? q * ug : q);
+      const int rg0 = g0 > base ? (g0 - base + n - 1) / n : 0;
+      const int rg1 = min(ug, g1 > base ? (g1 - base + n - 1) / n : 0);
+      const uint32_t v = (uint32_t)t * (uint32_t)d * 2u;
+      for (int rg = rg0; rg < rg1; ++rg)
+        tokoff[(size_t)(base + rg * n) * FFN_GU_TOK + (pr - 16 * tf)] = v;
+    };
+#pragma unroll
+    for (int r = 0; r < PPT; ++r)
+      if (s_r[r] >= 0)
+        put_tok(s_r[r], p_r[r] - off[s_r[r]], (int)(((uint64_t)(uint32_t)(q0 + r * WAVE) * kmul) >> 32));
+    if (tid < B)
+      for (int i = 0; i < ns; ++i) put_tok(n_sel + i, tid, tid);
   }
   if (!out) return;
   __syncthreads();
@@ -864,18 +920,15 @@ hipError_t launch_compact(int B, int K, int E, int budget, int ns, const int32_t
                           const int32_t *n_sel, const float *gdot, int32_t *offsets,
                           int32_t *pair_tok, float *pair_gate,
                           int32_t *pair_of, const int32_t *sel_ids, bool tables, int d,
-                          int I, uint32_t *tokoff, FfnHdr *hdr, FfnPart *parts_gu,
-                          FfnPart *parts_dn, int n_cu, hipStream_t st) {
+                          int I, uint32_t *tokoff, FfnHdr *hdr, FfnUnit *units_gu,
+                          FfnUnit *units_dn, int n_cu, hipStream_t st) {
   const int ppt = (B * K + CP_THREADS - 1) / CP_THREADS;
   const uint64_t kmul = ((1ull << 32) + (uint64_t)K - 1) / (uint64_t)K;
-  const int sg = ffn_parts_bound(B, K, budget, ns, FFN_GU_PT);
-  const int sd = ffn_parts_bound(B, K, budget, ns, FFN_DN_PT);
-  const unsigned blocks = tables ? N_XCD : 1u;   // one copy of the tables per die
+  const unsigned blocks = tables ? N_XCD : 1u;   // one workgroup per die
 #define BASE_COMPACT(P)                                                                    \
   launch_k(k_compact<P>, dim3(blocks), dim3(CP_THREADS), 0, st, B, K, kmul, E, budget, ns, \
            exec_ids, exec_gates, slot_of, n_sel, gdot, offsets, pair_tok, pair_gate,      \
-           pair_of, sel_ids, (int)tables, d, I, tokoff, hdr, parts_gu, parts_dn, sg, sd,  \
-           n_cu)
+           pair_of, sel_ids, (int)tables, d, I, tokoff, hdr, units_gu, units_dn, n_cu)
   if (ppt <= 1) BASE_COMPACT(1);
   else if (ppt <= 2) BASE_COMPACT(2);
   else if (ppt <= 4) BASE_COMPACT(4);
