@@ -324,7 +324,12 @@ base_status base_pack_experts(const base_layer *L, void *w13_packed,
  * z_bar = z_t / ||z_t|| (fp64); per expert u the statistics add
  *   n_u, sum y, sum y^2                (fp64),
  *   sum z_bar [d], sum z_bar y [d]     (fp64),
- *   G_u = sum z_bar z_bar^T [d][d]     (fp32 products and sums per batch).
+ *   G_u = sum z_bar z_bar^T [d][d]     (fp32 products and sums per batch,
+ *                                       on the matrix cores, then one add).
+ * G_u is kept exactly symmetric: each call reads only the blocks on and
+ * above the diagonal (128 x 128 blocks) and writes the new values there and,
+ * transposed, below; statistics not made by base_calib_reset and this call
+ * must be symmetric too.
  * Layout of `stats` (device, 256-B aligned, base_calib_stats_bytes(L)
  * bytes; each array starts on a 256-byte boundary, in this order):
  *   double head[E][4] (n, sum y, sum y^2, unused); double sz[E][d];

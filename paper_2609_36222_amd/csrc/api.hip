@@ -475,7 +475,8 @@ size_t base_calib_ws_bytes(const base_layer *L, int32_t B) {
   if (!L) return 0;
   const base_layer C = calib_layer(L);
   if (check_layer(&C, B, false, false, false) != BASE_OK) return 0;
-  return layout(&C, B, C.E).total + up256((size_t)B * 8) + up256((size_t)B * C.K * 8);
+  return layout(&C, B, C.E).total + up256((size_t)B * 8) + up256((size_t)B * C.K * 8) +
+         up256((size_t)(B + 1) * C.d * 4);
 }
 
 base_status base_calib_reset(const base_layer *L, void *stats, void *stream) {
@@ -536,8 +537,10 @@ base_status base_calib_accumulate(const base_layer *L, const void *z, int32_t B,
                       at<void>(ws, o.H), at<float>(ws, o.pairbuf), st));
   double *inv = at<double>(ws, o.total);
   double *y = at<double>(ws, o.total + up256((size_t)B * 8));
+  float *zbuf = at<float>(ws, o.total + up256((size_t)B * 8) + up256((size_t)B * C.K * 8));
   HIP_TRY(launch_calib_stats(z, bf16, B, C.d, C.E, C.K, at<float>(ws, o.pairbuf), nsel, sel,
-                             offsets, pair_tok, inv, y, calib_stats_at(stats, C.E, C.d), st));
+                             offsets, pair_tok, inv, y, zbuf, calib_stats_at(stats, C.E, C.d),
+                             st));
   return BASE_OK;
 }
 

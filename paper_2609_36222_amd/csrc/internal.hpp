@@ -223,7 +223,7 @@ hipError_t launch_calib_zero(void *stats, size_t bytes, hipStream_t st);
 hipError_t launch_calib_stats(const void *x, bool bf16, int B, int d, int E, int K,
                               const float *pairbuf, const int32_t *n_sel,
                               const int32_t *sel_ids, const int32_t *offsets,
-                              const int32_t *pair_tok, double *inv, double *y,
+                              const int32_t *pair_tok, double *inv, double *y, float *zbuf,
                               CalibStats st, hipStream_t s);
 
 // internal flags bit of the backfill: unit gates (calibration runs the
