@@ -166,7 +166,7 @@ __device__ __forceinline__ void gateup_unit(uint8_t *ring, uint8_t *dummy, int d
   constexpr int SLOT = NT * 2048;       // one step's token lines in the ring
   constexpr int LPS = 6;                // loads per step and wavefront
   static_assert(NT <= W, "one token tile per wavefront");
-  static_assert(DW % 2 == 0 && DW / 2 > DT, "weights requested before the step's tokens");
+  static_assert(DW % 2 == 0 && DT == DW / 2 + 1, "tokens requested before the step's weights");
   const int w = wave_id_u(), lane = lane_id();
   const int KS = d / 32, NS = KS / 2;
   const bool active = w < nrp;
@@ -207,30 +207,43 @@ __device__ __forceinline__ void gateup_unit(uint8_t *ring, uint8_t *dummy, int d
   f32x4 ag[NT], au[NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j) { ag[j] = f32x4{0, 0, 0, 0}; au[j] = f32x4{0, 0, 0, 0}; }
-  // the first token loads before the first weight loads: the wait of step
-  // st below allows (DT - 1) * LPS younger loads, and for the first steps
-  // the prologue's weight loads are among them
-#pragma unroll
-  for (int p = 0; p < DT; ++p) tok_load(p);
+  // Loads go out in groups, one per step: the token lines of step st + DT
+  // (DT = DW / 2 + 1) and then the weights of step st + DW / 2.  A step's
+  // tokens are thus requested one group before its weights, so the wait for
+  // the weights (at most DW / 2 - 1 younger groups in flight) covers the
+  // tokens too and never waits for weights still ahead; vmcnt counts in
+  // issue order.  The prologue issues groups -DT .. -1 the same way.
   bf16x8 wg[DW], wu[DW];
 #pragma unroll
-  for (int p = 0; p < DW; ++p) {
-    wg[p] = bload(ws.r0, ws.v0, ksoff(ws, p, KS));
-    wu[p] = bload(ws.r1, ws.v1, ksoff(ws, p, KS));
+  for (int j = 0; j < DT; ++j) {
+    tok_load(j);
+    if (j >= DT - DW / 2) {
+      const int q = 2 * (j - (DT - DW / 2));
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        wg[q + e] = bload(ws.r0, ws.v0, ksoff(ws, q + e, KS));
+        wu[q + e] = bload(ws.r1, ws.v1, ksoff(ws, q + e, KS));
+      }
+    }
   }
   for (int k0 = 0; k0 < KS; k0 += DW) {
 #pragma unroll
     for (int p = 0; p < DW; p += 2) {
       const int ks = k0 + p, st = ks / 2;
-      // this wavefront's loads of step st are done: at most the loads of
-      // the DT - 1 later steps are in flight
-      wait_vm<(DT - 1) * LPS>();
+      // this wavefront's loads of step st are done: at most the DW / 2 - 1
+      // later groups are in flight; after the barrier the ring slot of step
+      // st - 1 is free for the tokens of step st + DT (issued before the
+      // MFMAs), and each k-step's weight registers are refilled as soon as
+      // its MFMAs have read them
+      wait_vm<(DW / 2 - 1) * LPS>();
       wg_barrier();
       __builtin_amdgcn_sched_barrier(0);
-      if (active) {
-        const uint8_t *sb = ring + (st % (DT + 1)) * SLOT;
+      tok_load(st + DT);
+      __builtin_amdgcn_sched_barrier(0);
+      const uint8_t *sb = ring + (st % (DT + 1)) * SLOT;
 #pragma unroll
-        for (int e = 0; e < 2; ++e) {
+      for (int e = 0; e < 2; ++e) {
+        if (active) {
           const uint8_t *se = sb + (e == 0 ? rb0 : rb1);
           bf16x8 xc = *reinterpret_cast<const bf16x8 *>(se);
 #pragma unroll
@@ -243,15 +256,11 @@ __device__ __forceinline__ void gateup_unit(uint8_t *ring, uint8_t *dummy, int d
             xc = xn;
           }
         }
-      }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
+        __builtin_amdgcn_sched_barrier(0);
         wg[p + e] = bload(ws.r0, ws.v0, ksoff(ws, ks + e + DW, KS));
         wu[p + e] = bload(ws.r1, ws.v1, ksoff(ws, ks + e + DW, KS));
+        __builtin_amdgcn_sched_barrier(0);
       }
-      tok_load(st + DT);
-      __builtin_amdgcn_sched_barrier(0);
     }
   }
   wait_vm<0>();

@@ -66,11 +66,11 @@ inline int ffn_max_tiles(int B, int K, int budget, int ns) {
 // shared slot; a unit of work is (part, row group), one per workgroup of
 // FFN_WAVES wavefronts at a time, each wavefront owning 16-row tiles over the
 // whole contraction with weights requested FFN_GU_DW (gate/up) or FFN_DN_DW
-// (down) k-steps ahead and token fragments FFN_GU_DT steps (two k-steps each)
-// or FFN_DN_DT k-steps ahead.
+// (down) k-steps ahead and token fragments FFN_GU_DT steps (two k-steps each,
+// one step further ahead than the weights) or FFN_DN_DT k-steps ahead.
 constexpr int FFN_WAVES = 8;
 constexpr int FFN_GU_DW = 8;
-constexpr int FFN_GU_DT = 2;
+constexpr int FFN_GU_DT = FFN_GU_DW / 2 + 1;
 constexpr int FFN_DN_DW = 2;
 constexpr int FFN_DN_DT = 2;
 // wavefronts per SIMD the down kernel's registers allow: three workgroups
