@@ -427,10 +427,11 @@ void k_gateup_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w13
 }
 static_assert(FFN_GU_PT == 6, "gate/up tile-count cases");
 
-// down: FFN_WAVES row tiles of 16 rows of d per unit, DW k-steps of weights
-// in flight; registers for WPE wavefronts per SIMD (FFN_DN_WPE / FFN_DN_DW
-// for the usual short contractions, FFN_DN_WPE_LONG / FFN_DN_DW_LONG for
-// long ones, whose few units each stream many k-steps).
+// down: hdr.rt_dn row tiles of 16 rows of d per unit (FFN_WAVES, fewer for
+// a long contraction when the units would not fill the workgroups), DW
+// k-steps of weights in flight; registers for WPE wavefronts per SIMD
+// (FFN_DN_WPE / FFN_DN_DW for the usual short contractions, FFN_DN_WPE_LONG
+// / FFN_DN_DW_LONG for long ones, whose few units each stream many k-steps).
 template <bool PACKED, int DW, int WPE>
 __global__ __launch_bounds__(FFN_WAVES * WAVE, WPE)
 void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
@@ -441,6 +442,8 @@ void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
   __shared__ __attribute__((aligned(16))) uint8_t dummy[FFN_WAVES * 1024];
   hdr += blockIdx.x % N_XCD;   // this die's header and run
   const int T = d / 16;          // row tiles per expert
+  const int RD = __builtin_amdgcn_readfirstlane(hdr->rt_dn);
+  if (RD < 1 || RD > FFN_WAVES) return;
   const Run run = die_run(hdr->dn0, hdr->dn1);
   for (int k = run.k0; k < run.k1; k += run.step) {
     const PartU pt = load_unit(units + k);
@@ -448,7 +451,7 @@ void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
     const uint16_t *w2 = pt.u < E ? w2r : w2s;
     PartU q = pt;
     q.u = pt.u < E ? pt.u : pt.u - E;
-    const int rt0 = pt.rg * FFN_WAVES, nrt = min(FFN_WAVES, T - rt0);
+    const int rt0 = pt.rg * RD, nrt = min(RD, T - rt0);
     if (nrt < 1) continue;
     wg_barrier();
 #define BASE_DN(N) case N: down_unit<N, PACKED, DW>(ring, dummy, d, I, w2, q, rt0, nrt, pair_gate, hp, pairbuf); break;

@@ -96,15 +96,16 @@ static_assert((size_t)MAX_B * 16384 * 2 < FFN_TOK_PAD, "token row offsets below 
 // A unit: expert u (u >= E: shared expert u - E), the part's first 16-pair
 // tile, its tile count, its first pair in the compacted order and its pair
 // count, and the unit's row group (gate/up: hdr.rp_gu row-pair tiles;
-// down: FFN_WAVES row tiles).
+// down: hdr.rt_dn row tiles).
 struct alignas(32) FfnUnit {
   int32_t u, tile0, nt, p0, n, rg, pad0, pad1;
 };
 // Die x's header, written by the compaction workgroup that ran on die x:
-// gate/up's row group and die x's runs of units, [gu0, gu1) of the gate/up
-// table and [dn0, dn1) of the down table.
+// gate/up's row group (rp_gu row-pair tiles), down's (rt_dn row tiles) and
+// die x's runs of units, [gu0, gu1) of the gate/up table and [dn0, dn1) of
+// the down table.
 struct alignas(32) FfnHdr {
-  int32_t rp_gu, gu0, gu1, dn0, dn1, pad0, pad1, pad2;
+  int32_t rp_gu, gu0, gu1, dn0, dn1, rt_dn, pad1, pad2;
 };
 
 // Upper bound of the parts of a launch with at most pt tiles per part: the
@@ -113,12 +114,12 @@ inline int ffn_parts_bound(int B, int K, int budget, int ns, int pt) {
   return ffn_max_tiles(B, K, budget, ns) / pt + budget + ns + 1;
 }
 // Upper bounds of the units: every part times its row groups (gate/up: at
-// least FFN_WAVES / 2 row-pair tiles per group; down: FFN_WAVES row tiles).
+// least FFN_WAVES / 2 row-pair tiles per group; down: at least 2 row tiles).
 inline int ffn_units_bound_gu(int B, int K, int budget, int ns, int I) {
   return ffn_parts_bound(B, K, budget, ns, FFN_GU_PT) * ((I / 16 + FFN_WAVES / 2 - 1) / (FFN_WAVES / 2));
 }
 inline int ffn_units_bound_dn(int B, int K, int budget, int ns, int d) {
-  return ffn_parts_bound(B, K, budget, ns, FFN_DN_PT) * ((d / 16 + FFN_WAVES - 1) / FFN_WAVES);
+  return ffn_parts_bound(B, K, budget, ns, FFN_DN_PT) * ((d / 16 + 1) / 2);
 }
 // Workgroups of the FFN launches: a multiple of N_XCD, from the device's
 // compute units -- gate/up one per CU (its registers allow no second), down

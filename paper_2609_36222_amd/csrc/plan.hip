@@ -751,7 +751,30 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
       const int cost = (int)ceilf((float)units / per_die) * c;
       if (cost < best_cost) { rp = c; best_cost = cost; }
     }
-    const int ug = (T + rp - 1) / rp, ud = (d / 16 + FFN_WAVES - 1) / FFN_WAVES;
+    // down's row group: FFN_WAVES row tiles, or for a long contraction (one
+    // workgroup per CU) fewer when that gives the busiest workgroup fewer
+    const int Td = d / 16;
+    int rd = FFN_WAVES;
+    if (ffn_dn_long(I)) {
+      int pdmax = (Pd + N_XCD - 1) / N_XCD;
+      if (whole) {
+        pdmax = 0;
+        for (int y = 0, j = 0; y < N_XCD; ++y) {
+          const int jn = j + (nslot - y + N_XCD - 1) / N_XCD;
+          pdmax = max(pdmax, pre_dn[jn] - pre_dn[j]);
+          j = jn;
+        }
+      }
+      const float wgs = (float)(ffn_dn_grid(n_cu, I) / N_XCD);
+      int best = 0x7FFFFFFF;
+      for (int c = FFN_WAVES; c >= 2; c /= 2) {
+        const int units = whole ? pdmax * ((Td + c - 1) / c)
+                                : (Pd * ((Td + c - 1) / c) + N_XCD - 1) / N_XCD;
+        const int cost = (int)ceilf((float)units / wgs) * c;
+        if (cost < best) { rd = c; best = cost; }
+      }
+    }
+    const int ug = (T + rp - 1) / rp, ud = (Td + rd - 1) / rd;
     // die y's first unit in both tables and first position.  Whole slots:
     // the first position of die y.  Otherwise, from the target gate/up unit
     // Pg ug y / N_XCD at position j: the start of its row group r of ug, and
@@ -796,7 +819,8 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
       FfnHdr h;
       h.rp_gu = rp;
       h.gu0 = g0; h.gu1 = g1; h.dn0 = d0; h.dn1 = d1;
-      h.pad0 = h.pad1 = h.pad2 = 0;
+      h.rt_dn = rd;
+      h.pad1 = h.pad2 = 0;
       hdr[x] = h;
     }
     // unit i: its position (the first j with pre[j + 1] * upp > i) and
