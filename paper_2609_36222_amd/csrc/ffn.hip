@@ -282,6 +282,10 @@ __device__ __forceinline__ void gateup_unit(uint8_t *ring, uint8_t *dummy, int d
   }
 }
 
+// Down's token depth: FFN_DN_DT k-steps, or for the deep instance one
+// k-step beyond its weights.
+constexpr int dn_token_depth(int dw) { return dw > FFN_DN_DW ? dw + 1 : FFN_DN_DT; }
+
 // One unit of down: wavefront w owns row tile rt = rt0 + w (rows 16 rt ..
 // 16 rt + 15 of W_d), if w < nrt; the tokens are the part's SwiGLU
 // activations.  pairbuf[p][c] = gate_p * (H[p] . W_d[c]).
@@ -291,7 +295,9 @@ __device__ __forceinline__ void down_unit(uint8_t *ring, uint8_t *dummy, int d, 
                                           int rt0, int nrt, const float *__restrict__ pair_gate,
                                           const uint16_t *__restrict__ hp,
                                           float *__restrict__ pairbuf) {
-  constexpr int W = FFN_WAVES, DT = FFN_DN_DT;
+  // the deep instance requests tokens one k-step before its weights
+  constexpr bool TA = DW > FFN_DN_DW;
+  constexpr int W = FFN_WAVES, DT = dn_token_depth(DW);
   constexpr int NTK = (NT + W - 1) / W;
   const int w = wave_id_u(), lane = lane_id();
   const int KS = I / 32;
@@ -337,19 +343,34 @@ __device__ __forceinline__ void down_unit(uint8_t *ring, uint8_t *dummy, int d, 
 #pragma unroll
   for (int j = 0; j < NT; ++j) acc[j] = f32x4{0, 0, 0, 0};
   bf16x8 wb[DW];
-  // token loads next, then the weights (see gateup_unit); the gate loads are
-  // older still, so the first k-step's wait also covers them (their L2 round
-  // trip overlaps the first weights' HBM one)
+  // token loads next, then the weights; the gate loads are older still, so
+  // the first k-step's wait also covers them (their L2 round trip overlaps
+  // the first weights' HBM one).  The deep instance issues its loads in
+  // groups as gate/up does (the tokens of k-step ks + DT, then the weights
+  // of ks + DW, DT = DW + 1), so that its wait for a k-step's weights
+  // covers that k-step's tokens and leaves the later weights in flight; the
+  // short one waits for the tokens of DT = DW k-steps back, which with two
+  // k-steps of weights in flight measured faster.
+  if (TA) {
 #pragma unroll
-  for (int p = 0; p < DT; ++p) tok_load(p);
+    for (int j = 0; j < DT; ++j) {
+      tok_load(j);
+      if (j >= DT - DW) wb[j - (DT - DW)] = bload(ws.r0, ws.v0, ksoff(ws, j - (DT - DW), KS));
+    }
+  } else {
 #pragma unroll
-  for (int p = 0; p < DW; ++p) wb[p] = bload(ws.r0, ws.v0, ksoff(ws, p, KS));
+    for (int p = 0; p < DT; ++p) tok_load(p);
+#pragma unroll
+    for (int p = 0; p < DW; ++p) wb[p] = bload(ws.r0, ws.v0, ksoff(ws, p, KS));
+  }
   for (int k0 = 0; k0 < KS; k0 += DW) {
 #pragma unroll
     for (int p = 0; p < DW; ++p) {
       const int ks = k0 + p;
-      wait_vm<(DT - 1) * (1 + NTK)>();
+      wait_vm<(TA ? DW - 1 : DT - 1) * (1 + NTK)>();
       wg_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      if (TA) tok_load(ks + DT);
       __builtin_amdgcn_sched_barrier(0);
       if (active) {
         const uint8_t *sb = ring + (ks % (DT + 1)) * (NT * 1024) + lane * 16;
@@ -365,7 +386,7 @@ __device__ __forceinline__ void down_unit(uint8_t *ring, uint8_t *dummy, int d, 
       }
       __builtin_amdgcn_sched_barrier(0);
       wb[p] = bload(ws.r0, ws.v0, ksoff(ws, ks + DW, KS));
-      tok_load(ks + DT);
+      if (!TA) tok_load(ks + DT);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
@@ -438,7 +459,7 @@ void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
                  const uint16_t *__restrict__ w2s, const FfnHdr *__restrict__ hdr,
                  const FfnUnit *__restrict__ units, const float *__restrict__ pair_gate,
                  const uint16_t *__restrict__ hp, float *__restrict__ pairbuf) {
-  __shared__ __attribute__((aligned(16))) uint8_t ring[(FFN_DN_DT + 1) * FFN_DN_PT * 1024];
+  __shared__ __attribute__((aligned(16))) uint8_t ring[(dn_token_depth(DW) + 1) * FFN_DN_PT * 1024];
   __shared__ __attribute__((aligned(16))) uint8_t dummy[FFN_WAVES * 1024];
   hdr += blockIdx.x % N_XCD;   // this die's header and run
   const int T = d / 16;          // row tiles per expert

@@ -67,7 +67,8 @@ inline int ffn_max_tiles(int B, int K, int budget, int ns) {
 // FFN_WAVES wavefronts at a time, each wavefront owning 16-row tiles over the
 // whole contraction with weights requested FFN_GU_DW (gate/up) or FFN_DN_DW
 // (down) k-steps ahead and token fragments FFN_GU_DT steps (two k-steps each,
-// one step further ahead than the weights) or FFN_DN_DT k-steps ahead.
+// one step further ahead than the weights) or FFN_DN_DT k-steps ahead (the
+// deep down instance: one k-step further ahead than its weights).
 constexpr int FFN_WAVES = 8;
 constexpr int FFN_GU_DW = 8;
 constexpr int FFN_GU_DT = FFN_GU_DW / 2 + 1;

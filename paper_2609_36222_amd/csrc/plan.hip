@@ -746,7 +746,10 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
     }
     int rp = FFN_WAVES, best_cost = 0x7FFFFFFF;
     for (int c = FFN_WAVES; c >= FFN_WAVES / 2; --c) {
-      const int units = pmax * ((T + c - 1) / c);
+      // the busiest die's units: its dealt parts' row groups, or an equal
+      // share of all of them
+      const int units = whole ? pmax * ((T + c - 1) / c)
+                              : (Pg * ((T + c - 1) / c) + N_XCD - 1) / N_XCD;
       // rounds = ceil(units / per_die); exact in fp32 for these small integers
       const int cost = (int)ceilf((float)units / per_die) * c;
       if (cost < best_cost) { rp = c; best_cost = cost; }
