@@ -282,8 +282,8 @@ __device__ __forceinline__ void gateup_unit(uint8_t *ring, uint8_t *dummy, int d
   }
 }
 
-// Down's token depth: FFN_DN_DT k-steps, or for the deep instance one
-// k-step beyond its weights.
+// Down's token depth: FFN_DN_DT k-steps, or for the deeper instances one
+// k-step beyond their weights.
 constexpr int dn_token_depth(int dw) { return dw > FFN_DN_DW ? dw + 1 : FFN_DN_DT; }
 
 // One unit of down: wavefront w owns row tile rt = rt0 + w (rows 16 rt ..
@@ -295,7 +295,7 @@ __device__ __forceinline__ void down_unit(uint8_t *ring, uint8_t *dummy, int d, 
                                           int rt0, int nrt, const float *__restrict__ pair_gate,
                                           const uint16_t *__restrict__ hp,
                                           float *__restrict__ pairbuf) {
-  // the deep instance requests tokens one k-step before its weights
+  // the deeper instances request tokens one k-step before their weights
   constexpr bool TA = DW > FFN_DN_DW;
   constexpr int W = FFN_WAVES, DT = dn_token_depth(DW);
   constexpr int NTK = (NT + W - 1) / W;
@@ -345,9 +345,9 @@ __device__ __forceinline__ void down_unit(uint8_t *ring, uint8_t *dummy, int d, 
   bf16x8 wb[DW];
   // token loads next, then the weights; the gate loads are older still, so
   // the first k-step's wait also covers them (their L2 round trip overlaps
-  // the first weights' HBM one).  The deep instance issues its loads in
+  // the first weights' HBM one).  The deeper instances issue their loads in
   // groups as gate/up does (the tokens of k-step ks + DT, then the weights
-  // of ks + DW, DT = DW + 1), so that its wait for a k-step's weights
+  // of ks + DW, DT = DW + 1), so that the wait for a k-step's weights
   // covers that k-step's tokens and leaves the later weights in flight; the
   // short one waits for the tokens of DT = DW k-steps back, which with two
   // k-steps of weights in flight measured faster.
@@ -450,9 +450,11 @@ static_assert(FFN_GU_PT == 6, "gate/up tile-count cases");
 
 // down: hdr.rt_dn row tiles of 16 rows of d per unit (FFN_WAVES, fewer for
 // a long contraction when the units would not fill the workgroups), DW
-// k-steps of weights in flight; registers for WPE wavefronts per SIMD
-// (FFN_DN_WPE / FFN_DN_DW for the usual short contractions, FFN_DN_WPE_LONG
-// / FFN_DN_DW_LONG for long ones, whose few units each stream many k-steps).
+// k-steps of weights in flight; registers for WPE wavefronts per SIMD.
+// Three instances (ffn_dn_kind): FFN_DN_WPE / FFN_DN_DW for launches with
+// many kept slots, FFN_DN_WPE_MID / FFN_DN_DW_MID for few, FFN_DN_WPE_LONG
+// / FFN_DN_DW_LONG for long contractions, whose few units each stream many
+// k-steps.
 template <bool PACKED, int DW, int WPE>
 __global__ __launch_bounds__(FFN_WAVES * WAVE, WPE)
 void k_down_bf16(int d, int I, int E, int ns, const uint16_t *__restrict__ w2r,
@@ -616,13 +618,15 @@ hipError_t launch_down(bool bf16, bool packed, int B, int d, int I, int E, int K
                        const FfnHdr *hdr, const FfnUnit *units, int n_cu,
                        const float *pair_gate, const void *H, float *pairbuf, hipStream_t st) {
   if (bf16) {
-    const bool lng = ffn_dn_long(I);
+    const int kind = ffn_dn_kind(budget, ns, I);
     const auto kern =
-        lng ? (packed ? k_down_bf16<true, FFN_DN_DW_LONG, FFN_DN_WPE_LONG>
-                      : k_down_bf16<false, FFN_DN_DW_LONG, FFN_DN_WPE_LONG>)
-            : (packed ? k_down_bf16<true, FFN_DN_DW, FFN_DN_WPE>
-                      : k_down_bf16<false, FFN_DN_DW, FFN_DN_WPE>);
-    launch_k(kern, dim3(ffn_dn_grid(n_cu, I)), dim3(FFN_WAVES * WAVE), 0, st, d, I, E, ns,
+        kind == 2 ? (packed ? k_down_bf16<true, FFN_DN_DW_LONG, FFN_DN_WPE_LONG>
+                            : k_down_bf16<false, FFN_DN_DW_LONG, FFN_DN_WPE_LONG>)
+        : kind == 1 ? (packed ? k_down_bf16<true, FFN_DN_DW_MID, FFN_DN_WPE_MID>
+                              : k_down_bf16<false, FFN_DN_DW_MID, FFN_DN_WPE_MID>)
+                    : (packed ? k_down_bf16<true, FFN_DN_DW, FFN_DN_WPE>
+                              : k_down_bf16<false, FFN_DN_DW, FFN_DN_WPE>);
+    launch_k(kern, dim3(ffn_dn_grid(n_cu, kind)), dim3(FFN_WAVES * WAVE), 0, st, d, I, E, ns,
              (const uint16_t *)w2,
              (const uint16_t *)w2s, hdr, units, pair_gate, (const uint16_t *)H, pairbuf);
   } else {

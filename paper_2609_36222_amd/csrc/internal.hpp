@@ -84,6 +84,16 @@ constexpr int FFN_DN_LONG_KS = 64;
 constexpr int FFN_DN_DW_LONG = 8;
 constexpr int FFN_DN_WPE_LONG = 2;
 __host__ __device__ inline bool ffn_dn_long(int I) { return I / 32 > FFN_DN_LONG_KS; }
+// down for launches with few kept slots (fewer than 4 per die, so that the
+// compaction cuts each slot's row groups over the dies): fewer units, so
+// four k-steps of weights in flight and two workgroups per CU
+constexpr int FFN_DN_DW_MID = 4;
+constexpr int FFN_DN_WPE_MID = 4;
+// down's instance: 2 long contraction, 1 few slots (budget + shared ones),
+// 0 otherwise
+__host__ __device__ inline int ffn_dn_kind(int budget, int ns, int I) {
+  return ffn_dn_long(I) ? 2 : (budget + ns < 4 * N_XCD ? 1 : 0);
+}
 constexpr int FFN_GU_PT = 6;
 constexpr int FFN_DN_PT = 8;
 // gate/up reads its token rows straight from the hidden states: entry i of
@@ -124,12 +134,13 @@ inline int ffn_units_bound_dn(int B, int K, int budget, int ns, int d) {
 }
 // Workgroups of the FFN launches: a multiple of N_XCD, from the device's
 // compute units -- gate/up one per CU (its registers allow no second), down
-// FFN_DN_WPE / 2 (or FFN_DN_WPE_LONG / 2) per CU: a workgroup of FFN_WAVES
-// wavefronts puts two on each SIMD.
+// FFN_DN_WPE / 2 (FFN_DN_WPE_MID / 2, FFN_DN_WPE_LONG / 2) per CU: a
+// workgroup of FFN_WAVES wavefronts puts two on each SIMD.
 __host__ __device__ inline unsigned ffn_cu_grid(int n_cu) { return (unsigned)(((n_cu + N_XCD - 1) / N_XCD) * N_XCD); }
 __host__ __device__ inline unsigned ffn_gu_grid(int n_cu) { return ffn_cu_grid(n_cu); }
-__host__ __device__ inline unsigned ffn_dn_grid(int n_cu, int I) {
-  return (unsigned)((ffn_dn_long(I) ? FFN_DN_WPE_LONG : FFN_DN_WPE) / 2) * ffn_cu_grid(n_cu);
+__host__ __device__ inline unsigned ffn_dn_grid(int n_cu, int kind) {
+  const int wpe = kind == 2 ? FFN_DN_WPE_LONG : kind == 1 ? FFN_DN_WPE_MID : FFN_DN_WPE;
+  return (unsigned)(wpe / 2) * ffn_cu_grid(n_cu);
 }
 
 // rows: n_router of Wr (logits, + beta), then the vector G when given (gdot)

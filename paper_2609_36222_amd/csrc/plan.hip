@@ -768,7 +768,7 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
           j = jn;
         }
       }
-      const float wgs = (float)(ffn_dn_grid(n_cu, I) / N_XCD);
+      const float wgs = (float)(ffn_dn_grid(n_cu, 2) / N_XCD);
       int best = 0x7FFFFFFF;
       for (int c = FFN_WAVES; c >= 2; c /= 2) {
         const int units = whole ? pdmax * ((Td + c - 1) / c)
