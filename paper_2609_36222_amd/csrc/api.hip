@@ -92,8 +92,8 @@ base_status check_ptr(const void *p, size_t a) {
 // Workspace layout: every array starts on a 256-byte boundary.
 struct Layout {
   size_t logits, gdot, topk_ids, topk_w, cost, scores, counts, sel_ids, n_sel,
-      slot_of, exec_ids, exec_gates, offsets, pair_tok, pair_gate, pair_of,
-      hdr, units_gu, units_dn, tokoff, H, pairbuf, total;
+      slot_of, exec_ids, exec_gates, offsets, pair_tok, pair_gate, pair_of, order, ex,
+      den, hdr, units_gu, units_dn, tokoff, H, pairbuf, total;
 };
 
 size_t up256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -125,6 +125,11 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
   o.pair_tok = take(P * 4);
   o.pair_gate = take(P * 4);
   o.pair_of = take((size_t)B * (L->K + ns) * 4);
+  // k_tail's rank order, exp(l - l_max) in rank order and denominators,
+  // for the fused layer's backfill
+  o.order = take((size_t)B * L->E);
+  o.ex = take((size_t)B * L->E * 4);
+  o.den = take((size_t)B * 4);
   // the FFN's part tables and their header (bf16)
   const bool bf = L->dtype == BASE_BF16;
   // (one header per die; every die's run of units written on that die)
@@ -421,16 +426,19 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
   HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E, shared_gate(L),
                         logits, at<float>(ws, o.gdot), st));
   stage_end(st);
-  stage(1);   // top-K, weights and (the method's rule) the routed pairs' predictor
+  uint8_t *order = at<uint8_t>(ws, o.order);
+  float *ex = at<float>(ws, o.ex), *den = at<float>(ws, o.den);
+  stage(1);   // top-K, weights, (the method's rule) the routed pairs' predictor,
+              // and each token's experts in rank order for the backfill
   HIP_TRY(launch_tail(bf16, B, L->E, L->K, L->d, L->norm_topk, logits, x, L->pred_a,
-                      L->pred_b, ids, w, cost, 3, L->score_rule, st));
+                      L->pred_b, ids, w, cost, 3, L->score_rule, st, order, ex, den));
   stage_end(st);
   stage(2);   // selection and backfill in one launch
   HIP_TRY(launch_select_backfill(B, L->K, L->E, ids, cost, bc,
-                                 L->score_rule == BASE_SCORE_TOP1, L->norm_topk, flags,
-                                 logits, at<float>(ws, o.scores), at<int32_t>(ws, o.counts),
-                                 sel, nsel, slot, at<int32_t>(ws, o.exec_ids),
-                                 at<float>(ws, o.exec_gates), st));
+                                 L->score_rule == BASE_SCORE_TOP1, flags, order, ex, den,
+                                 at<float>(ws, o.scores), at<int32_t>(ws, o.counts), sel, nsel,
+                                 slot, at<int32_t>(ws, o.exec_ids), at<float>(ws, o.exec_gates),
+                                 st));
   stage_end(st);
   BASE_TRY(run_forward(L, x, B, logits, ids, sel, nsel, slot, bc, flags,
                        residual, y, ws, o, st, true));

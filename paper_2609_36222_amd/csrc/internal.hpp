@@ -153,21 +153,27 @@ constexpr int SCORE_BASE = 0, SCORE_TOP1 = 1, SCORE_WEIGHT = 2, SCORE_WEIGHT_SQ 
               SCORE_STATIC = 4;
 // mode bit 0: top-K + weights from logits; bit 1: per-pair scores of `rule`
 // (SCORE_BASE: the predictor a_u . x / ||x|| from x (rows of d) and A)
+// order / ex / den (optional, route mode): per token the experts in rank
+// order [B][E] (bytes), exp(l - l_max) in rank order [B][E] and the router's
+// softmax denominator S [B], for the fused layer's backfill
 hipError_t launch_tail(bool bf16, int B, int E, int K, int d, int norm_topk,
                        const float *logits, const void *x, const float *A, const float *bp,
                        int32_t *ids, float *w, float *cost, int mode, int rule,
-                       hipStream_t st);
+                       hipStream_t st, uint8_t *order = nullptr, float *ex = nullptr,
+                       float *den = nullptr);
 // binary: rank by (score > 0) instead of the score (the top-1-union rule)
 hipError_t launch_select(int B, int K, int E, const int32_t *ids,
                          const float *cost, int budget, bool binary, float *scores,
                          int32_t *counts, int32_t *sel_ids, int32_t *n_sel,
                          int32_t *slot_of, hipStream_t st);
 // selection and backfill in one launch (same results as the two launches)
+// (order / ex / den: k_tail's rank rows and denominators of the batch)
 hipError_t launch_select_backfill(int B, int K, int E, const int32_t *ids, const float *cost,
-                                  int budget, bool binary, int norm_topk, int flags,
-                                  const float *logits, float *scores, int32_t *counts,
-                                  int32_t *sel_ids, int32_t *n_sel, int32_t *slot_of,
-                                  int32_t *exec_ids, float *exec_gates, hipStream_t st);
+                                  int budget, bool binary, int flags, const uint8_t *order,
+                                  const float *ex, const float *den, float *scores,
+                                  int32_t *counts, int32_t *sel_ids, int32_t *n_sel,
+                                  int32_t *slot_of, int32_t *exec_ids, float *exec_gates,
+                                  hipStream_t st);
 hipError_t launch_backfill(int B, int E, int K, int norm_topk, int flags,
                            const float *logits, const int32_t *ids,
                            const int32_t *slot_of, const int32_t *n_sel,

@@ -372,58 +372,92 @@ void k_backfill(int B, int E, int K, int norm_topk, int flags,
                           route_of(ids, tc, K), slot_of, *n_sel_p, exec_ids, exec_gates);
 }
 
-// Selection and backfill in one launch: every workgroup makes the batch's
-// selection itself (the same fixed-order arithmetic, so the same result
-// everywhere; workgroup 0 writes it out) and then backfills its own
-// SB_TOK tokens, one per wavefront, against the kept set in its LDS (more
-// workgroups with fewer tokens each: the backfill's vector work spreads
-// over more CUs).
+// Selection and backfill in one launch (the fused layer): every workgroup
+// makes the batch's selection itself (the same fixed-order arithmetic, so
+// the same result everywhere; workgroup 0 writes it out) and then backfills
+// its own SB_TOK tokens, one per wavefront, on the tokens' own die.  The
+// backfill takes the token's experts in rank order (order, written by
+// k_tail with exp(l - l_max) in rank order, ex, and the router's
+// denominator S, den), requested before the selection: the first
+// min(K, n_sel) kept ones are executed (drop: its routed experts, ranks
+// 0 .. K - 1, that were kept, in routing order), each with numerator
+// exp(l - l_max) and denominator S or, renormalised, the numerators' sum in
+// execution order -- the values and the order of backfill_body.
+template <int NCH>
 __global__ __launch_bounds__(SEL_THREADS)
 void k_select_backfill(int B, int K, int E, const int32_t *__restrict__ ids,
-                       const float *__restrict__ cost, int budget, int binary,
-                       int norm_topk, int flags, const float *__restrict__ logits,
-                       float *__restrict__ scores, int32_t *__restrict__ counts,
-                       int32_t *__restrict__ sel_ids, int32_t *__restrict__ n_sel_out,
-                       int32_t *__restrict__ slot_of, int32_t *__restrict__ exec_ids,
-                       float *__restrict__ exec_gates) {
-  __shared__ union {
-    SelLds sel;
-    BfLds<SB_WAVES> bf;
-  } U;
+                       const float *__restrict__ cost, int budget, int binary, int flags,
+                       const uint8_t *__restrict__ order, const float *__restrict__ ex,
+                       const float *__restrict__ den, float *__restrict__ scores,
+                       int32_t *__restrict__ counts, int32_t *__restrict__ sel_ids,
+                       int32_t *__restrict__ n_sel_out, int32_t *__restrict__ slot_of,
+                       int32_t *__restrict__ exec_ids, float *__restrict__ exec_gates) {
+  __shared__ SelLds S;
   __shared__ int slot_s[MAX_E];
-  __shared__ float lrow[SB_TOK][MAX_E];
-  // the backfill's own loads first (its token's logits row and routes), so
-  // that they are in flight while the selection runs
   const int lane = lane_id(), wv = wave_id();
   int tg, tq;
   xcd_group(blockIdx.x, TOK_GROUP / SB_TOK, tg, tq);
   if (tg * TOK_GROUP >= B) return;
   const bool active = wv < SB_TOK;
-  // the tokens of group tg sit on die tg % N_XCD, where their logits were
-  // written
+  // the tokens of group tg sit on die tg % N_XCD, where k_tail wrote their
+  // rank rows
   const int t = tg * TOK_GROUP + tq * SB_TOK + wv, tc = min(t, B - 1);
-  float lv[MAX_E / WAVE];
+  int ov[NCH];
+  float xv[NCH];
 #pragma unroll
-  for (int i = 0; i < MAX_E / WAVE; ++i) {
-    const int e = lane + WAVE * i;
-    lv[i] = (active && e < E) ? logits[(size_t)tc * E + e] : 0.0f;
+  for (int c = 0; c < NCH; ++c) {
+    const int r = min(WAVE * c + lane, E - 1);
+    ov[c] = active ? order[(size_t)tc * E + r] : 0;
+    xv[c] = active ? ex[(size_t)tc * E + r] : 0.0f;
   }
-  const int r_k = route_of(ids, tc, K);
+  const float dv = active ? den[tc] : 1.0f;
   int uk[MAX_K];
   float ck[MAX_K];
-  load_routes(B, K, ids, cost, U.sel.V, uk, ck);
-  const int n_sel = select_body(U.sel, B, K, E, budget, binary, uk, ck, blockIdx.x == 0,
-                                scores, counts, sel_ids, n_sel_out, slot_of, slot_s);
-  if (active) {
+  load_routes(B, K, ids, cost, S.V, uk, ck);
+  const int n_sel = select_body(S, B, K, E, budget, binary, uk, ck, blockIdx.x == 0, scores,
+                                counts, sel_ids, n_sel_out, slot_of, slot_s);
+  __syncthreads();   // slot_s complete
+  if (!active || t >= B) return;
+  const int kp = min(K, n_sel);
+  const bool drop = flags & 2, renorm = flags & 1;
+  const uint64_t below = (1ull << lane) - 1ull;
+  int nx = 0;
+  float Ssum = 0.0f;
+  int tj[NCH];   // this lane's execution position in chunk c (-1: none)
 #pragma unroll
-    for (int i = 0; i < MAX_E / WAVE; ++i) {
-      const int e = lane + WAVE * i;
-      if (e < E) lrow[wv][e] = lv[i];
+  for (int c = 0; c < NCH; ++c) {
+    tj[c] = -1;
+    if (drop ? c == 0 : nx < kp) {
+      const int r = WAVE * c + lane;
+      const int e = ov[c];
+      const bool cand = (drop ? lane < K : r < E) && e < E && slot_s[e] >= 0;
+      const int j = nx + __popcll(__ballot(cand) & below);
+      const bool take = cand && (drop || j < kp);
+      if (take) tj[c] = j;
+      uint64_t mt = __ballot(take);
+      nx += __popcll(mt);
+      if (renorm) {
+        while (mt) {
+          const int b = __builtin_ctzll(mt);
+          Ssum = Ssum + __builtin_bit_cast(
+                            float, __builtin_amdgcn_readlane(__float_as_int(xv[c]), b));
+          mt &= mt - 1;
+        }
+      }
     }
   }
-  __syncthreads();   // slot_s and lrow complete; the selection's LDS is free
-  backfill_body<SB_WAVES>(U.bf, active, t, B, E, K, norm_topk, flags,
-                          lrow[active ? wv : 0], r_k, slot_s, n_sel, exec_ids, exec_gates);
+  if (!renorm) Ssum = dv;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    if (tj[c] >= 0) {
+      exec_ids[(size_t)t * K + tj[c]] = ov[c];
+      exec_gates[(size_t)t * K + tj[c]] = (flags & FLAG_UNIT_GATES) ? 1.0f : xv[c] / Ssum;
+    }
+  }
+  if (lane < K && lane >= nx) {
+    exec_ids[(size_t)t * K + lane] = -1;
+    exec_gates[(size_t)t * K + lane] = 0.0f;
+  }
 }
 
 // Exclusive prefixes over slots s < n of cnt[s] (pairs) and ceil(cnt[s] /
@@ -920,14 +954,20 @@ hipError_t launch_select(int B, int K, int E, const int32_t *ids,
 }
 
 hipError_t launch_select_backfill(int B, int K, int E, const int32_t *ids, const float *cost,
-                                  int budget, bool binary, int norm_topk, int flags,
-                                  const float *logits, float *scores, int32_t *counts,
-                                  int32_t *sel_ids, int32_t *n_sel, int32_t *slot_of,
-                                  int32_t *exec_ids, float *exec_gates, hipStream_t st) {
-  launch_k(k_select_backfill, dim3(xcd_grid((B + TOK_GROUP - 1) / TOK_GROUP, TOK_GROUP / SB_TOK)),
-           dim3(SEL_THREADS), 0, st,
-           B, K, E, ids, cost, budget, (int)binary, norm_topk, flags, logits, scores, counts,
-           sel_ids, n_sel, slot_of, exec_ids, exec_gates);
+                                  int budget, bool binary, int flags, const uint8_t *order,
+                                  const float *ex, const float *den, float *scores,
+                                  int32_t *counts, int32_t *sel_ids, int32_t *n_sel,
+                                  int32_t *slot_of, int32_t *exec_ids, float *exec_gates,
+                                  hipStream_t st) {
+  const dim3 grid(xcd_grid((B + TOK_GROUP - 1) / TOK_GROUP, TOK_GROUP / SB_TOK));
+#define BASE_SB(C)                                                                         \
+  launch_k(k_select_backfill<C>, grid, dim3(SEL_THREADS), 0, st, B, K, E, ids, cost, budget, \
+           (int)binary, flags, order, ex, den, scores, counts, sel_ids, n_sel, slot_of,     \
+           exec_ids, exec_gates)
+  if (E <= WAVE) BASE_SB(1);
+  else if (E <= 2 * WAVE) BASE_SB(2);
+  else BASE_SB(4);
+#undef BASE_SB
   return hipGetLastError();
 }
 

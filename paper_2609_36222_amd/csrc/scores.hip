@@ -276,7 +276,8 @@ __global__ __launch_bounds__(TL_MAXW * WAVE)
 void k_tail(int B, int E, int K, int d, int norm_topk, const float *__restrict__ logits,
             const XT *__restrict__ x, const float *__restrict__ A,
             const float *__restrict__ bp, int32_t *__restrict__ ids_io,
-            float *__restrict__ w_io, float *__restrict__ cost, int mode, int rule) {
+            float *__restrict__ w_io, float *__restrict__ cost, int mode, int rule,
+            uint8_t *__restrict__ order, float *__restrict__ ex, float *__restrict__ den) {
   __shared__ __attribute__((aligned(16))) uint64_t keys[MAX_E];
   __shared__ float lrow[MAX_E];
   __shared__ int part[TL_RANK];
@@ -350,10 +351,10 @@ void k_tail(int B, int E, int K, int d, int norm_topk, const float *__restrict__
       part[tid] = r;
     }
     __syncthreads();
+    int my_rank = 0;   // thread tid < E: the rank of expert tid
     if (tid < E) {
-      int r = 0;
-      for (int c = 0; c < C; ++c) r += part[c * E2 + tid];
-      if (r < K) route[r] = tid;
+      for (int c = 0; c < C; ++c) my_rank += part[c * E2 + tid];
+      if (my_rank < K) route[my_rank] = tid;
     }
     __syncthreads();
     my_id = route[min(lane, K - 1)];
@@ -375,6 +376,15 @@ void k_tail(int B, int E, int K, int d, int norm_topk, const float *__restrict__
     if (w == 0 && lane < K) {
       ids_io[(size_t)t * K + lane] = my_id;
       w_io[(size_t)t * K + lane] = my_w;
+    }
+    if (order) {
+      // for the fused layer's backfill: the experts in rank order, their
+      // exp(l - l_max) in rank order, and the router's denominator S
+      if (tid < E) {
+        order[(size_t)t * E + my_rank] = (uint8_t)tid;
+        ex[(size_t)t * E + my_rank] = base_exp(lrow[tid] - lmax);
+      }
+      if (tid == 0) den[t] = S;
     }
   }
   if (!(mode & 2)) return;
@@ -470,15 +480,15 @@ hipError_t launch_scores(bool bf16, const void *x, int B, int d, const float *Wr
 hipError_t launch_tail(bool bf16, int B, int E, int K, int d, int norm_topk,
                        const float *logits, const void *x, const float *A, const float *bp,
                        int32_t *ids, float *w, float *cost, int mode, int rule,
-                       hipStream_t st) {
+                       hipStream_t st, uint8_t *order, float *ex, float *den) {
   const dim3 block(tail_waves(K, (mode & 2) && rule == SCORE_BASE) * WAVE);
   const dim3 grid(xcd_grid((B + TOK_GROUP - 1) / TOK_GROUP, TOK_GROUP));
   if (bf16)
     launch_k(k_tail<uint16_t>, grid, block, 0, st, B, E, K, d, norm_topk, logits,
-             (const uint16_t *)x, A, bp, ids, w, cost, mode, rule);
+             (const uint16_t *)x, A, bp, ids, w, cost, mode, rule, order, ex, den);
   else
     launch_k(k_tail<float>, grid, block, 0, st, B, E, K, d, norm_topk, logits,
-             (const float *)x, A, bp, ids, w, cost, mode, rule);
+             (const float *)x, A, bp, ids, w, cost, mode, rule, order, ex, den);
   return hipGetLastError();
 }
 
