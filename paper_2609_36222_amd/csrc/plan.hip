@@ -904,8 +904,14 @@ void k_compact(int B, int K, uint64_t kmul, int E, int budget, int ns,
       // in [g0, g1)
       const int n = whole ? 1 : np_gu[j];
       const int base = pre_gu[j] * ug + (whole ? q * ug : q);
-      const int rg0 = g0 > base ? (g0 - base + n - 1) / n : 0;
-      const int rg1 = min(ug, g1 > base ? (g1 - base + n - 1) / n : 0);
+      int rg0, rg1;
+      if (whole) {   // n = 1: no division
+        rg0 = max(g0 - base, 0);
+        rg1 = min(ug, max(g1 - base, 0));
+      } else {
+        rg0 = g0 > base ? (g0 - base + n - 1) / n : 0;
+        rg1 = min(ug, g1 > base ? (g1 - base + n - 1) / n : 0);
+      }
       const uint32_t v = (uint32_t)t * (uint32_t)d * 2u;
       for (int rg = rg0; rg < rg1; ++rg)
         tokoff[(size_t)(base + rg * n) * FFN_GU_TOK + (pr - 16 * tf)] = v;
