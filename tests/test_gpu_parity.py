@@ -462,7 +462,8 @@ def test_qwen3_stack48_residual_carried(gu):
     takes the GPU's own x_l and h_l (teacher forcing, so no error
     accumulates between the two sides) and every plan array must match bit
     for bit; y is checked on 8 sampled tokens per layer against the fp64
-    restricted MoE plus residual."""
+    restricted MoE plus residual, and the same layer's MoE output alone (a
+    second call without the residual) against the plain 2e-2 bar."""
     from paper_2609_36222_amd import binding as bd
     name = "qwen3_stack48"
     sh = W.WORKLOADS[name]
@@ -493,9 +494,20 @@ def test_qwen3_stack48_residual_carried(gu):
         y_np = gu.to_np_f32(y)
         err = np.abs(y_np[sample].astype(np.float64) - y_ref)
         union = int((ref["counts"] > 0).sum())
+        # the MoE output alone (no residual: |y| small) at the plain bar
+        y_moe = gl.y_like(B)
+        bd.base_decode_layer(gl.desc, x, B, budget, 0, None, y_moe, ws)
+        torch.cuda.synchronize()
+        m_ref = method.moe_restricted64(
+            x_np[sample], ref["exec_ids"][sample], ref["n_exec"][sample],
+            ref["exec_gates"][sample], ex)
+        m_err = np.abs(gu.to_np_f32(y_moe)[sample].astype(np.float64) - m_ref)
         _flush(f"stack layer {layer}: |U|={union} n_sel={ref['n_sel']} "
                f"rms(h)={float(np.sqrt(np.mean(y_np.astype(np.float64) ** 2))):.3f} "
-               f"max|h|={np.abs(y_np).max():.3f} max err={err.max():.4f}")
+               f"max|h|={np.abs(y_np).max():.3f} max err={err.max():.4f} "
+               f"MoE alone max err={m_err.max():.4f}")
         assert np.all(err <= _y_tol_bf16(y_ref)), (layer, float(err.max()))
+        assert np.all(m_err <= Y_TOL[True]), (layer, float(m_err.max()))
         h_np, h = y_np, y
+        del y_moe
         del gl, ws, inp, ex, x
