@@ -354,13 +354,15 @@ base_status base_calib_accumulate(const base_layer *L, const void *z, int32_t B,
  * the pair is that kernel's execution time, with nothing added to the
  * stream between kernels.  A stage that launches no kernel (stage 5
  * always) records its pair back to back.
- * Stages: 0 scores (router logits, predictor dot products, norms), 1 tail
- * (top-K, router weights, predicted costs), 2 aggregation + selection,
+ * Stages: 0 scores (router logits, the shared experts' gate dots), 1 tail
+ * (top-K, router weights, the routed pairs' predictor dot products, norms
+ * and predicted costs), 2 aggregation + selection,
  * 3 backfill + gates, 4 compaction and the FFN's part tables, 5 (no
  * kernel: FFN gate/up gathers its own token rows), 6 FFN gate/up, 7 FFN
  * down, 8 combine.  base_route runs stages 0 and 1,
- * base_select stage 2, base_moe_forward 3 to 8 (base_predict_cost runs its
- * own kernel, untimed); base_decode_layer runs all of them except that one
+ * base_select stage 2, base_moe_forward 3 to 8 (base_predict_cost runs the
+ * tail kernel in its cost mode, untimed); base_decode_layer runs all of
+ * them except that one
  * kernel makes the selection and the backfill: stage 2 times it and stage 3
  * records its pair back to back.  The setting belongs
  * to the calling host thread; the caller keeps the events alive while it
