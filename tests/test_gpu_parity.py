@@ -221,6 +221,8 @@ EDGE = [
     (1024, 60, 4, 320, 1024, True, {}, 14),    # B at its maximum
     (256, 32, 8, 64, 1000, True, {}, 20),      # 8000 routed pairs: 8 per compaction thread
     (256, 64, 16, 64, 1024, True, {}, 40),     # B and K at their maxima: 16384 pairs
+    (16384, 8, 2, 128, 16, True, {}, 4),       # d at its maximum (512 k-steps of gate/up)
+    (256, 4, 1, 32768, 8, True, {}, 2),        # I at its maximum (the deep down instance)
 ]
 
 
