@@ -366,7 +366,8 @@ base_status base_calib_accumulate(const base_layer *L, const void *z, int32_t B,
  * kernel makes the selection and the backfill: stage 2 times it and stage 3
  * records its pair back to back.  The setting belongs
  * to the calling host thread; the caller keeps the events alive while it
- * is set, and does not set it around calls on a capturing stream.
+ * is set.  Calls on a stream that is being captured ignore it (no event is
+ * recorded into the graph).
  * Returns BASE_ERR_SHAPE if n_events != 2 * BASE_N_STAGES. */
 #define BASE_N_STAGES 9
 base_status base_set_stage_events(void *const *events, int32_t n_events);

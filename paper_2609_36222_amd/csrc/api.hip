@@ -155,10 +155,14 @@ Layout layout(const base_layer *L, int32_t B, int32_t bc) {
 thread_local void *const *g_stage_events = nullptr;
 thread_local KernelEvents g_next;
 
-// the events of stage i go to the next kernel launched
-void stage(int i) {
-  if (g_stage_events)
-    g_next = {(hipEvent_t)g_stage_events[2 * i], (hipEvent_t)g_stage_events[2 * i + 1]};
+// the events of stage i go to the next kernel launched on st; on a stream
+// that is being captured the setting is ignored, so that no event of the
+// calling thread's timing set is recorded into a graph
+void stage(int i, hipStream_t st) {
+  if (!g_stage_events) return;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return;
+  g_next = {(hipEvent_t)g_stage_events[2 * i], (hipEvent_t)g_stage_events[2 * i + 1]};
 }
 
 // a stage that launched no kernel records its pair back to back
@@ -231,12 +235,12 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
   int32_t *pair_tok = at<int32_t>(ws, o.pair_tok);
   float *pair_gate = at<float>(ws, o.pair_gate);
   int32_t *pair_of = at<int32_t>(ws, o.pair_of);
-  stage(3);
+  stage(3, st);
   if (!backfilled)
     HIP_TRY(launch_backfill(B, L->E, L->K, L->norm_topk, flags, logits, ids,
                             slot_of, n_sel, exec_ids, exec_gates, st));
   stage_end(st);
-  stage(4);
+  stage(4, st);
   const int ns = L->n_shared;
   const int n_cu = device_cus();
   FfnHdr *hdr = at<FfnHdr>(ws, o.hdr);
@@ -248,20 +252,20 @@ base_status run_forward(const base_layer *L, const void *x, int32_t B,
                          pair_tok, pair_gate, pair_of, sel_ids, bf16, L->d, L->I, tokoff,
                          hdr, units_gu, units_dn, n_cu, st));
   stage_end(st);
-  stage(5);   // no launch of its own: gate/up gathers its tokens itself
+  stage(5, st);   // no launch of its own: gate/up gathers its tokens itself
   stage_end(st);
-  stage(6);
+  stage(6, st);
   const bool packed = L->w_layout == BASE_W_PACKED;
   HIP_TRY(launch_gateup(bf16, packed, x, B, L->d, L->I, L->E, L->K, bc, ns, L->w13,
                         L->w13_shared, sel_ids, n_sel, offsets, pair_tok, hdr, units_gu, n_cu,
                         tokoff, at<void>(ws, o.H), st));
   stage_end(st);
-  stage(7);
+  stage(7, st);
   HIP_TRY(launch_down(bf16, packed, B, L->d, L->I, L->E, L->K, bc, ns, L->w2,
                       L->w2_shared, sel_ids, n_sel, offsets, hdr, units_dn, n_cu, pair_gate,
                       at<void>(ws, o.H), at<float>(ws, o.pairbuf), st));
   stage_end(st);
-  stage(8);
+  stage(8, st);
   HIP_TRY(launch_combine(bf16, B, L->d, L->K + ns, pair_of, at<float>(ws, o.pairbuf),
                          residual, y, st));
   stage_end(st);
@@ -318,11 +322,11 @@ base_status base_route(const base_layer *L, const void *x, int32_t B,
   BASE_TRY(check_ptr(topk_w, 4));
   hipStream_t st = (hipStream_t)stream;
   const bool bf16 = L->dtype == BASE_BF16;
-  stage(0);
+  stage(0, st);
   HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E, nullptr, logits,
                         nullptr, st));
   stage_end(st);
-  stage(1);
+  stage(1, st);
   HIP_TRY(launch_tail(bf16, B, L->E, L->K, L->d, L->norm_topk, logits, nullptr, nullptr,
                       nullptr, topk_ids, topk_w, nullptr, 1, BASE_SCORE_BASE, st));
   stage_end(st);
@@ -360,7 +364,7 @@ base_status base_select(const base_layer *L, int32_t B, const int32_t *topk_ids,
   BASE_TRY(check_ptr(n_sel, 4));
   BASE_TRY(check_ptr(slot_of_expert, 4));
   const int32_t bc = budget < L->E ? budget : L->E;
-  stage(2);
+  stage(2, (hipStream_t)stream);
   HIP_TRY(launch_select(B, L->K, L->E, topk_ids, cost, bc,
                         L->score_rule == BASE_SCORE_TOP1, scores, counts, sel_ids,
                         n_sel, slot_of_expert, (hipStream_t)stream));
@@ -422,18 +426,18 @@ base_status base_decode_layer(const base_layer *L, const void *x, int32_t B,
   int32_t *sel = at<int32_t>(ws, o.sel_ids);
   int32_t *nsel = at<int32_t>(ws, o.n_sel);
   int32_t *slot = at<int32_t>(ws, o.slot_of);
-  stage(0);
+  stage(0, st);
   HIP_TRY(launch_scores(bf16, x, B, L->d, L->w_router, L->b_router, L->E, shared_gate(L),
                         logits, at<float>(ws, o.gdot), st));
   stage_end(st);
   uint8_t *order = at<uint8_t>(ws, o.order);
   float *ex = at<float>(ws, o.ex), *den = at<float>(ws, o.den);
-  stage(1);   // top-K, weights, (the method's rule) the routed pairs' predictor,
+  stage(1, st);   // top-K, weights, (the method's rule) the routed pairs' predictor,
               // and each token's experts in rank order for the backfill
   HIP_TRY(launch_tail(bf16, B, L->E, L->K, L->d, L->norm_topk, logits, x, L->pred_a,
                       L->pred_b, ids, w, cost, 3, L->score_rule, st, order, ex, den));
   stage_end(st);
-  stage(2);   // selection and backfill in one launch
+  stage(2, st);   // selection and backfill in one launch
   HIP_TRY(launch_select_backfill(B, L->K, L->E, ids, cost, bc,
                                  L->score_rule == BASE_SCORE_TOP1, flags, order, ex, den,
                                  at<float>(ws, o.scores), at<int32_t>(ws, o.counts), sel, nsel,

@@ -441,6 +441,68 @@ def test_graph_replay_matches_eager(gu):
             assert got["n_sel"] == ref["n_sel"]
 
 
+def test_stage_events_ignored_under_capture(gu):
+    """Stage events set while base_decode_layer is captured: the captured
+    call records none of them (the capture succeeds and its replay equals an
+    eager call bit for bit), and an eager call made afterwards with the same
+    setting still times every kernel stage."""
+    import ctypes
+    import re
+    from paper_2609_36222_amd import binding as bd
+    maps = open("/proc/self/maps").read()
+    hip = ctypes.CDLL(sorted(set(re.findall(r"(/\S*libamdhip64\.so[.\d]*)", maps)))[0])
+    hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float),
+                                        ctypes.c_void_p, ctypes.c_void_p]
+    hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    evs = []
+    for _ in range(2 * bd.N_STAGES):
+        e = ctypes.c_void_p()
+        assert hip.hipEventCreate(ctypes.byref(e)) == 0
+        evs.append(e.value)
+    inp = named("qwen3_b64")
+    sh = inp["shape"]
+    B, budget, flags = sh.B, 32, 0
+    gl = gu.GpuLayer(inp, packed=True)
+    x = gl.x(W.decode_tokens(sh, data_seed=5))
+    ws, y = gl.workspace(B, budget), gl.y_like(B)
+    ws_e, y_e = gl.workspace(B, budget), gl.y_like(B)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        bd.base_decode_layer(gl.desc, x, B, budget, flags, None, y, ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    keep = bd.base_set_stage_events(evs)
+    try:
+        _flush("capture with stage events set")
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            bd.base_decode_layer(gl.desc, x, B, budget, flags, None, y, ws)
+        torch.cuda.synchronize()
+        _flush("eager call with stage events set")
+        bd.base_decode_layer(gl.desc, x, B, budget, flags, None, y_e, ws_e)
+        torch.cuda.synchronize()
+    finally:
+        bd.base_set_stage_events(None)
+    del keep
+    ms = ctypes.c_float()
+    # every stage with a kernel of its own in base_decode_layer (3 and 5
+    # record their pairs back to back)
+    for s in (0, 1, 2, 4, 6, 7, 8):
+        assert hip.hipEventElapsedTime(ctypes.byref(ms), evs[2 * s], evs[2 * s + 1]) == 0, s
+        assert ms.value > 0.0, s
+    y.fill_(float("nan"))
+    torch.cuda.synchronize()
+    _flush("replay of the graph captured with stage events set")
+    graph.replay()
+    torch.cuda.synchronize()
+    assert np.array_equal(y.view(torch.int16).cpu().numpy(),
+                          y_e.view(torch.int16).cpu().numpy())
+    for e in evs:
+        hip.hipEventDestroy(e)
+
+
 # ------------------------------------------------- few large experts, stack --
 @pytest.mark.timeout(600)
 def test_mixtral_full_size(gu):
