@@ -83,8 +83,9 @@ __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "mem
 // FFN_DN_DW k-steps ahead into registers.  Per k-step: wait for this wavefront's share of the
 // k-step's token loads, meet the other wavefronts (the barrier also tells
 // every wavefront that the ring slot about to be refilled has been read),
-// read the fragments from LDS one ahead of the MFMAs, then request the next
-// k-steps.  Waves without rows in a unit (a short last row group) read past
+// read the fragments from LDS (gate/up: all of the step's at once, so that
+// one LDS round trip per step is exposed, not one per tile; down: one ahead
+// of the MFMAs), then request the next k-steps.  Waves without rows in a unit (a short last row group) read past
 // their resource (zero, no memory access) and skip the MFMAs, but still take
 // their share of the token loads.
 //
@@ -241,19 +242,22 @@ __device__ __forceinline__ void gateup_unit(uint8_t *ring, uint8_t *dummy, int d
       tok_load(st + DT);
       __builtin_amdgcn_sched_barrier(0);
       const uint8_t *sb = ring + (st % (DT + 1)) * SLOT;
+      // both k-steps' fragments of the step in one batch of LDS reads
+      bf16x8 xf[2][NT];
+      if (active) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+#pragma unroll
+          for (int j = 0; j < NT; ++j)
+            xf[e][j] = *reinterpret_cast<const bf16x8 *>(sb + (e == 0 ? rb0 : rb1) + j * 2048);
+      }
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         if (active) {
-          const uint8_t *se = sb + (e == 0 ? rb0 : rb1);
-          bf16x8 xc = *reinterpret_cast<const bf16x8 *>(se);
 #pragma unroll
           for (int j = 0; j < NT; ++j) {
-            bf16x8 xn = xc;
-            if (j + 1 < NT) xn = *reinterpret_cast<const bf16x8 *>(se + (j + 1) * 2048);
-            ag[j] = mfma16(wg[p + e], xc, ag[j]);
-            au[j] = mfma16(wu[p + e], xc, au[j]);
-            __builtin_amdgcn_sched_barrier(0);
-            xc = xn;
+            ag[j] = mfma16(wg[p + e], xf[e][j], ag[j]);
+            au[j] = mfma16(wu[p + e], xf[e][j], au[j]);
           }
         }
         __builtin_amdgcn_sched_barrier(0);
