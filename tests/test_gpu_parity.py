@@ -169,8 +169,11 @@ def qwen3_b256():
     return named("qwen3_b256")
 
 
-@pytest.mark.parametrize("budget", [32, 64, 128])
+@pytest.mark.parametrize("budget", [4, 8, 32, 64, 128])
 def test_qwen3_b256_full_size(gu, qwen3_b256, budget):
+    """The batch-256 layer in full: 4 and 8 kept experts take the tables cut
+    over the dies (gate/up units of four row-pair tiles, down's instance for
+    few slots), 32 to 128 the slots dealt whole."""
     ref, _ = run_case(gu, qwen3_b256, budget)
     if budget == 128:   # covers the whole union: dense top-K
         assert np.array_equal(ref["exec_ids"], ref["topk_ids"])
